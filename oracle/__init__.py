@@ -1,0 +1,230 @@
+"""CPU oracle for the spiking-conv pipeline -- TEST INFRASTRUCTURE.
+
+ctypes wrappers over spk_oracle.c (plain C, fp64 where the paper leaves the
+precision open).  Only the tests, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package; the GPU library
+never does, and the two share no code.  All arrays are numpy, C-contiguous.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+NEVER = 255
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "spk_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle_spk.so")
+
+WINNER_DTYPE = np.dtype([("c", "<i4"), ("y", "<i4"), ("x", "<i4"), ("t", "<i4"), ("v", "<f4")])
+STDP_DTYPE = np.dtype([("a_causal", "<f4"), ("a_anticausal", "<f4"), ("lower", "<f4"),
+                       ("upper", "<f4"), ("stabilize", "<i4")])
+
+
+def build() -> str:
+    """Compile spk_oracle.c into liboracle_spk.so (plain gcc, no contraction)."""
+    tmp = _LIB + ".tmp"
+    subprocess.check_call(["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fPIC", "-shared",
+                           "-Wall", "-o", tmp, _SRC, "-lm"])
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i, d, f, i64 = ctypes.c_int, ctypes.c_double, ctypes.c_float, ctypes.c_int64
+        L.or_dog_kernel.argtypes = [i, d, d, P]
+        L.or_dog_filter.argtypes = [P, i, i, i, i, P, P, P, i, i, P]
+        L.or_latency_code.argtypes = [P, i, i64, i, f, i, P]
+        L.or_times_to_frames.argtypes = [P, i, i, i64, P]
+        L.or_frames_to_times.argtypes = [P, i, i, i64, P]
+        L.or_conv_neuron.argtypes = [P, i, i, i, i, P, i, i, i, i, i, i, i, i, P]
+        L.or_fire_neuron.argtypes = [P, i, d, P, P]
+        L.or_conv_fire.argtypes = [P, i, i, i, i, i, P, i, i, i, i, i, d, P, P, P]
+        L.or_pool.argtypes = [P, i, i, i, i, i, i, i, i, P]
+        L.or_inhibit.argtypes = [P, P, i, i, i, i]
+        L.or_kwta.argtypes = [P, P, i, i, i, i, i, i, i, i, P, P]
+        L.or_stdp_update.argtypes = [P, i, i, i, i, i, i, P, i, i, i, P, P, i, P, i, P]
+        L.or_stdp_update.restype = i
+        L.or_rstdp_select.argtypes = [P, P, i, i, P, i, P]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    assert a.flags.c_contiguous
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+# ----------------------------------------------------------------------- DoG
+
+def dog_kernel(ksize: int, sigma1: float, sigma2: float) -> np.ndarray:
+    k = np.empty((ksize, ksize), np.float32)
+    lib().or_dog_kernel(ksize, sigma1, sigma2, _p(k))
+    return k
+
+
+def dog_filter(img: np.ndarray, filters, pad: int = -1) -> np.ndarray:
+    """img uint8 B x C x H x W; filters = [(K, sigma1, sigma2), ...]."""
+    img = _c(img, np.uint8)
+    B, C, H, W = img.shape
+    ks = np.array([f[0] for f in filters], np.int32)
+    s1 = np.array([f[1] for f in filters], np.float64)
+    s2 = np.array([f[2] for f in filters], np.float64)
+    F = len(filters)
+    Ho = H if pad < 0 else H + 2 * pad - int(ks[0]) + 1
+    Wo = W if pad < 0 else W + 2 * pad - int(ks[0]) + 1
+    out = np.empty((B, C * F, Ho, Wo), np.float32)
+    lib().or_dog_filter(_p(img), B, C, H, W, _p(ks), _p(s1), _p(s2), F, pad, _p(out))
+    return out
+
+
+# -------------------------------------------------------------- latency code
+
+def latency_code(x: np.ndarray, T: int, min_value: float = 0.01, mode: int = 0) -> np.ndarray:
+    x = _c(x, np.float32)
+    B = x.shape[0]
+    n = int(np.prod(x.shape[1:]))
+    times = np.empty(x.shape, np.uint8)
+    lib().or_latency_code(_p(x), B, n, T, min_value, mode, _p(times))
+    return times
+
+
+def times_to_frames(times: np.ndarray, T: int) -> np.ndarray:
+    times = _c(times, np.uint8)
+    B = times.shape[0]
+    n = int(np.prod(times.shape[1:]))
+    frames = np.empty((B, T) + times.shape[1:], np.uint8)
+    lib().or_times_to_frames(_p(times), B, T, n, _p(frames))
+    return frames
+
+
+def frames_to_times(frames: np.ndarray) -> np.ndarray:
+    frames = _c(frames, np.uint8)
+    B, T = frames.shape[:2]
+    n = int(np.prod(frames.shape[2:]))
+    times = np.empty((B,) + frames.shape[2:], np.uint8)
+    lib().or_frames_to_times(_p(frames), B, T, n, _p(times))
+    return times
+
+
+# -------------------------------------------------------------- conv + fire
+
+def conv_neuron(in_times, w, T, stride, pad, b, o, y, x) -> np.ndarray:
+    in_times = _c(in_times, np.uint8)
+    w = _c(w, np.float32)
+    _, Ci, Hi, Wi = in_times.shape
+    _, _, Kh, Kw = w.shape
+    V = np.empty(T, np.float64)
+    lib().or_conv_neuron(_p(in_times), T, Ci, Hi, Wi, _p(w), Kh, Kw, stride, pad,
+                         int(b), int(o), int(y), int(x), _p(V))
+    return V
+
+
+def fire_neuron(V: np.ndarray, theta: float):
+    V = _c(V, np.float64)
+    t = np.empty(1, np.uint8)
+    v = np.empty(1, np.float64)
+    lib().or_fire_neuron(_p(V), V.shape[0], theta, _p(t), _p(v))
+    return int(t[0]), float(v[0])
+
+
+def conv_fire(in_times, w, T, stride, pad, theta, potentials: bool = False):
+    """Returns (t_f uint8 B x Co x Ho x Wo, V_key float32[, potentials float32 B x T x Co x Ho x Wo])."""
+    in_times = _c(in_times, np.uint8)
+    w = _c(w, np.float32)
+    B, Ci, Hi, Wi = in_times.shape
+    Co, Ci2, Kh, Kw = w.shape
+    assert Ci == Ci2
+    Ho = (Hi + 2 * pad - Kh) // stride + 1
+    Wo = (Wi + 2 * pad - Kw) // stride + 1
+    tf = np.empty((B, Co, Ho, Wo), np.uint8)
+    vk = np.empty((B, Co, Ho, Wo), np.float32)
+    V = np.empty((B, T, Co, Ho, Wo), np.float32) if potentials else None
+    lib().or_conv_fire(_p(in_times), B, T, Ci, Hi, Wi, _p(w), Co, Kh, Kw, stride, pad,
+                       float(theta), _p(tf), _p(vk), _p(V) if V is not None else None)
+    return (tf, vk, V) if potentials else (tf, vk)
+
+
+# --------------------------------------------------------------------- pool
+
+def pool(in_times, k, stride, pad=0):
+    in_times = _c(in_times, np.uint8)
+    B, C, Hi, Wi = in_times.shape
+    kh, kw = (k, k) if np.isscalar(k) else k
+    Ho = (Hi + 2 * pad - kh) // stride + 1
+    Wo = (Wi + 2 * pad - kw) // stride + 1
+    out = np.empty((B, C, Ho, Wo), np.uint8)
+    lib().or_pool(_p(in_times), B, C, Hi, Wi, kh, kw, stride, pad, _p(out))
+    return out
+
+
+# ------------------------------------------------------- inhibition / k-WTA
+
+def inhibit(times, vkey) -> np.ndarray:
+    t = np.array(times, np.uint8, copy=True, order="C")
+    vkey = _c(vkey, np.float32)
+    B, C, H, W = t.shape
+    lib().or_inhibit(_p(t), _p(vkey), B, C, H, W)
+    return t
+
+
+def kwta(times, vkey, T, k, radius, readout=False):
+    times = _c(times, np.uint8)
+    vkey = _c(vkey, np.float32)
+    B, C, H, W = times.shape
+    win = np.zeros((B, max(k, 1)), WINNER_DTYPE)[:, :k].copy()
+    nw = np.zeros(B, np.int32)
+    lib().or_kwta(_p(times), _p(vkey), B, C, H, W, T, k, radius, int(bool(readout)),
+                  _p(win), _p(nw))
+    return win, nw
+
+
+# --------------------------------------------------------------------- STDP
+
+def stdp_configs(cfgs) -> np.ndarray:
+    """cfgs: iterable of (a_causal, a_anticausal, lower, upper, stabilize)."""
+    return np.array([tuple(c) for c in cfgs], STDP_DTYPE)
+
+
+def stdp_update(w, in_times, winners, n_winners, cfgs, stride, pad, winner_cfg=None):
+    w_new = np.array(w, np.float32, copy=True, order="C")
+    in_times = _c(in_times, np.uint8)
+    winners = _c(winners, WINNER_DTYPE)
+    n_winners = _c(n_winners, np.int32)
+    cfg = _c(cfgs if isinstance(cfgs, np.ndarray) else stdp_configs(cfgs), STDP_DTYPE)
+    B, Ci, Hi, Wi = in_times.shape
+    Co, Ci2, Kh, Kw = w_new.shape
+    assert Ci == Ci2
+    k = winners.shape[1]
+    wc = None if winner_cfg is None else _c(winner_cfg, np.int32)
+    rc = lib().or_stdp_update(_p(w_new), Co, Ci, Kh, Kw, stride, pad, _p(in_times), B, Hi, Wi,
+                              _p(winners), _p(n_winners), k, _p(cfg), len(cfg),
+                              _p(wc) if wc is not None else None)
+    if rc != 0:
+        raise ValueError("STDP configurations with different bounds in one update")
+    return w_new
+
+
+def rstdp_select(winners, n_winners, labels, group) -> np.ndarray:
+    winners = _c(winners, WINNER_DTYPE)
+    n_winners = _c(n_winners, np.int32)
+    labels = _c(labels, np.int32)
+    B, k = winners.shape
+    out = np.empty((B, k), np.int32)
+    lib().or_rstdp_select(_p(winners), _p(n_winners), B, k, _p(labels), group, _p(out))
+    return out

@@ -1,0 +1,487 @@
+/*
+ * spk_oracle.c -- TEST INFRASTRUCTURE, not part of the product.
+ *
+ * A plain, slow, obviously correct CPU implementation of the spiking-conv
+ * pipeline of Spyker (arXiv 2301.13659): DoG filtering, rank-order latency
+ * coding, convolution with integrate-and-fire, spike-time max-pooling,
+ * lateral inhibition with k-winners-take-all, and STDP / R-STDP.  It exists
+ * only to check the GPU library against.  Only the tests, the smoke check and
+ * the benchmark's CPU-baseline leg may load it.  It shares no code, header,
+ * table or helper with the GPU library.
+ *
+ * Precision: double everywhere the paper leaves it open (potentials, weight
+ * updates).  Two places use float on purpose because a float value decides an
+ * integer there and both implementations must take that decision in the same
+ * precision: the DoG output (its ranks become spike times) and the linear
+ * (no-sort) coding formula.
+ *
+ * Every function is written from the definitions in the paper, in the order
+ * the paper states them; no blocking, fusion or reordering.  Readings of
+ * passages the paper leaves open are noted where they are taken.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fPIC -shared (build() in oracle/__init__.py).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define OR_NEVER 255
+
+/* ------------------------------------------------------------------------ */
+/* DoG filter bank: §II-C.1 (Difference of Gaussian filter), §II-C.4 Eq. 1. */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * One DoG kernel of odd size K: the difference of two discrete Gaussians with
+ * standard deviations s1 and s2 (§II-C.1: each filter is described by two
+ * standard deviations).  Reading: each Gaussian is sampled at integer offsets
+ * in [-R, R]^2, R = (K-1)/2, and normalised to unit sum in double; the
+ * difference is then rounded once to float.
+ */
+void or_dog_kernel(int K, double s1, double s2, float *k)
+{
+    int R = (K - 1) / 2;
+    double *g1 = (double *)malloc(sizeof(double) * K * K);
+    double *g2 = (double *)malloc(sizeof(double) * K * K);
+    double sum1 = 0.0, sum2 = 0.0;
+    for (int i = -R; i <= R; i++)
+        for (int j = -R; j <= R; j++) {
+            double r2 = (double)(i * i + j * j);
+            g1[(i + R) * K + (j + R)] = exp(-r2 / (2.0 * s1 * s1));
+            g2[(i + R) * K + (j + R)] = exp(-r2 / (2.0 * s2 * s2));
+            sum1 += g1[(i + R) * K + (j + R)];
+            sum2 += g2[(i + R) * K + (j + R)];
+        }
+    for (int n = 0; n < K * K; n++)
+        k[n] = (float)(g1[n] / sum1 - g2[n] / sum2);
+    free(g1);
+    free(g2);
+}
+
+/*
+ * Filter a uint8 image batch (B x C x H x W) with F DoG kernels applied to each
+ * channel separately (§II-C.4: C_o = C_i * K_c).  Output channel c*F + f.
+ * pad < 0 selects "same" padding per filter ((K_f - 1) / 2, so filters of
+ * different sizes give one output size); pad >= 0 applies Eq. 1 with one
+ * padding, which requires every filter to have the same K.
+ *
+ * Arithmetic, all in float with round-to-nearest and no fused multiply-add:
+ * pixel x = (float)u / 255; acc = 0; acc = acc + k[i][j] * x over the window
+ * in row-major order; pixels outside the image count as 0.
+ */
+void or_dog_filter(const uint8_t *img, int B, int C, int H, int W,
+                   const int *ksize, const double *sigma1, const double *sigma2,
+                   int F, int pad, float *out)
+{
+    int K0 = ksize[0];
+    int Ho = pad < 0 ? H : H + 2 * pad - K0 + 1;
+    int Wo = pad < 0 ? W : W + 2 * pad - K0 + 1;
+    for (int f = 0; f < F; f++) {
+        int K = ksize[f];
+        int P = pad < 0 ? (K - 1) / 2 : pad;
+        float *k = (float *)malloc(sizeof(float) * K * K);
+        or_dog_kernel(K, sigma1[f], sigma2[f], k);
+        for (int b = 0; b < B; b++)
+            for (int c = 0; c < C; c++)
+                for (int y = 0; y < Ho; y++)
+                    for (int x = 0; x < Wo; x++) {
+                        float acc = 0.0f;
+                        for (int i = 0; i < K; i++)
+                            for (int j = 0; j < K; j++) {
+                                int iy = y + i - P, ix = x + j - P;
+                                float v = 0.0f;
+                                if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+                                    v = (float)img[((size_t)(b * C + c) * H + iy) * W + ix] / 255.0f;
+                                float prod = k[i * K + j] * v;
+                                acc = acc + prod;
+                            }
+                        out[((size_t)(b * C * F + c * F + f) * Ho + y) * Wo + x] = acc;
+                    }
+        free(k);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Rank-order latency coding: §II-D.2 and §II-D.3 (Coding in Spyker).        */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    float v;
+    int64_t i;
+} or_vi;
+
+/* value descending, then flat index ascending (the reading of the sort's tie-break) */
+static int or_cmp_rank(const void *pa, const void *pb)
+{
+    const or_vi *a = (const or_vi *)pa, *b = (const or_vi *)pb;
+    if (a->v > b->v) return -1;
+    if (a->v < b->v) return 1;
+    return (a->i < b->i) ? -1 : (a->i > b->i);
+}
+
+/*
+ * For each sample, every value above min_value spikes once (values at or
+ * below it never do: the threshold applied before coding in the paper's
+ * transform).  mode 0 (rank): the eligible values of the whole sample
+ * (C*H*W jointly) are sorted by intensity, higher first, and the N spikes
+ * are spread evenly over T steps: the value of rank r fires at floor(r*T/N).
+ * mode 1 (no sort, "linear"): t = min(T-1, floor((1 - v/vmax) * T)) in float,
+ * vmax the sample maximum.  Non-spiking neurons get NEVER (255).
+ */
+void or_latency_code(const float *x, int B, int64_t n_per_sample, int T,
+                     float min_value, int mode, uint8_t *times)
+{
+    or_vi *buf = (or_vi *)malloc(sizeof(or_vi) * (size_t)(n_per_sample > 0 ? n_per_sample : 1));
+    for (int b = 0; b < B; b++) {
+        const float *xs = x + (size_t)b * n_per_sample;
+        uint8_t *ts = times + (size_t)b * n_per_sample;
+        int64_t N = 0;
+        for (int64_t i = 0; i < n_per_sample; i++) {
+            ts[i] = OR_NEVER;
+            if (xs[i] > min_value) {
+                buf[N].v = xs[i];
+                buf[N].i = i;
+                N++;
+            }
+        }
+        if (N == 0) continue;
+        if (mode == 0) {
+            qsort(buf, (size_t)N, sizeof(or_vi), or_cmp_rank);
+            for (int64_t r = 0; r < N; r++)
+                ts[buf[r].i] = (uint8_t)((r * (int64_t)T) / N);
+        } else {
+            float vmax = buf[0].v;
+            for (int64_t r = 1; r < N; r++)
+                if (buf[r].v > vmax) vmax = buf[r].v;
+            for (int64_t r = 0; r < N; r++) {
+                float q = buf[r].v / vmax;
+                float s = 1.0f - q;
+                float u = s * (float)T;
+                int t = (int)floorf(u);
+                if (t > T - 1) t = T - 1;
+                if (t < 0) t = 0;
+                ts[buf[r].i] = (uint8_t)t;
+            }
+        }
+    }
+    free(buf);
+}
+
+/* Cumulative frames (§II-D.3): a neuron that fires at t_i is on in every frame t >= t_i. */
+void or_times_to_frames(const uint8_t *times, int B, int T, int64_t n_per_sample, uint8_t *frames)
+{
+    for (int b = 0; b < B; b++)
+        for (int t = 0; t < T; t++)
+            for (int64_t i = 0; i < n_per_sample; i++)
+                frames[((size_t)b * T + t) * n_per_sample + i] =
+                    (uint8_t)(times[(size_t)b * n_per_sample + i] <= t);
+}
+
+/* Inverse of the above: the first frame in which the neuron is on, else NEVER. */
+void or_frames_to_times(const uint8_t *frames, int B, int T, int64_t n_per_sample, uint8_t *times)
+{
+    for (int b = 0; b < B; b++)
+        for (int64_t i = 0; i < n_per_sample; i++) {
+            uint8_t t_first = OR_NEVER;
+            for (int t = T - 1; t >= 0; t--)
+                if (frames[((size_t)b * T + t) * n_per_sample + i]) t_first = (uint8_t)t;
+            times[(size_t)b * n_per_sample + i] = t_first;
+        }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Convolution + integrate-and-fire: §II-E.1 (Convolution), Eq. 2.           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Potentials of one output neuron (b, o, y, x) at every step t: the 2-D
+ * convolution of frame t of the input (S_t[c, iy, ix] = [time <= t]) with
+ * kernel o, with zero padding and stride (Eq. 2), summed in double:
+ *   V_t = sum over c, ky, kx of W[o, c, ky, kx] * S_t[c, y*s + ky - p, x*s + kx - p].
+ */
+void or_conv_neuron(const uint8_t *in_times, int T, int Ci, int Hi, int Wi,
+                    const float *w, int Kh, int Kw, int stride, int pad,
+                    int b, int o, int y, int x, double *V)
+{
+    for (int t = 0; t < T; t++) {
+        double acc = 0.0;
+        for (int c = 0; c < Ci; c++)
+            for (int ky = 0; ky < Kh; ky++)
+                for (int kx = 0; kx < Kw; kx++) {
+                    int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
+                    double s = 0.0;
+                    if (iy >= 0 && iy < Hi && ix >= 0 && ix < Wi &&
+                        in_times[((size_t)(b * Ci + c) * Hi + iy) * Wi + ix] <= t)
+                        s = 1.0;
+                    acc += (double)w[((size_t)(o * Ci + c) * Kh + ky) * Kw + kx] * s;
+                }
+        V[t] = acc;
+    }
+}
+
+/*
+ * Integrate-and-fire on one neuron's potentials: it spikes where the
+ * potential is higher than the threshold (§II-E.1), once (rank-order coding:
+ * a neuron fires at most once, §II-B), so its spike time is the first t with
+ * V_t > theta, else NEVER (theta = +inf never fires).  Its key potential is V
+ * at that step, or V at the last step if it never fires (the potential that
+ * breaks ties between equal spike times in winner selection, §II-F.3).
+ */
+void or_fire_neuron(const double *V, int T, double theta, uint8_t *t_f, double *vkey)
+{
+    *t_f = OR_NEVER;
+    *vkey = V[T - 1];
+    for (int t = 0; t < T; t++)
+        if (V[t] > theta) {
+            *t_f = (uint8_t)t;
+            *vkey = V[t];
+            return;
+        }
+}
+
+/*
+ * The whole layer: every (b, o, y, x) of B x Co x Ho x Wo, with Ho and Wo from
+ * Eq. 2.  potentials (nullable) receives B x T x Co x Ho x Wo (the BTCHW
+ * order of §II-A).
+ */
+void or_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int Hi, int Wi,
+                  const float *w, int Co, int Kh, int Kw, int stride, int pad, double theta,
+                  uint8_t *out_times, float *out_vkey, float *potentials)
+{
+    int Ho = (Hi + 2 * pad - Kh) / stride + 1;
+    int Wo = (Wi + 2 * pad - Kw) / stride + 1;
+    double *V = (double *)malloc(sizeof(double) * T);
+    for (int b = 0; b < B; b++)
+        for (int o = 0; o < Co; o++)
+            for (int y = 0; y < Ho; y++)
+                for (int x = 0; x < Wo; x++) {
+                    or_conv_neuron(in_times, T, Ci, Hi, Wi, w, Kh, Kw, stride, pad, b, o, y, x, V);
+                    uint8_t tf;
+                    double vk;
+                    or_fire_neuron(V, T, theta, &tf, &vk);
+                    size_t n = ((size_t)(b * Co + o) * Ho + y) * Wo + x;
+                    out_times[n] = tf;
+                    out_vkey[n] = (float)vk;
+                    if (potentials)
+                        for (int t = 0; t < T; t++)
+                            potentials[(((size_t)b * T + t) * Co + o) * Ho * Wo + (size_t)y * Wo + x] =
+                                (float)V[t];
+                }
+    free(V);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Pooling: §II-E.3, Eq. 3.                                                  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Max-pooling under rank-order coding keeps the neuron of the window that
+ * fires earliest: out = min over the window of the input times.  Window
+ * positions in the padding count as never firing.
+ */
+void or_pool(const uint8_t *in_times, int B, int C, int Hi, int Wi, int Kh, int Kw,
+             int stride, int pad, uint8_t *out_times)
+{
+    int Ho = (Hi + 2 * pad - Kh) / stride + 1;
+    int Wo = (Wi + 2 * pad - Kw) / stride + 1;
+    for (int b = 0; b < B; b++)
+        for (int c = 0; c < C; c++)
+            for (int y = 0; y < Ho; y++)
+                for (int x = 0; x < Wo; x++) {
+                    uint8_t m = OR_NEVER;
+                    for (int ky = 0; ky < Kh; ky++)
+                        for (int kx = 0; kx < Kw; kx++) {
+                            int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
+                            if (iy >= 0 && iy < Hi && ix >= 0 && ix < Wi) {
+                                uint8_t v = in_times[((size_t)(b * C + c) * Hi + iy) * Wi + ix];
+                                if (v < m) m = v;
+                            }
+                        }
+                    out_times[((size_t)(b * C + c) * Ho + y) * Wo + x] = m;
+                }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Lateral inhibition and k-WTA: §II-F.3.                                    */
+/* ------------------------------------------------------------------------ */
+
+/* (t, -v, index) order: earlier spike first, then higher potential, then lower index */
+static int or_better(int ta, float va, int64_t ia, int tb, float vb, int64_t ib)
+{
+    if (ta != tb) return ta < tb;
+    if (va != vb) return va > vb;
+    return ia < ib;
+}
+
+/*
+ * Pointwise lateral inhibition: at each location (b, y, x) only the neuron of
+ * the map that fires first survives (ties: higher potential, then lower
+ * channel); every other fired neuron there is set to NEVER.  In place.
+ */
+void or_inhibit(uint8_t *times, const float *vkey, int B, int C, int H, int W)
+{
+    for (int b = 0; b < B; b++)
+        for (int y = 0; y < H; y++)
+            for (int x = 0; x < W; x++) {
+                int best = -1;
+                for (int c = 0; c < C; c++) {
+                    size_t n = ((size_t)(b * C + c) * H + y) * W + x;
+                    if (times[n] == OR_NEVER) continue;
+                    if (best < 0) { best = c; continue; }
+                    size_t m = ((size_t)(b * C + best) * H + y) * W + x;
+                    if (or_better(times[n], vkey[n], c, times[m], vkey[m], best)) best = c;
+                }
+                for (int c = 0; c < C; c++) {
+                    size_t n = ((size_t)(b * C + c) * H + y) * W + x;
+                    if (c != best) times[n] = OR_NEVER;
+                }
+            }
+}
+
+typedef struct {
+    int32_t c, y, x, t;
+    float v;
+} or_winner;
+
+/*
+ * k-winners-take-all for convolution (the paper's convwta(array, radius,
+ * count)).  Per sample, up to k rounds: the best remaining candidate wins
+ * (earliest spike, then higher potential, then lower flat index (c*H+y)*W+x);
+ * its whole map and every neuron of any map within Chebyshev distance
+ * `radius` of its location stop being candidates.  Candidates are the fired
+ * neurons; in readout mode (no threshold) every neuron is a candidate and
+ * the rank is potential only (higher first, then lower index) with t = T-1.
+ * Unused slots get c = -1.  Returns nothing; n_winners[b] is the count.
+ */
+void or_kwta(const uint8_t *times, const float *vkey, int B, int C, int H, int W, int T,
+             int k, int radius, int readout, or_winner *winners, int32_t *n_winners)
+{
+    size_t per = (size_t)C * H * W;
+    uint8_t *alive = (uint8_t *)malloc(per ? per : 1);
+    for (int b = 0; b < B; b++) {
+        const uint8_t *tb = times + b * per;
+        const float *vb = vkey + b * per;
+        for (size_t n = 0; n < per; n++) alive[n] = readout ? 1 : (tb[n] != OR_NEVER);
+        int count = 0;
+        for (int round = 0; round < k; round++) {
+            int64_t best = -1;
+            for (size_t n = 0; n < per; n++) {
+                if (!alive[n]) continue;
+                if (best < 0) { best = (int64_t)n; continue; }
+                int tn = readout ? 0 : tb[n], tm = readout ? 0 : tb[best];
+                if (or_better(tn, vb[n], (int64_t)n, tm, vb[best], best)) best = (int64_t)n;
+            }
+            if (best < 0) break;
+            int c = (int)(best / ((int64_t)H * W));
+            int y = (int)((best / W) % H);
+            int x = (int)(best % W);
+            or_winner *wn = &winners[(size_t)b * k + count];
+            wn->c = c;
+            wn->y = y;
+            wn->x = x;
+            wn->t = readout ? T - 1 : tb[best];
+            wn->v = vb[best];
+            count++;
+            for (int cc = 0; cc < C; cc++)
+                for (int yy = 0; yy < H; yy++)
+                    for (int xx = 0; xx < W; xx++) {
+                        int near = abs(yy - y) <= radius && abs(xx - x) <= radius;
+                        if (cc == c || near) alive[((size_t)cc * H + yy) * W + xx] = 0;
+                    }
+        }
+        n_winners[b] = count;
+        for (int s = count; s < k; s++) {
+            or_winner *wn = &winners[(size_t)b * k + s];
+            wn->c = -1;
+            wn->y = wn->x = wn->t = -1;
+            wn->v = 0.0f;
+        }
+    }
+    free(alive);
+}
+
+/* ------------------------------------------------------------------------ */
+/* STDP and R-STDP: §II-F.1 Eq. 4-6, §II-F.2 Eq. 7.                          */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    float a_causal, a_anticausal, lower, upper;
+    int32_t stabilize;
+} or_stdp_cfg;
+
+/*
+ * Update the weights of the winners' kernels.  For winner (b, o=c, y, x, t_post)
+ * with configuration q, each synapse (ci, ky, kx) of kernel o sees the input
+ * neuron at (ci, y*s+ky-p, x*s+kx-p) of sample b with spike time t_pre (NEVER
+ * in the padding).  A pre spike at or before the post spike potentiates
+ * (Eq. 4 first case, taken for the t_pre == t_post overlap), a later or
+ * missing one depresses.  With the stabiliser, dW = A * (W - L) * (U - W)
+ * (Eq. 4), without it dW = A (Eq. 5), from the weight before the update.
+ * The mini-batch rule does not differ from the single-sample rule
+ * (§II-F.1): every winner's dW is taken from the pre-update weights and the
+ * changes are summed; then W = clamp(W + sum, L, U) (Eq. 6, read as clipping
+ * the updated weight) for every weight that received a change.  All in double.
+ * winner_cfg (nullable: all 0) maps winner b*k+slot to a configuration.
+ * R-STDP (Eq. 7) is this same update with a reward and a punish configuration.
+ */
+int or_stdp_update(float *w, int Co, int Ci, int Kh, int Kw, int stride, int pad,
+                   const uint8_t *in_times, int B, int Hi, int Wi,
+                   const or_winner *winners, const int32_t *n_winners, int k,
+                   const or_stdp_cfg *cfg, int n_cfg, const int32_t *winner_cfg)
+{
+    /* One clamp range per call: configurations with different bounds would
+     * leave the clamp of a weight touched by both undefined. */
+    for (int q = 1; q < n_cfg; q++)
+        if (cfg[q].lower != cfg[0].lower || cfg[q].upper != cfg[0].upper) return -1;
+    size_t nw = (size_t)Co * Ci * Kh * Kw;
+    double *D = (double *)calloc(nw ? nw : 1, sizeof(double));
+    uint8_t *touched = (uint8_t *)calloc(nw ? nw : 1, 1);
+    double L = cfg[0].lower, U = cfg[0].upper;
+    for (int b = 0; b < B; b++)
+        for (int s = 0; s < n_winners[b]; s++) {
+            const or_winner *wn = &winners[(size_t)b * k + s];
+            const or_stdp_cfg *q = &cfg[winner_cfg ? winner_cfg[(size_t)b * k + s] : 0];
+            int o = wn->c;
+            for (int c = 0; c < Ci; c++)
+                for (int ky = 0; ky < Kh; ky++)
+                    for (int kx = 0; kx < Kw; kx++) {
+                        int iy = wn->y * stride + ky - pad, ix = wn->x * stride + kx - pad;
+                        int t_pre = OR_NEVER;
+                        if (iy >= 0 && iy < Hi && ix >= 0 && ix < Wi)
+                            t_pre = in_times[((size_t)(b * Ci + c) * Hi + iy) * Wi + ix];
+                        double A = (t_pre <= wn->t) ? (double)q->a_causal : (double)q->a_anticausal;
+                        size_t n = ((size_t)(o * Ci + c) * Kh + ky) * Kw + kx;
+                        double W0 = (double)w[n];
+                        double dW = q->stabilize ? A * (W0 - L) * (U - W0) : A;
+                        D[n] += dW;
+                        touched[n] = 1;
+                    }
+        }
+    for (size_t n = 0; n < nw; n++) {
+        if (!touched[n]) continue;
+        double v = (double)w[n] + D[n];
+        if (v > U) v = U;
+        if (v < L) v = L;
+        w[n] = (float)v;
+    }
+    free(D);
+    free(touched);
+    return 0;
+}
+
+/*
+ * R-STDP configuration choice (§II-F.2): a winner is rewarded (configuration
+ * 0) when the class of its map, c / group, equals the sample's label, and
+ * punished (configuration 1) otherwise.
+ */
+void or_rstdp_select(const or_winner *winners, const int32_t *n_winners, int B, int k,
+                     const int32_t *labels, int group, int32_t *winner_cfg)
+{
+    for (int b = 0; b < B; b++)
+        for (int s = 0; s < k; s++) {
+            const or_winner *wn = &winners[(size_t)b * k + s];
+            winner_cfg[(size_t)b * k + s] =
+                (s < n_winners[b] && wn->c / group == labels[b]) ? 0 : 1;
+        }
+}
