@@ -1,0 +1,183 @@
+#!/usr/bin/env python3
+"""Throughput of the spiking-conv hot path on one MI355X.
+
+A step is one pass of the whole path over one batch of seeded synthetic input
+(DoG filtering, rank-order coding, and per conv layer conv + fire, inhibition
++ k-WTA + STDP for learning layers, pooling between layers).  Default
+workload: the three-layer network at batch 64, T = 15.
+
+Prints ONE JSON line: whole-job samples/s, per-layer samples/s and synaptic
+events/s, the roofline position of the dominant kernel (timed live with HIP
+events on the stream it runs on) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X datasheet peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_F16_MFMA_TFLOPS = 2500.0
+PEAK_F32_VALU_TFLOPS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2, help="1..5 (default: three-layer net)")
+    ap.add_argument("--density", type=int, default=1, help="spike-density index of workload 5")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU budget of the oracle baseline (0 disables it)")
+    ap.add_argument("--no-breakdown", action="store_true")
+    return ap.parse_args()
+
+
+def fanout_events(t_in, spec, torch):
+    """Synaptic events of a conv layer: every input spike counted once times its fan-out
+    (number of output neurons whose window holds it)."""
+    import torch.nn.functional as F
+    B, C, H, W = t_in.shape
+    Ho = (H + 2 * spec.pad - spec.k) // spec.stride + 1
+    Wo = (W + 2 * spec.pad - spec.k) // spec.stride + 1
+    cover = F.conv_transpose2d(torch.ones((1, 1, Ho, Wo), device=t_in.device),
+                               torch.ones((1, 1, spec.k, spec.k), device=t_in.device),
+                               stride=spec.stride, padding=spec.pad)
+    cover = F.pad(cover, (0, W - cover.shape[-1], 0, H - cover.shape[-2]))[0, 0]
+    fired = (t_in != 255).to(torch.float64).sum(dim=(0, 1))
+    return float((fired * cover.to(torch.float64)).sum().item()) * spec.co
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle (plain C, one thread) on whole samples of the same workload until the
+    budget is spent; samples/s."""
+    import numpy as np
+
+    import oracle
+    from paper_2301_13659_amd import workloads as wls
+
+    imgs = wls.make_images(wl) if wl.image_hw is not None else None
+    spikes = wls.make_spike_times(wl, 1) if wl.image_hw is None else None
+    ws = [wls.make_weights(wl, i + 1) for i in range(len(wl.convs))]
+    labels = wls.make_labels(wl)
+    cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
+    filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
+    done = 0
+    t0 = time.perf_counter()
+    while done < wl.batch and time.perf_counter() - t0 < budget_s:
+        b = done
+        if imgs is not None:
+            x = oracle.dog_filter(imgs[b:b + 1], filters)
+            t = oracle.latency_code(x, wl.T, wl.min_value)
+        else:
+            t = spikes[b:b + 1]
+        li = 0
+        for kind, s in wl.stages:
+            if kind == "pool":
+                t = oracle.pool(t, s.k, s.stride, s.pad)
+                continue
+            tf, vk = oracle.conv_fire(t, ws[li], wl.T, s.stride, s.pad, s.theta)
+            if s.stdp or s.readout:
+                cand = tf if s.readout else oracle.inhibit(tf, vk)
+                win, n = oracle.kwta(cand, vk, wl.T, s.k_win, s.radius, s.readout)
+                if s.stdp:
+                    wc = (oracle.rstdp_select(win, n, labels[b:b + 1], wl.rstdp_group)
+                          if wl.rstdp_group else None)
+                    ws[li] = oracle.stdp_update(ws[li], t, win, n, cfgs, s.stride, s.pad, winner_cfg=wc)
+            t = tf
+            li += 1
+        done += 1
+    el = time.perf_counter() - t0
+    return {"value": done / el, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of the {wl.batch} samples of one batch, whole step, "
+                      f"{el:.1f} s single-threaded C"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the path shards over the batch, see the design notes", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2301_13659_amd import spk
+    from paper_2301_13659_amd import workloads as wls
+    from paper_2301_13659_amd.pipeline import Pipeline, conv_flops
+
+    dev = torch.device("cuda:0")
+    wl = wls.get(args.workload)
+    pipe = Pipeline(wl, dev, density_index=args.density)
+    flops = conv_flops(wl)
+    dom = max(range(len(flops)), key=lambda i: flops[i])
+    dom_name = f"conv{dom + 1}"
+
+    for _ in range(args.warmup):
+        pipe.step()
+    torch.cuda.synchronize()
+
+    timers = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        pipe.step(timers=timers, only={dom_name})
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom_ms = sum(a.elapsed_time(b) for a, b in timers[dom_name]) / len(timers[dom_name])
+
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = wl.batch * args.steps / elapsed
+
+    # per-stage breakdown (separate, untimed pass) and per-layer events
+    per_layer = []
+    stage_ms = {}
+    if not args.no_breakdown:
+        br = {}
+        kept = None
+        for i in range(max(3, min(args.steps, 10))):
+            o = pipe.step(timers=br, keep=(i == 0))
+            kept = kept or o
+        torch.cuda.synchronize()
+        stage_ms = {k: sum(a.elapsed_time(b) for a, b in v) / len(v) for k, v in br.items()}
+        for li, spec in enumerate(wl.convs):
+            n = li + 1
+            ev = fanout_events(kept.layer_in[li], spec, torch)
+            names = [f"conv{n}", f"wta{n}", f"select{n}", f"stdp{n}"]
+            lay_ms = sum(stage_ms.get(k, 0.0) for k in names)
+            conv_ms = stage_ms[f"conv{n}"]
+            per_layer.append({
+                "layer": f"conv{n}", "ms": round(lay_ms, 4), "conv_ms": round(conv_ms, 4),
+                "samples_per_s": wl.batch / (lay_ms * 1e-3),
+                "events": ev, "events_per_s": ev / (conv_ms * 1e-3),
+                "dense_tflops": flops[li] / (conv_ms * 1e-3) / 1e12})
+
+    achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
+    roofline = {"kernel": f"spk_conv_fire ({dom_name})", "bound": "alu", "achieved": achieved,
+                "peak": PEAK_F32_VALU_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_F32_VALU_TFLOPS,
+                "traffic": None, "kernel_ms": dom_ms,
+                "work": "dense-interface flop 2*B*T*Ho*Wo*Co*Ci*Kh*Kw per launch"}
+    line = {
+        "metric": "samples/sec and synaptic events/sec per layer; % fp16 MFMA / HBM peak",
+        "value": value, "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.description, "batch": wl.batch,
+                   "T": wl.T, "parallelism": "single GPU"},
+        "per_layer": per_layer, "stage_ms": stage_ms, "roofline": roofline,
+        "library": spk.version(),
+    }
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

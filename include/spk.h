@@ -1,0 +1,262 @@
+/*
+ * spk.h -- C ABI of libspk, the MI355X (gfx950) hot path of convolutional
+ * spiking networks as described in Spyker (Shirsavar & Dehaqani, arXiv
+ * 2301.13659): DoG filtering, rank-order latency coding, spiking convolution
+ * with integrate-and-fire, spike-time pooling, lateral inhibition with
+ * k-winners-take-all, and STDP / R-STDP.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Array arguments are DEVICE pointers owned by the caller, contiguous,
+ *    in NCHW order (B x C x H x W); frame and potential arrays are BTCHW
+ *    (batch, time, channel, height, width), the order of the paper's §II-A.
+ *    Small descriptor arrays (spk_dog_desc, spk_stdp_config) are HOST pointers.
+ *  - Spike activity is held as a uint8 first-spike-time map: entry t in
+ *    [0, T) means the neuron fires at step t and, frames being cumulative
+ *    (§II-D.3), stays on in every later frame; SPK_NEVER (255) means it never
+ *    fires.  Hence T <= SPK_MAX_T (254).
+ *  - The library never allocates device memory and never synchronises.  Calls
+ *    that need scratch take a caller workspace (ws, ws_bytes) sized by the
+ *    matching *_workspace_size query; ws may be NULL when that size is 0.
+ *  - Every call enqueues its kernels on `stream` (a hipStream_t; NULL is the
+ *    null stream) and returns before they run.  Faults of the kernels surface
+ *    at the caller's next synchronisation.
+ *  - All arguments are validated on the host before anything is launched.  A
+ *    call that returns anything but SPK_OK or SPK_E_HIP has launched nothing
+ *    and touched no memory; spk_last_error() (per thread) then describes why.
+ *    SPK_E_HIP means a launch failed after earlier kernels of the call may
+ *    already have been enqueued.
+ *  - Outputs may not alias inputs unless a call says so.
+ */
+#ifndef SPK_H
+#define SPK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPK_NEVER 255
+#define SPK_MAX_T 254
+
+typedef enum {
+    SPK_OK = 0,
+    SPK_E_ARG = 1,          /* NULL pointer, non-positive size, bad enum   */
+    SPK_E_SHAPE = 2,        /* derived size <= 0, T out of range, size limit */
+    SPK_E_UNSUPPORTED = 3,  /* dtype or parameter combination not supported */
+    SPK_E_WORKSPACE = 4,    /* workspace missing or smaller than required  */
+    SPK_E_HIP = 5           /* a HIP launch reported an error              */
+} spk_status;
+
+typedef enum { SPK_F32 = 0, SPK_F16 = 1 } spk_dtype;
+typedef enum { SPK_CODE_RANK = 0, SPK_CODE_LINEAR = 1 } spk_code_mode;
+
+typedef void *spk_stream; /* hipStream_t */
+
+/* One DoG filter: odd kernel size and the two standard deviations (§II-C.1). */
+typedef struct {
+    int32_t ksize;
+    double sigma1, sigma2;
+} spk_dog_desc;
+
+/* One k-WTA winner (§II-F.3): map c, location (y, x), spike time t, key potential v. */
+typedef struct {
+    int32_t c, y, x, t;
+    float v;
+} spk_winner;
+
+/* One STDP configuration, the paper's STDPConfig(positive, negative, stabilize,
+ * lower, upper) of §II-F.1: a_causal applies when the pre spike comes at or
+ * before the post spike, a_anticausal otherwise. */
+typedef struct {
+    float a_causal, a_anticausal, lower, upper;
+    int32_t stabilize;
+} spk_stdp_config;
+
+/* Library version string ("spk <major>.<minor> gfx950"). */
+const char *spk_version(void);
+
+/* Description of the last failure of a call made by this thread ("" if none). */
+const char *spk_last_error(void);
+
+/* Output extent of a convolution or pooling window along one axis, Eq. 2 / Eq. 3
+ * (§II-E.1, §II-E.3): floor((in + 2*pad - k) / stride) + 1, or -1 when the
+ * arguments give no output (k < 1, stride < 1, pad < 0 or in + 2*pad < k). */
+int spk_out_extent(int in, int k, int stride, int pad);
+
+/*
+ * spk_dog_filter -- DoG feature enhancement, §II-C.1 with the shape rule of
+ * §II-C.4 (Eq. 1): every one of the F filters is applied to every input
+ * channel separately, giving B x (C*F) x Ho x Wo, output channel c*F + f.
+ *   img      uint8 B x C x H x W (device); pixel value u is taken as u / 255.
+ *   filters  F descriptors (host); each kernel is the difference of two
+ *            unit-sum discrete Gaussians sampled on [-R, R]^2, R = (K-1)/2,
+ *            computed in double on the host and rounded to float.
+ *   pad      -1: "same" padding per filter, Ho = H, Wo = W (filters may have
+ *            different sizes); >= 0: Eq. 1, Ho = H + 2*pad - K + 1, all
+ *            filters must then share K.
+ *   out      float B x (C*F) x Ho x Wo (device).
+ * Each output is accumulated in float, window row-major, without fused
+ * multiply-add, so results are reproducible bit for bit.
+ * Errors: SPK_E_ARG (NULL, sizes <= 0, even or < 1 ksize, sigma <= 0),
+ * SPK_E_SHAPE (ksize > 21, F > 8, or output size <= 0), SPK_E_UNSUPPORTED
+ * (pad >= 0 with mixed kernel sizes).
+ */
+spk_status spk_dog_filter(const uint8_t *img, int B, int C, int H, int W,
+                          const spk_dog_desc *filters, int F, int pad,
+                          float *out, spk_stream stream);
+
+/*
+ * spk_latency_code -- rank-order (latency) coding, §II-D.2 and §II-D.3.
+ * Per sample, the values above min_value (the threshold applied before
+ * coding) each fire once; the rest never fire.
+ *   SPK_CODE_RANK   the eligible values of the whole sample (all C*H*W
+ *                   jointly) are sorted, higher first, ties to the lower flat
+ *                   index; the N spikes are spread evenly over T steps: rank
+ *                   r fires at floor(r*T/N).
+ *   SPK_CODE_LINEAR the sort disabled: t = min(T-1, floor((1 - v/vmax)*T)) in
+ *                   float, vmax the largest value of the sample.
+ *   x       float B x C x H x W (device).
+ *   times   uint8 B x C x H x W (device) first-spike times.
+ *   frames  nullable uint8 B x T x C x H x W (device) cumulative frames.
+ *   ws      workspace of spk_latency_code_workspace_size(B, C, H, W) bytes.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (T < 1 or > SPK_MAX_T, C*H*W >= 2^31),
+ * SPK_E_WORKSPACE.
+ */
+size_t spk_latency_code_workspace_size(int B, int C, int H, int W);
+spk_status spk_latency_code(const float *x, int B, int C, int H, int W, int T,
+                            float min_value, int mode, uint8_t *times, uint8_t *frames,
+                            void *ws, size_t ws_bytes, spk_stream stream);
+
+/*
+ * spk_conv_fire -- spiking convolution with integrate-and-fire, §II-E.1
+ * (Eq. 2 for the output size).  For every output neuron (b, o, y, x) and
+ * step t, V_t = sum over c, ky, kx of W[o, c, ky, kx] * S_t[b, c, y*stride +
+ * ky - pad, x*stride + kx - pad], where S_t = [in_times <= t] is frame t of
+ * the cumulative input and padding is silent.  The neuron fires once, at the
+ * first t with V_t > theta (§II-E.1; at most once under rank-order coding,
+ * §II-B); theta = +inf never fires (readout).
+ *   in_times   uint8 B x Ci x Hi x Wi (device).
+ *   w          Co x Ci x Kh x Kw (device): float (SPK_F32 master weights) or
+ *              IEEE half bits (SPK_F16 operand).
+ *   out_times  uint8 B x Co x Ho x Wo (device): spike time, or SPK_NEVER.
+ *   out_vkey   float B x Co x Ho x Wo (device): V at the spike time, or V at
+ *              step T-1 for neurons that never fire (the potential that
+ *              orders equal spike times in winner selection, §II-F.3).
+ *   potentials nullable float B x T x Co x Ho x Wo (device): every V_t
+ *              (the paper's dense interface, §II-B).
+ *   ws         workspace of spk_conv_fire_workspace_size(...) bytes.
+ * Potentials are accumulated in float.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (T out of range, Ho or Wo <= 0),
+ * SPK_E_UNSUPPORTED (w_dtype), SPK_E_WORKSPACE.
+ */
+size_t spk_conv_fire_workspace_size(int B, int T, int Ci, int Hi, int Wi, int Co,
+                                    int Kh, int Kw, int stride, int pad);
+spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int Hi, int Wi,
+                         const void *w, spk_dtype w_dtype, int Co, int Kh, int Kw,
+                         int stride, int pad, float theta,
+                         uint8_t *out_times, float *out_vkey, float *potentials,
+                         void *ws, size_t ws_bytes, spk_stream stream);
+
+/*
+ * spk_pool -- max-pooling of spikes under rank-order coding, §II-E.3 (Eq. 3
+ * for the size): each output keeps the earliest spike of its Kh x Kw window,
+ * i.e. the minimum input time; window cells in the padding never fire.
+ *   in_times  uint8 B x C x Hi x Wi (device); out_times uint8 B x C x Ho x Wo.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (Ho or Wo <= 0).
+ */
+spk_status spk_pool(const uint8_t *in_times, int B, int C, int Hi, int Wi,
+                    int Kh, int Kw, int stride, int pad, uint8_t *out_times,
+                    spk_stream stream);
+
+/*
+ * spk_inhibit_winners -- lateral inhibition and convolutional k-WTA, §II-F.3.
+ *   pointwise  1: first keep, at every location (b, y, x), only the map that
+ *              fires first (equal times: higher vkey, then lower channel);
+ *              the other neurons there count as never firing.
+ *   k, radius  per sample, up to k rounds: the best remaining candidate wins
+ *              (earliest time, then higher vkey, then lower flat index
+ *              (c*H + y)*W + x); its map and every neuron of every map within
+ *              Chebyshev distance radius of (y, x) stop being candidates.
+ *   readout    1 (a layer with an infinite threshold): every neuron is a
+ *              candidate, ranked by vkey (higher first, then lower index),
+ *              and winners report t = T-1; pointwise must then be 0.
+ *   times, vkey  uint8 / float B x C x H x W (device), from spk_conv_fire.
+ *   inhibited  nullable uint8 B x C x H x W (device): times after pointwise
+ *              inhibition (may alias times for the in-place form).
+ *   winners    spk_winner B x k (device); slots past n_winners[b] get c = -1.
+ *   n_winners  int32 B (device).
+ *   ws         workspace of spk_inhibit_winners_workspace_size(B, C, H, W).
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (H*W > 2^20, k > 4096), SPK_E_UNSUPPORTED
+ * (readout with pointwise), SPK_E_WORKSPACE.
+ */
+size_t spk_inhibit_winners_workspace_size(int B, int C, int H, int W);
+spk_status spk_inhibit_winners(const uint8_t *times, const float *vkey,
+                               int B, int C, int H, int W, int T,
+                               int pointwise, int k, int radius, int readout,
+                               uint8_t *inhibited, spk_winner *winners, int32_t *n_winners,
+                               void *ws, size_t ws_bytes, spk_stream stream);
+
+/*
+ * spk_stdp_update -- STDP (§II-F.1, Eq. 4-6) and R-STDP (§II-F.2, Eq. 7) on
+ * the winners' receptive fields.  For winner slot s of sample b with map o,
+ * location (y, x), time t_post and configuration q = winner_cfg[b*k + s],
+ * every synapse (c, ky, kx) of kernel o sees the input neuron (b, c,
+ * y*stride + ky - pad, x*stride + kx - pad) with time t_pre (SPK_NEVER in the
+ * padding): t_pre <= t_post takes a_causal, otherwise a_anticausal.  With the
+ * stabiliser dW = (a * (W - L)) * (U - W), without it dW = a, always from the
+ * weights before the call.  The batch rule equals the single-sample rule
+ * (§II-F.1): the dW of all winners are summed in float in the order (b
+ * ascending, slot ascending), then W = min(U, max(L, W + sum)) for every
+ * weight that received a change.
+ *   w          float Co x Ci x Kh x Kw master weights (device, in/out).
+ *   w_f16      nullable IEEE-half Co x Ci x Kh x Kw (device): refreshed with
+ *              the round-to-nearest-even half of every updated weight.
+ *   in_times   uint8 B x Ci x Hi x Wi (device): the layer's input.
+ *   winners, n_winners  from spk_inhibit_winners (device), k slots per sample.
+ *   cfg        n_cfg configurations (host); all must share lower and upper.
+ *   winner_cfg nullable int32 B x k (device); NULL = configuration 0.
+ *   ws         workspace of spk_stdp_update_workspace_size(...) bytes.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (Ci*Kh*Kw > 16384, n_cfg > 16),
+ * SPK_E_UNSUPPORTED (configurations with different bounds), SPK_E_WORKSPACE.
+ */
+size_t spk_stdp_update_workspace_size(int Co, int Ci, int Kh, int Kw, int B, int k);
+spk_status spk_stdp_update(float *w, uint16_t *w_f16, int Co, int Ci, int Kh, int Kw,
+                           int stride, int pad, const uint8_t *in_times, int B, int Hi, int Wi,
+                           const spk_winner *winners, const int32_t *n_winners, int k,
+                           const spk_stdp_config *cfg, int n_cfg, const int32_t *winner_cfg,
+                           void *ws, size_t ws_bytes, spk_stream stream);
+
+/*
+ * spk_rstdp_select -- reward / punish choice of R-STDP, §II-F.2: winner slot s
+ * of sample b gets configuration 0 (reward) when its map's class c / group
+ * equals labels[b], else 1 (punish); empty slots get 1 and are never used.
+ *   winners B x k, n_winners B, labels int32 B, winner_cfg int32 B x k (device).
+ * Errors: SPK_E_ARG.
+ */
+spk_status spk_rstdp_select(const spk_winner *winners, const int32_t *n_winners, int B, int k,
+                            const int32_t *labels, int group, int32_t *winner_cfg,
+                            spk_stream stream);
+
+/*
+ * Cumulative frames <-> first-spike times (§II-D.3, §II-B): frames is uint8
+ * B x T x n (1 = on), times uint8 B x n; a neuron's time is its first on
+ * frame.  spk_frames_to_times expects cumulative frames; a frame sequence
+ * that switches a neuron off again is reduced to its first on frame.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (T out of range).
+ */
+spk_status spk_frames_to_times(const uint8_t *frames, int B, int T, int64_t n,
+                               uint8_t *times, spk_stream stream);
+spk_status spk_times_to_frames(const uint8_t *times, int B, int T, int64_t n,
+                               uint8_t *frames, spk_stream stream);
+
+/* float -> IEEE half bits, round to nearest even (the SPK_F16 conv operand). */
+spk_status spk_cast_f16(const float *x, uint16_t *y, int64_t n, spk_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPK_H */

@@ -1,0 +1,318 @@
+// spk_latency_code: rank-order latency coding (Spyker §II-D.2, §II-D.3).
+//
+// Ranking uses one 64-bit key per value: the high word maps the float to an
+// unsigned integer whose ascending order is descending value order, the low
+// word is the flat index inside the sample.  Keys are unique, so any sort of
+// them is the stable "value descending, index ascending" order, and the rank
+// of an eligible value is its position among the sorted keys.  Ineligible
+// values (<= min_value, NaN) get the all-ones key, sort to the end and are
+// written as never firing up front.
+//
+//  - Samples of up to kSmall values are ranked by one workgroup each, with a
+//    bitonic sort of the keys in LDS.
+//  - Larger samples: workgroups sort kSmall-key chunks in LDS, then merge
+//    passes double the sorted runs (merge-path split per thread) until each
+//    sample is one run; the ping-pong buffers live in the caller workspace.
+#include <cstring>
+
+#include "spk_internal.h"
+
+namespace {
+
+constexpr int kSmall = 8192;    // keys per LDS sort (64 KB)
+constexpr int kThreads = 1024;
+constexpr int kMergePerThread = 8;
+constexpr uint64_t kDead = ~0ull;
+
+__device__ __forceinline__ uint32_t order_desc(float v)
+{
+    if (v == 0.0f) v = 0.0f;  // -0 and +0 are one value
+    uint32_t u = __float_as_uint(v);
+    uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);  // ascending float order
+    return ~asc;
+}
+
+__device__ __forceinline__ uint64_t make_key(float v, float min_value, uint32_t i)
+{
+    return (v > min_value) ? (((uint64_t)order_desc(v) << 32) | i) : kDead;
+}
+
+// Ascending bitonic sort of n (a power of two) keys in LDS by the whole block.
+__device__ void bitonic_sort_lds(uint64_t *s, int n)
+{
+    for (int k = 2; k <= n; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < n; i += blockDim.x) {
+                int ixj = i ^ j;
+                if (ixj > i) {
+                    uint64_t a = s[i], b = s[ixj];
+                    bool up = (i & k) == 0;
+                    if ((a > b) == up) {
+                        s[i] = b;
+                        s[ixj] = a;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+}
+
+__device__ __forceinline__ int block_sum(int v, int *red)
+{
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, 64);
+    int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    if (lane == 0) red[wid] = v;
+    __syncthreads();
+    int tot = 0;
+    if (threadIdx.x == 0) {
+        for (int w = 0; w < (int)(blockDim.x >> 6); w++) tot += red[w];
+        red[0] = tot;
+    }
+    __syncthreads();
+    tot = red[0];
+    __syncthreads();
+    return tot;
+}
+
+// Whole sample in one workgroup: keys -> LDS sort -> times.
+__global__ __launch_bounds__(kThreads) void k_code_small(const float *__restrict__ x, int n, int T,
+                                                         float min_value,
+                                                         uint8_t *__restrict__ times)
+{
+    extern __shared__ uint64_t keys[];
+    __shared__ int red[kThreads / 64];
+    const int b = blockIdx.x;
+    const float *xs = x + (size_t)b * n;
+    uint8_t *ts = times + (size_t)b * n;
+    int np2 = 1;
+    while (np2 < n) np2 <<= 1;
+    int mine = 0;
+    for (int i = threadIdx.x; i < np2; i += blockDim.x) {
+        uint64_t key = kDead;
+        if (i < n) {
+            key = make_key(xs[i], min_value, (uint32_t)i);
+            if (key == kDead) ts[i] = spk::kNever;
+            else mine++;
+        }
+        keys[i] = key;
+    }
+    const int N = block_sum(mine, red);
+    bitonic_sort_lds(keys, np2);
+    for (int r = threadIdx.x; r < N; r += blockDim.x)
+        ts[(uint32_t)keys[r]] = (uint8_t)(((long long)r * T) / N);
+}
+
+// Large samples, step 1: keys, never-firing outputs, eligible counts.
+__global__ void k_code_keys(const float *__restrict__ x, int B, int n, float min_value,
+                            uint64_t *__restrict__ keys, uint8_t *__restrict__ times,
+                            int *__restrict__ count)
+{
+    __shared__ int red[256 / 64];
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    int mine = 0;
+    if (i < n) {
+        uint64_t key = make_key(x[(size_t)b * n + i], min_value, (uint32_t)i);
+        keys[(size_t)b * n + i] = key;
+        if (key == kDead) times[(size_t)b * n + i] = spk::kNever;
+        else mine = 1;
+    }
+    int tot = block_sum(mine, red);
+    if (threadIdx.x == 0 && tot) atomicAdd(&count[b], tot);
+}
+
+__global__ void k_zero_int(int *p, int n)
+{
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
+}
+
+// Large samples, step 2: sort kSmall-key chunks in LDS.
+__global__ __launch_bounds__(kThreads) void k_code_chunks(uint64_t *__restrict__ keys, int n)
+{
+    extern __shared__ uint64_t s[];
+    const int b = blockIdx.y;
+    const int base = blockIdx.x * kSmall;
+    const int len = min(kSmall, n - base);
+    uint64_t *g = keys + (size_t)b * n + base;
+    for (int i = threadIdx.x; i < kSmall; i += blockDim.x) s[i] = (i < len) ? g[i] : kDead;
+    __syncthreads();
+    bitonic_sort_lds(s, kSmall);
+    for (int i = threadIdx.x; i < len; i += blockDim.x) g[i] = s[i];
+}
+
+// Large samples, step 3: merge sorted runs of `width` pairwise, src -> dst.
+__global__ void k_code_merge(const uint64_t *__restrict__ src, uint64_t *__restrict__ dst, int n,
+                             int width)
+{
+    const int b = blockIdx.y;
+    const long long first = ((long long)blockIdx.x * blockDim.x + threadIdx.x) * kMergePerThread;
+    if (first >= n) return;
+    const uint64_t *S = src + (size_t)b * n;
+    uint64_t *D = dst + (size_t)b * n;
+    const int lo = (int)(first / (2LL * width)) * 2 * width;
+    const int na = min(width, n - lo);
+    const int nb = max(0, min(width, n - lo - width));
+    const uint64_t *A = S + lo, *Bv = S + lo + na;
+    const int p = (int)first - lo;
+    // co-rank: number i of A keys among the first p merged keys
+    int ilo = max(0, p - nb), ihi = min(p, na);
+    while (ilo < ihi) {
+        int i = (ilo + ihi) >> 1;
+        if (A[i] < Bv[p - i - 1]) ilo = i + 1;
+        else ihi = i;
+    }
+    int i = ilo, j = p - ilo;
+    const int end = min(p + kMergePerThread, na + nb);
+    for (int q = p; q < end; q++) {
+        bool takeA = (j >= nb) || (i < na && A[i] < Bv[j]);
+        D[lo + q] = takeA ? A[i++] : Bv[j++];
+    }
+}
+
+// Large samples, step 4: rank -> time.
+__global__ void k_code_scatter(const uint64_t *__restrict__ keys, int n, int T,
+                               const int *__restrict__ count, uint8_t *__restrict__ times)
+{
+    const int b = blockIdx.y;
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    const int N = count[b];
+    if (r >= N) return;
+    uint32_t idx = (uint32_t)keys[(size_t)b * n + r];
+    times[(size_t)b * n + idx] = (uint8_t)(((long long)r * T) / N);
+}
+
+// Linear mode (sort disabled): one workgroup per sample.
+__global__ __launch_bounds__(kThreads) void k_code_linear(const float *__restrict__ x, int n, int T,
+                                                          float min_value,
+                                                          uint8_t *__restrict__ times)
+{
+#pragma clang fp contract(off)
+    __shared__ float red[kThreads / 64];
+    const int b = blockIdx.x;
+    const float *xs = x + (size_t)b * n;
+    uint8_t *ts = times + (size_t)b * n;
+    float m = -INFINITY;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+        float v = xs[i];
+        if (v > min_value) m = fmaxf(m, v);
+    }
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_down(m, o, 64));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float mm = red[0];
+        for (int w = 1; w < (int)(blockDim.x >> 6); w++) mm = fmaxf(mm, red[w]);
+        red[0] = mm;
+    }
+    __syncthreads();
+    const float vmax = red[0];
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+        float v = xs[i];
+        uint8_t t = spk::kNever;
+        if (v > min_value) {
+            float q = v / vmax;
+            float s = 1.0f - q;
+            float u = s * (float)T;
+            int ti = (int)floorf(u);
+            ti = min(ti, T - 1);
+            ti = max(ti, 0);
+            t = (uint8_t)ti;
+        }
+        ts[i] = t;
+    }
+}
+
+__global__ void k_code_frames(const uint8_t *__restrict__ times, int T, int n,
+                              uint8_t *__restrict__ frames)
+{
+    const int b = blockIdx.z, t = blockIdx.y;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    frames[((size_t)b * T + t) * n + i] = (uint8_t)(times[(size_t)b * n + i] <= t);
+}
+
+size_t ws_layout(int B, long long n, size_t *off_b, size_t *off_cnt)
+{
+    if (n <= kSmall) {
+        *off_b = *off_cnt = 0;
+        return 0;
+    }
+    size_t keys = spk::align_up((size_t)B * n * sizeof(uint64_t), 256);
+    *off_b = keys;
+    *off_cnt = 2 * keys;
+    return 2 * keys + spk::align_up((size_t)B * sizeof(int), 256);
+}
+
+}  // namespace
+
+extern "C" size_t spk_latency_code_workspace_size(int B, int C, int H, int W)
+{
+    if (B <= 0 || C <= 0 || H <= 0 || W <= 0) return 0;
+    size_t a, c;
+    return ws_layout(B, (long long)C * H * W, &a, &c);
+}
+
+extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int W, int T,
+                                       float min_value, int mode, uint8_t *times, uint8_t *frames,
+                                       void *ws, size_t ws_bytes, spk_stream stream)
+{
+    spk::clear_error();
+    SPK_REQUIRE(x && times, SPK_E_ARG, "spk_latency_code: NULL pointer");
+    SPK_REQUIRE(B > 0 && C > 0 && H > 0 && W > 0, SPK_E_ARG,
+                "spk_latency_code: B=%d C=%d H=%d W=%d must be positive", B, C, H, W);
+    SPK_REQUIRE(mode == SPK_CODE_RANK || mode == SPK_CODE_LINEAR, SPK_E_ARG,
+                "spk_latency_code: unknown mode %d", mode);
+    SPK_REQUIRE(T >= 1 && T <= SPK_MAX_T, SPK_E_SHAPE, "spk_latency_code: T=%d not in [1, %d]", T,
+                SPK_MAX_T);
+    const long long nl = (long long)C * H * W;
+    SPK_REQUIRE(nl < (1LL << 31) && (long long)B * nl < (1LL << 40), SPK_E_SHAPE,
+                "spk_latency_code: sample of %lld values too large", nl);
+    SPK_REQUIRE(B <= 65535, SPK_E_SHAPE, "spk_latency_code: B=%d > 65535", B);
+    const int n = (int)nl;
+    size_t off_b, off_cnt;
+    const size_t need = mode == SPK_CODE_RANK ? ws_layout(B, n, &off_b, &off_cnt) : 0;
+    SPK_REQUIRE(ws_bytes >= need && (need == 0 || ws), SPK_E_WORKSPACE,
+                "spk_latency_code: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+    hipStream_t s = spk::stream_of(stream);
+
+    if (mode == SPK_CODE_LINEAR) {
+        hipLaunchKernelGGL(k_code_linear, dim3(B), dim3(kThreads), 0, s, x, n, T, min_value, times);
+        SPK_LAUNCHED("spk_latency_code");
+    } else if (n <= kSmall) {
+        int np2 = 1;
+        while (np2 < n) np2 <<= 1;
+        hipLaunchKernelGGL(k_code_small, dim3(B), dim3(kThreads), np2 * sizeof(uint64_t), s, x, n,
+                           T, min_value, times);
+        SPK_LAUNCHED("spk_latency_code");
+    } else {
+        uint64_t *ka = (uint64_t *)ws;
+        uint64_t *kb = (uint64_t *)((char *)ws + off_b);
+        int *cnt = (int *)((char *)ws + off_cnt);
+        hipLaunchKernelGGL(k_zero_int, dim3(spk::ceil_div(B, 256)), dim3(256), 0, s, cnt, B);
+        SPK_LAUNCHED("spk_latency_code");
+        hipLaunchKernelGGL(k_code_keys, dim3(spk::ceil_div(n, 256), B), dim3(256), 0, s, x, B, n,
+                           min_value, ka, times, cnt);
+        SPK_LAUNCHED("spk_latency_code");
+        hipLaunchKernelGGL(k_code_chunks, dim3(spk::ceil_div(n, kSmall), B), dim3(kThreads),
+                           kSmall * sizeof(uint64_t), s, ka, n);
+        SPK_LAUNCHED("spk_latency_code");
+        uint64_t *src = ka, *dst = kb;
+        for (long long width = kSmall; width < n; width *= 2) {
+            dim3 grid(spk::ceil_div(spk::ceil_div(n, kMergePerThread), 256), B);
+            hipLaunchKernelGGL(k_code_merge, grid, dim3(256), 0, s, src, dst, n, (int)width);
+            SPK_LAUNCHED("spk_latency_code");
+            std::swap(src, dst);
+        }
+        hipLaunchKernelGGL(k_code_scatter, dim3(spk::ceil_div(n, 256), B), dim3(256), 0, s, src, n,
+                           T, cnt, times);
+        SPK_LAUNCHED("spk_latency_code");
+    }
+    if (frames) {
+        SPK_REQUIRE(T <= 65535, SPK_E_SHAPE, "spk_latency_code: T too large for frames");
+        hipLaunchKernelGGL(k_code_frames, dim3(spk::ceil_div(n, 256), T, B), dim3(256), 0, s, times,
+                           T, n, frames);
+        SPK_LAUNCHED("spk_latency_code");
+    }
+    return SPK_OK;
+}

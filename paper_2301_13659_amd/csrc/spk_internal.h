@@ -1,0 +1,41 @@
+// Internal helpers of libspk (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "spk.h"
+
+namespace spk {
+
+constexpr int kNever = SPK_NEVER;
+
+void clear_error();
+void set_error(const char *fmt, ...) __attribute__((format(printf, 1, 2)));
+
+// Report the first launch failure of a call as SPK_E_HIP.
+spk_status check_launch(const char *what);
+
+inline hipStream_t stream_of(spk_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
+
+inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+}  // namespace spk
+
+#define SPK_REQUIRE(cond, code, ...)        \
+    do {                                    \
+        if (!(cond)) {                      \
+            spk::set_error(__VA_ARGS__);    \
+            return (code);                  \
+        }                                   \
+    } while (0)
+
+#define SPK_LAUNCHED(what)                                  \
+    do {                                                    \
+        spk_status st_ = spk::check_launch(what);           \
+        if (st_ != SPK_OK) return st_;                      \
+    } while (0)

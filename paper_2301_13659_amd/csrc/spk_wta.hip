@@ -1,0 +1,229 @@
+// spk_inhibit_winners: lateral inhibition and convolutional k-WTA (Spyker §II-F.3).
+//
+// Pointwise inhibition is one coalesced sweep over the spike-time and
+// potential maps: one thread per location (b, y, x) walks the C maps and
+// keeps the earliest neuron (then the higher potential, then the lower map).
+// Its survivor is written as an 8-byte record (time|map, potential) to the
+// workspace, and optionally the inhibited time map.  Winner selection then
+// runs one workgroup per sample: up to k rounds of a block-wide arg-min over
+// the surviving records, with the suppressed maps and locations kept as bit
+// sets in LDS.  Readout layers (no threshold) and calls without pointwise
+// inhibition rank the neurons themselves instead of per-location records.
+#include "spk_internal.h"
+
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kMaxPos = 1 << 19;      // H*W per sample (64 KB location bit set)
+constexpr int kMaxMaps = 1 << 16;     // C (8 KB map bit set)
+constexpr int kMaxK = 4096;
+
+struct Rec {
+    uint32_t tc;  // time << 24 | map; time == NEVER: no survivor here
+    float v;
+};
+
+__device__ __forceinline__ uint32_t order_desc(float v)
+{
+    if (v == 0.0f) v = 0.0f;
+    uint32_t u = __float_as_uint(v);
+    uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ~asc;
+}
+
+__global__ void k_pointwise(const uint8_t *times, const float *__restrict__ vkey, int C, int HW,
+                            long long total, Rec *__restrict__ recs, uint8_t *inhibited)
+{
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;  // b*HW + p
+    if (i >= total) return;
+    const long long b = i / HW, p = i - b * HW;
+    const size_t base = (size_t)b * C * HW + p;
+    int bt = spk::kNever, bc = -1;
+    float bv = 0.0f;
+    for (int c = 0; c < C; c++) {
+        int t = times[base + (size_t)c * HW];
+        if (t == spk::kNever || t > bt) continue;
+        float v = vkey[base + (size_t)c * HW];
+        if (t < bt || v > bv) {
+            bt = t;
+            bv = v;
+            bc = c;
+        }
+    }
+    recs[i] = Rec{((uint32_t)bt << 24) | (uint32_t)(bc < 0 ? 0 : bc), bv};
+    if (inhibited)
+        for (int c = 0; c < C; c++)
+            inhibited[base + (size_t)c * HW] = (c == bc) ? (uint8_t)bt : (uint8_t)spk::kNever;
+}
+
+// Lexicographic (hi, lo) minimum across the block; returns the winner to all.
+__device__ void block_argmin(uint64_t &hi, uint32_t &lo, uint64_t *s_hi, uint32_t *s_lo)
+{
+    for (int o = 32; o > 0; o >>= 1) {
+        uint64_t h2 = __shfl_xor(hi, o, 64);
+        uint32_t l2 = __shfl_xor(lo, o, 64);
+        if (h2 < hi || (h2 == hi && l2 < lo)) {
+            hi = h2;
+            lo = l2;
+        }
+    }
+    const int wid = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        s_hi[wid] = hi;
+        s_lo[wid] = lo;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < (int)(blockDim.x >> 6); w++)
+            if (s_hi[w] < s_hi[0] || (s_hi[w] == s_hi[0] && s_lo[w] < s_lo[0])) {
+                s_hi[0] = s_hi[w];
+                s_lo[0] = s_lo[w];
+            }
+    }
+    __syncthreads();
+    hi = s_hi[0];
+    lo = s_lo[0];
+    __syncthreads();
+}
+
+struct WtaArgs {
+    int C, H, W, T, k, radius, readout, by_record;
+};
+
+__global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__ times,
+                                                     const float *__restrict__ vkey,
+                                                     const Rec *__restrict__ recs, WtaArgs a,
+                                                     spk_winner *__restrict__ winners,
+                                                     int32_t *__restrict__ n_winners)
+{
+    extern __shared__ uint32_t bits[];  // [positions][maps]
+    __shared__ uint64_t s_hi[kThreads / 64];
+    __shared__ uint32_t s_lo[kThreads / 64];
+    const int b = blockIdx.x;
+    const int HW = a.H * a.W;
+    const int pw = (HW + 31) / 32, cw = (a.C + 31) / 32;
+    uint32_t *pos_dead = bits, *map_dead = bits + pw;
+    for (int i = threadIdx.x; i < pw + cw; i += blockDim.x) bits[i] = 0;
+    __syncthreads();
+    const uint64_t kNone = ~0ull;
+    int count = 0;
+    for (int round = 0; round < a.k; round++) {
+        uint64_t hi = kNone;
+        uint32_t lo = ~0u;
+        if (a.by_record) {
+            const Rec *rb = recs + (size_t)b * HW;
+            for (int p = threadIdx.x; p < HW; p += blockDim.x) {
+                if (pos_dead[p >> 5] & (1u << (p & 31))) continue;
+                Rec r = rb[p];
+                uint32_t t = r.tc >> 24, c = r.tc & 0xFFFFFFu;
+                if (t == (uint32_t)spk::kNever || (map_dead[c >> 5] & (1u << (c & 31)))) continue;
+                uint64_t h = ((uint64_t)t << 32) | order_desc(r.v);
+                uint32_t l = c * (uint32_t)HW + (uint32_t)p;
+                if (h < hi || (h == hi && l < lo)) {
+                    hi = h;
+                    lo = l;
+                }
+            }
+        } else {
+            const size_t base = (size_t)b * a.C * HW;
+            const int n = a.C * HW;
+            for (int i = threadIdx.x; i < n; i += blockDim.x) {
+                int c = i / HW, p = i - c * HW;
+                if (pos_dead[p >> 5] & (1u << (p & 31))) continue;
+                if (map_dead[c >> 5] & (1u << (c & 31))) continue;
+                uint32_t t = times[base + i];
+                if (!a.readout && t == (uint32_t)spk::kNever) continue;
+                uint64_t h = ((uint64_t)(a.readout ? 0u : t) << 32) | order_desc(vkey[base + i]);
+                if (h < hi || (h == hi && (uint32_t)i < lo)) {
+                    hi = h;
+                    lo = (uint32_t)i;
+                }
+            }
+        }
+        block_argmin(hi, lo, s_hi, s_lo);
+        if (hi == kNone) break;
+        const int c = (int)(lo / (uint32_t)HW), p = (int)(lo % (uint32_t)HW);
+        const int y = p / a.W, x = p - y * a.W;
+        if (threadIdx.x == 0) {
+            spk_winner wn;
+            wn.c = c;
+            wn.y = y;
+            wn.x = x;
+            wn.t = a.readout ? a.T - 1 : (int)(hi >> 32);
+            wn.v = vkey[(size_t)b * a.C * HW + (size_t)c * HW + p];
+            winners[(size_t)b * a.k + count] = wn;
+            map_dead[c >> 5] |= 1u << (c & 31);
+        }
+        const int r = a.radius, side = 2 * r + 1;
+        for (int i = threadIdx.x; i < side * side; i += blockDim.x) {
+            int yy = y - r + i / side, xx = x - r + i % side;
+            if (yy >= 0 && yy < a.H && xx >= 0 && xx < a.W) {
+                int q = yy * a.W + xx;
+                atomicOr(&pos_dead[q >> 5], 1u << (q & 31));
+            }
+        }
+        count++;
+        __syncthreads();
+    }
+    for (int s = count + threadIdx.x; s < a.k; s += blockDim.x)
+        winners[(size_t)b * a.k + s] = spk_winner{-1, -1, -1, -1, 0.0f};
+    if (threadIdx.x == 0) n_winners[b] = count;
+}
+
+}  // namespace
+
+extern "C" size_t spk_inhibit_winners_workspace_size(int B, int C, int H, int W)
+{
+    (void)C;
+    if (B <= 0 || H <= 0 || W <= 0) return 0;
+    return spk::align_up((size_t)B * H * W * sizeof(Rec), 256);
+}
+
+extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vkey, int B, int C,
+                                          int H, int W, int T, int pointwise, int k, int radius,
+                                          int readout, uint8_t *inhibited, spk_winner *winners,
+                                          int32_t *n_winners, void *ws, size_t ws_bytes,
+                                          spk_stream stream)
+{
+    spk::clear_error();
+    SPK_REQUIRE(times && vkey && n_winners && (winners || k == 0), SPK_E_ARG,
+                "spk_inhibit_winners: NULL pointer");
+    SPK_REQUIRE(B > 0 && C > 0 && H > 0 && W > 0 && k >= 0 && radius >= 0, SPK_E_ARG,
+                "spk_inhibit_winners: B=%d C=%d H=%d W=%d k=%d radius=%d", B, C, H, W, k, radius);
+    SPK_REQUIRE(T >= 1 && T <= SPK_MAX_T, SPK_E_SHAPE, "spk_inhibit_winners: T=%d not in [1, %d]",
+                T, SPK_MAX_T);
+    SPK_REQUIRE((long long)H * W <= kMaxPos && C <= kMaxMaps && k <= kMaxK &&
+                    (long long)C * H * W < (1LL << 31),
+                SPK_E_SHAPE, "spk_inhibit_winners: H*W <= %d, C <= %d, k <= %d required", kMaxPos,
+                kMaxMaps, kMaxK);
+    SPK_REQUIRE(!(readout && pointwise), SPK_E_UNSUPPORTED,
+                "spk_inhibit_winners: readout ranks all neurons; pointwise must be 0");
+    SPK_REQUIRE(B <= 65535 || !pointwise, SPK_E_SHAPE, "spk_inhibit_winners: B > 65535");
+    const size_t need = pointwise ? spk_inhibit_winners_workspace_size(B, C, H, W) : 0;
+    SPK_REQUIRE(ws_bytes >= need && (need == 0 || ws), SPK_E_WORKSPACE,
+                "spk_inhibit_winners: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+    hipStream_t s = spk::stream_of(stream);
+    const int HW = H * W;
+    Rec *recs = (Rec *)ws;
+    if (pointwise) {
+        const long long total = (long long)B * HW;
+        hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 256)), dim3(256), 0, s, times,
+                           vkey, C, HW, total, recs, inhibited);
+        SPK_LAUNCHED("spk_inhibit_winners");
+    } else if (inhibited && inhibited != times) {
+        SPK_REQUIRE(hipMemcpyAsync(inhibited, times, (size_t)B * C * HW, hipMemcpyDeviceToDevice,
+                                   s) == hipSuccess,
+                    SPK_E_HIP, "spk_inhibit_winners: copy of the time map failed");
+    }
+    WtaArgs a{C, H, W, T, k, radius, readout, pointwise};
+    const size_t lds = ((size_t)(HW + 31) / 32 + (C + 31) / 32) * sizeof(uint32_t);
+    if (k > 0) {
+        hipLaunchKernelGGL(k_select, dim3(B), dim3(kThreads), lds, s, times, vkey, recs, a,
+                           winners, n_winners);
+    } else {
+        hipLaunchKernelGGL(k_select, dim3(B), dim3(64), lds, s, times, vkey, recs, a, winners,
+                           n_winners);
+    }
+    SPK_LAUNCHED("spk_inhibit_winners");
+    return SPK_OK;
+}

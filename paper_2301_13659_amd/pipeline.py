@@ -1,0 +1,145 @@
+"""One step of a workload's spiking network, chained through libspk.
+
+A step is one pass of the hot path over one batch (the layer-wise training
+of Spyker's listings, §IV): DoG filtering and rank-order coding of the images
+(or a given spike-time input), then per conv layer: conv + fire, and for a
+learning layer lateral inhibition + k-WTA + STDP (R-STDP for a readout
+layer trained with labels), with pooling between layers.  The forward pass
+between layers is not inhibited; learning uses the outputs computed with the
+weights from before the step.  Readout layers (infinite threshold) pick
+their winners by potential.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import torch
+
+from . import spk
+from . import workloads as wls
+
+
+@dataclass
+class LayerState:
+    spec: wls.ConvSpec
+    w: torch.Tensor                       # float32 master
+    w16: torch.Tensor | None = None       # half operand (f16 layers)
+
+
+@dataclass
+class StepOutputs:
+    dog: torch.Tensor | None = None
+    times0: torch.Tensor | None = None
+    layer_in: list = field(default_factory=list)     # input time map of each conv layer
+    layer_out: list = field(default_factory=list)    # (t_f, v_key) of each conv layer
+    winners: dict = field(default_factory=dict)      # conv index -> (winners, n_winners)
+    winner_cfg: dict = field(default_factory=dict)   # conv index -> winner_cfg (R-STDP)
+    pooled: list = field(default_factory=list)
+
+
+class Pipeline:
+    def __init__(self, wl: wls.Workload, device="cuda", density_index: int = 0):
+        self.wl = wl
+        self.device = torch.device(device)
+        if wl.image_hw is not None:
+            self.images = torch.from_numpy(wls.make_images(wl)).to(self.device)
+            self.spike_input = None
+        else:
+            self.images = None
+            self.spike_input = torch.from_numpy(wls.make_spike_times(wl, density_index)).to(self.device)
+        self.layers = []
+        for li, spec in enumerate(wl.convs, start=1):
+            w = torch.from_numpy(wls.make_weights(wl, li)).to(self.device)
+            w16 = w.to(torch.float16) if spec.w_dtype == "f16" else None
+            self.layers.append(LayerState(spec, w, w16))
+        self.labels = torch.from_numpy(wls.make_labels(wl)).to(self.device) if wl.rstdp_group else None
+        self.cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
+        self.filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
+
+    def snapshot_weights(self):
+        return [(l.w.clone(), None if l.w16 is None else l.w16.clone()) for l in self.layers]
+
+    def restore_weights(self, snap):
+        for l, (w, w16) in zip(self.layers, snap):
+            l.w.copy_(w)
+            if w16 is not None:
+                l.w16.copy_(w16)
+
+    def step(self, keep: bool = False, learn: bool = True, timers: dict | None = None,
+             only: set | None = None) -> StepOutputs | None:
+        """One pass over the batch.  timers: stage name -> list of (start, end)
+        torch.cuda.Event pairs recorded on the current stream around each stage
+        (or only around the stages named in `only`)."""
+        wl = self.wl
+        out = StepOutputs() if keep else None
+
+        def timed(name, fn):
+            if timers is None or (only is not None and name not in only):
+                return fn()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            r = fn()
+            b.record()
+            timers.setdefault(name, []).append((a, b))
+            return r
+
+        if self.images is not None:
+            x = timed("dog", lambda: spk.spk_dog_filter(self.images, self.filters))
+            t = timed("code", lambda: spk.spk_latency_code(x, wl.T, wl.min_value))
+            if keep:
+                out.dog, out.times0 = x, t
+        else:
+            t = self.spike_input
+        li = 0
+        pi = 0
+        for kind, s in wl.stages:
+            if kind == "pool":
+                pi += 1
+                t = timed(f"pool{pi}", lambda: spk.spk_pool(t, s.k, s.stride, s.pad))
+                if keep:
+                    out.pooled.append(t)
+                continue
+            layer = self.layers[li]
+            w_op = layer.w16 if layer.w16 is not None else layer.w
+            n = li + 1
+            tf, vk = timed(f"conv{n}", lambda: spk.spk_conv_fire(t, w_op, wl.T, s.stride, s.pad,
+                                                                 s.theta))
+            if keep:
+                out.layer_in.append(t)
+                out.layer_out.append((tf, vk))
+            if s.stdp or s.readout:
+                win, nw = timed(f"wta{n}", lambda: spk.spk_inhibit_winners(
+                    tf, vk, wl.T, s.k_win, s.radius, pointwise=not s.readout, readout=s.readout))
+                if keep:
+                    out.winners[li] = (win, nw)
+                if s.stdp and learn:
+                    wc = None
+                    if wl.rstdp_group:
+                        wc = timed(f"select{n}", lambda: spk.spk_rstdp_select(
+                            win, nw, self.labels, wl.rstdp_group))
+                        if keep:
+                            out.winner_cfg[li] = wc
+                    timed(f"stdp{n}", lambda: spk.spk_stdp_update(
+                        layer.w, t, win, nw, self.cfgs, s.stride, s.pad, winner_cfg=wc,
+                        w_f16=layer.w16))
+            t = tf
+            li += 1
+        return out
+
+
+def conv_flops(wl: wls.Workload) -> list:
+    """Dense-interface work per conv layer and batch: 2*B*T*Ho*Wo*Co*Ci*Kh*Kw."""
+    C, H, W = wl.input_chw()
+    res = []
+    for kind, s in wl.stages:
+        if kind == "pool":
+            H = (H + 2 * s.pad - s.k) // s.stride + 1
+            W = (W + 2 * s.pad - s.k) // s.stride + 1
+            continue
+        Ho = (H + 2 * s.pad - s.k) // s.stride + 1
+        Wo = (W + 2 * s.pad - s.k) // s.stride + 1
+        res.append(2 * wl.batch * wl.T * Ho * Wo * s.co * s.ci * s.k * s.k)
+        C, H, W = s.co, Ho, Wo
+    return res

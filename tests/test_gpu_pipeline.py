@@ -1,0 +1,132 @@
+"""End-to-end parity of one workload step (the step bench.py times), stage by stage.
+
+Every stage of the GPU step is checked against the oracle run on the inputs
+that stage received on the GPU (stage isolation), so a neuron that sits on its
+threshold cannot cascade into later stages.  Reduced batches are compared in
+full; the full-size steps compare DoG, codes, pooling, winners and weights in
+full and the convolutions on sampled neurons.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from parity import (NEVER, W_ABS, check_fire, check_potentials, excused_from_potentials, gpu,
+                    np_, winners_list)
+from paper_2301_13659_amd import spk, workloads
+from paper_2301_13659_amd.pipeline import Pipeline
+
+pytestmark = pytest.mark.gpu
+
+
+def _sample_neurons(tf, rng, n):
+    """Random neurons plus neurons that fired (the interesting ones)."""
+    shape = tf.shape
+    idx = [tuple(int(v) for v in np.unravel_index(i, shape))
+           for i in rng.choice(tf.size, size=min(n, tf.size), replace=False)]
+    fired = np.argwhere(tf != NEVER)
+    if len(fired):
+        pick = rng.choice(len(fired), size=min(n // 2, len(fired)), replace=False)
+        idx += [tuple(int(v) for v in fired[i]) for i in pick]
+    return idx
+
+
+def _check_conv_sampled(t_in, w, spec, T, g_tf, g_vk, rng, n=300):
+    for (b, o, y, x) in _sample_neurons(g_tf, rng, n):
+        V = oracle.conv_neuron(t_in, w, T, spec.stride, spec.pad, b, o, y, x)
+        tf, vk = oracle.fire_neuron(V, spec.theta)
+        excused = np.isfinite(spec.theta) and np.any(np.abs(V - spec.theta) <= 1e-4 * abs(spec.theta))
+        if not excused:
+            assert g_tf[b, o, y, x] == tf, (b, o, y, x, g_tf[b, o, y, x], tf)
+            check_potentials(np.array([g_vk[b, o, y, x]]), np.array([vk]), "v_key")
+
+
+def _run_and_check(wl, full_conv: bool, density_index: int = 1):
+    dev = gpu()
+    pipe = Pipeline(wl, dev, density_index=density_index)
+    w_before = [np_(l.w16.float() if l.w16 is not None else l.w).copy() for l in pipe.layers]
+    master_before = [np_(l.w).copy() for l in pipe.layers]
+    out = pipe.step(keep=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(wl.index)
+    filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
+    if pipe.images is not None:
+        img = np_(pipe.images)
+        g_dog = np_(out.dog)
+        np.testing.assert_array_equal(g_dog.view(np.uint32),
+                                      oracle.dog_filter(img, filters).view(np.uint32))
+        np.testing.assert_array_equal(np_(out.times0), oracle.latency_code(g_dog, wl.T, wl.min_value))
+    excused_total = 0
+    pool_i = 0
+    li = 0
+    for kind, s in wl.stages:
+        if kind == "pool":
+            src = np_(out.layer_out[li - 1][0])
+            np.testing.assert_array_equal(np_(out.pooled[pool_i]), oracle.pool(src, s.k, s.stride, s.pad))
+            pool_i += 1
+            continue
+        t_in = np_(out.layer_in[li])
+        g_tf, g_vk = (np_(a) for a in out.layer_out[li])
+        if full_conv:
+            o_tf, o_vk, o_V = oracle.conv_fire(t_in, w_before[li], wl.T, s.stride, s.pad, s.theta,
+                                               potentials=True)
+            excused_total += check_fire(g_tf, g_vk, o_tf, o_vk, excused_from_potentials(o_V, s.theta))
+        else:
+            _check_conv_sampled(t_in, w_before[li], s, wl.T, g_tf, g_vk, rng)
+        if li in out.winners:
+            win, n = out.winners[li]
+            g_win, g_n = spk.winners_numpy(win), np_(n)
+            cand = g_tf if s.readout else oracle.inhibit(g_tf, g_vk)
+            o_win, o_n = oracle.kwta(cand, g_vk, wl.T, s.k_win, s.radius, s.readout)
+            np.testing.assert_array_equal(g_n, o_n)
+            assert winners_list(g_win, g_n) == winners_list(o_win, o_n)
+            if s.stdp:
+                wc = None
+                if wl.rstdp_group:
+                    wc = np_(out.winner_cfg[li])
+                    np.testing.assert_array_equal(
+                        wc, oracle.rstdp_select(g_win, g_n, np_(pipe.labels), wl.rstdp_group))
+                cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
+                ref = oracle.stdp_update(master_before[li], t_in, g_win, g_n, cfgs, s.stride, s.pad,
+                                         winner_cfg=wc)
+                got = np_(pipe.layers[li].w)
+                np.testing.assert_allclose(got, ref, rtol=0, atol=W_ABS)
+                if pipe.layers[li].w16 is not None:
+                    np.testing.assert_array_equal(np_(pipe.layers[li].w16), got.astype(np.float16))
+        li += 1
+    return excused_total
+
+
+@pytest.mark.parametrize("cfg,batch", [(1, 8), (2, 2), (3, 3), (4, 1)])
+def test_workload_step_reduced_batch(cfg, batch):
+    wl = workloads.get(cfg).with_batch(batch)
+    excused = _run_and_check(wl, full_conv=True)
+    assert excused <= 5
+
+
+@pytest.mark.parametrize("density_index", [0, 1, 2])
+def test_cfg5_step_reduced_batch(density_index):
+    wl = workloads.get(5).with_batch(1)
+    _run_and_check(wl, full_conv=False, density_index=density_index)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workload_step_full_size(cfg):
+    wl = workloads.get(cfg)
+    _run_and_check(wl, full_conv=(cfg == 1), density_index=1)
+
+
+def test_step_is_deterministic():
+    dev = gpu()
+    wl = workloads.get(2).with_batch(4)
+    outs = []
+    for _ in range(2):
+        pipe = Pipeline(wl, dev)
+        o = pipe.step(keep=True)
+        torch.cuda.synchronize()
+        outs.append((np_(o.times0), [np_(a[0]) for a in o.layer_out], [np_(a[1]) for a in o.layer_out],
+                     [np_(l.w) for l in pipe.layers]))
+    a, b = outs
+    np.testing.assert_array_equal(a[0], b[0])
+    for x, y in zip(a[1] + a[2] + a[3], b[1] + b[2] + b[3]):
+        np.testing.assert_array_equal(x, y)
