@@ -147,13 +147,18 @@ spk_status spk_latency_code(const float *x, int B, int C, int H, int W, int T,
  *              orders equal spike times in winner selection, §II-F.3).
  *   potentials nullable float B x T x Co x Ho x Wo (device): every V_t
  *              (the paper's dense interface, §II-B).
- *   ws         workspace of spk_conv_fire_workspace_size(...) bytes.
- * Potentials are accumulated in float.
+ *   ws         workspace of spk_conv_fire_workspace_size(..., theta, potentials
+ *              != NULL) bytes (non-zero only for readout calls: theta = +inf
+ *              without dense potentials).
+ * Potentials are accumulated in float from products that are exact: binary
+ * spikes times half weights, or times the two halves hi + lo of a float
+ * weight (hi = half(w), lo = half(w - hi)).
  * Errors: SPK_E_ARG, SPK_E_SHAPE (T out of range, Ho or Wo <= 0),
  * SPK_E_UNSUPPORTED (w_dtype), SPK_E_WORKSPACE.
  */
 size_t spk_conv_fire_workspace_size(int B, int T, int Ci, int Hi, int Wi, int Co,
-                                    int Kh, int Kw, int stride, int pad);
+                                    int Kh, int Kw, int stride, int pad, float theta,
+                                    int potentials);
 spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int Hi, int Wi,
                          const void *w, spk_dtype w_dtype, int Co, int Kh, int Kw,
                          int stride, int pad, float theta,

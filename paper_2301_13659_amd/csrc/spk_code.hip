@@ -8,8 +8,9 @@
 // values (<= min_value, NaN) get the all-ones key, sort to the end and are
 // written as never firing up front.
 //
-//  - Samples of up to kSmall values are ranked by one workgroup each, with a
-//    bitonic sort of the keys in LDS.
+//  - Samples of up to kSmall values are ranked by one workgroup each: every
+//    thread sorts 8 keys in registers, then merge-path levels in LDS merge
+//    the runs (no padding to a power of two).
 //  - Larger samples: workgroups sort kSmall-key chunks in LDS, then merge
 //    passes double the sorted runs (merge-path split per thread) until each
 //    sample is one run; the ping-pong buffers live in the caller workspace.
@@ -19,7 +20,7 @@
 
 namespace {
 
-constexpr int kSmall = 8192;    // keys per LDS sort (64 KB)
+constexpr int kSmall = 8192;    // keys per LDS sort (2 x 64 KB)
 constexpr int kThreads = 1024;
 constexpr int kMergePerThread = 8;
 constexpr uint64_t kDead = ~0ull;
@@ -35,26 +36,6 @@ __device__ __forceinline__ uint32_t order_desc(float v)
 __device__ __forceinline__ uint64_t make_key(float v, float min_value, uint32_t i)
 {
     return (v > min_value) ? (((uint64_t)order_desc(v) << 32) | i) : kDead;
-}
-
-// Ascending bitonic sort of n (a power of two) keys in LDS by the whole block.
-__device__ void bitonic_sort_lds(uint64_t *s, int n)
-{
-    for (int k = 2; k <= n; k <<= 1)
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = threadIdx.x; i < n; i += blockDim.x) {
-                int ixj = i ^ j;
-                if (ixj > i) {
-                    uint64_t a = s[i], b = s[ixj];
-                    bool up = (i & k) == 0;
-                    if ((a > b) == up) {
-                        s[i] = b;
-                        s[ixj] = a;
-                    }
-                }
-            }
-            __syncthreads();
-        }
 }
 
 __device__ __forceinline__ int block_sum(int v, int *red)
@@ -74,32 +55,90 @@ __device__ __forceinline__ int block_sum(int v, int *red)
     return tot;
 }
 
-// Whole sample in one workgroup: keys -> LDS sort -> times.
+// Sort 8 keys held by one thread (ascending), a fixed compare-exchange network.
+__device__ __forceinline__ void cswap(uint64_t &a, uint64_t &b)
+{
+    const uint64_t lo = a < b ? a : b, hi = a < b ? b : a;
+    a = lo;
+    b = hi;
+}
+
+__device__ __forceinline__ void sort8(uint64_t *k)
+{
+    // Batcher's odd-even merge sort for 8 elements (19 exchanges)
+    cswap(k[0], k[1]); cswap(k[2], k[3]); cswap(k[4], k[5]); cswap(k[6], k[7]);
+    cswap(k[0], k[2]); cswap(k[1], k[3]); cswap(k[4], k[6]); cswap(k[5], k[7]);
+    cswap(k[1], k[2]); cswap(k[5], k[6]);
+    cswap(k[0], k[4]); cswap(k[1], k[5]); cswap(k[2], k[6]); cswap(k[3], k[7]);
+    cswap(k[2], k[4]); cswap(k[3], k[5]);
+    cswap(k[1], k[2]); cswap(k[3], k[4]); cswap(k[5], k[6]);
+}
+
+// Merge runs of `width` sorted keys pairwise (src -> dst, n keys); thread t
+// produces outputs [8t, 8t + 8) from a merge-path split.
+__device__ void merge_level(const uint64_t *src, uint64_t *dst, int n, int width)
+{
+    const int first = threadIdx.x * 8;
+    if (first >= n) return;
+    const int lo = (first / (2 * width)) * 2 * width;
+    const int na = min(width, n - lo), nb = max(0, min(width, n - lo - width));
+    const uint64_t *A = src + lo, *Bv = src + lo + na;
+    const int p = first - lo;
+    int ilo = max(0, p - nb), ihi = min(p, na);
+    while (ilo < ihi) {
+        const int i = (ilo + ihi) >> 1;
+        if (A[i] < Bv[p - i - 1]) ilo = i + 1;
+        else ihi = i;
+    }
+    int i = ilo, j = p - ilo;
+    const int end = min(p + 8, na + nb);
+    for (int q = p; q < end; q++) {
+        const bool takeA = (j >= nb) || (i < na && A[i] < Bv[j]);
+        dst[lo + q] = takeA ? A[i++] : Bv[j++];
+    }
+}
+
+// Whole sample in one workgroup: keys -> register sort of 8 -> LDS merge
+// levels -> times.  n <= 8 * blockDim.
 __global__ __launch_bounds__(kThreads) void k_code_small(const float *__restrict__ x, int n, int T,
                                                          float min_value,
                                                          uint8_t *__restrict__ times)
 {
-    extern __shared__ uint64_t keys[];
+    extern __shared__ uint64_t keys[];  // two buffers of n keys
     __shared__ int red[kThreads / 64];
     const int b = blockIdx.x;
     const float *xs = x + (size_t)b * n;
     uint8_t *ts = times + (size_t)b * n;
-    int np2 = 1;
-    while (np2 < n) np2 <<= 1;
+    uint64_t k8[8];
     int mine = 0;
-    for (int i = threadIdx.x; i < np2; i += blockDim.x) {
+    const int first = threadIdx.x * 8;
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+        const int i = first + j;
         uint64_t key = kDead;
         if (i < n) {
             key = make_key(xs[i], min_value, (uint32_t)i);
             if (key == kDead) ts[i] = spk::kNever;
             else mine++;
         }
-        keys[i] = key;
+        k8[j] = key;
     }
     const int N = block_sum(mine, red);
-    bitonic_sort_lds(keys, np2);
+    sort8(k8);
+    uint64_t *src = keys, *dst = keys + n;
+#pragma unroll
+    for (int j = 0; j < 8; j++)
+        if (first + j < n) src[first + j] = k8[j];
+    __syncthreads();
+    for (int width = 8; width < n; width *= 2) {
+        merge_level(src, dst, n, width);
+        __syncthreads();
+        uint64_t *t = src;
+        src = dst;
+        dst = t;
+    }
     for (int r = threadIdx.x; r < N; r += blockDim.x)
-        ts[(uint32_t)keys[r]] = (uint8_t)(((long long)r * T) / N);
+        ts[(uint32_t)src[r]] = (uint8_t)(((long long)r * T) / N);
 }
 
 // Large samples, step 1: keys, never-firing outputs, eligible counts.
@@ -127,18 +166,33 @@ __global__ void k_zero_int(int *p, int n)
     if (i < n) p[i] = 0;
 }
 
-// Large samples, step 2: sort kSmall-key chunks in LDS.
+// Large samples, step 2: sort kSmall-key chunks (register sort of 8, then
+// merge levels in LDS).
 __global__ __launch_bounds__(kThreads) void k_code_chunks(uint64_t *__restrict__ keys, int n)
 {
-    extern __shared__ uint64_t s[];
+    extern __shared__ uint64_t s[];  // two buffers of kSmall keys
     const int b = blockIdx.y;
     const int base = blockIdx.x * kSmall;
     const int len = min(kSmall, n - base);
     uint64_t *g = keys + (size_t)b * n + base;
-    for (int i = threadIdx.x; i < kSmall; i += blockDim.x) s[i] = (i < len) ? g[i] : kDead;
+    uint64_t k8[8];
+    const int first = threadIdx.x * 8;
+#pragma unroll
+    for (int j = 0; j < 8; j++) k8[j] = (first + j < len) ? g[first + j] : kDead;
+    sort8(k8);
+    uint64_t *src = s, *dst = s + kSmall;
+#pragma unroll
+    for (int j = 0; j < 8; j++)
+        if (first + j < len) src[first + j] = k8[j];
     __syncthreads();
-    bitonic_sort_lds(s, kSmall);
-    for (int i = threadIdx.x; i < len; i += blockDim.x) g[i] = s[i];
+    for (int width = 8; width < len; width *= 2) {
+        merge_level(src, dst, len, width);
+        __syncthreads();
+        uint64_t *t = src;
+        src = dst;
+        dst = t;
+    }
+    for (int i = threadIdx.x; i < len; i += blockDim.x) g[i] = src[i];
 }
 
 // Large samples, step 3: merge sorted runs of `width` pairwise, src -> dst.
@@ -280,10 +334,11 @@ extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int 
         hipLaunchKernelGGL(k_code_linear, dim3(B), dim3(kThreads), 0, s, x, n, T, min_value, times);
         SPK_LAUNCHED("spk_latency_code");
     } else if (n <= kSmall) {
-        int np2 = 1;
-        while (np2 < n) np2 <<= 1;
-        hipLaunchKernelGGL(k_code_small, dim3(B), dim3(kThreads), np2 * sizeof(uint64_t), s, x, n,
-                           T, min_value, times);
+        const size_t lds = 2 * (size_t)n * sizeof(uint64_t);
+        if (lds > 64 * 1024)
+            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_code_small),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_code_small, dim3(B), dim3(kThreads), lds, s, x, n, T, min_value, times);
         SPK_LAUNCHED("spk_latency_code");
     } else {
         uint64_t *ka = (uint64_t *)ws;
@@ -294,8 +349,11 @@ extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int 
         hipLaunchKernelGGL(k_code_keys, dim3(spk::ceil_div(n, 256), B), dim3(256), 0, s, x, B, n,
                            min_value, ka, times, cnt);
         SPK_LAUNCHED("spk_latency_code");
-        hipLaunchKernelGGL(k_code_chunks, dim3(spk::ceil_div(n, kSmall), B), dim3(kThreads),
-                           kSmall * sizeof(uint64_t), s, ka, n);
+        const size_t clds = 2 * (size_t)kSmall * sizeof(uint64_t);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_code_chunks),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)clds);
+        hipLaunchKernelGGL(k_code_chunks, dim3(spk::ceil_div(n, kSmall), B), dim3(kThreads), clds, s,
+                           ka, n);
         SPK_LAUNCHED("spk_latency_code");
         uint64_t *src = ka, *dst = kb;
         for (long long width = kSmall; width < n; width *= 2) {

@@ -1,8 +1,10 @@
 // spk_conv_fire: spiking convolution + integrate-and-fire (Spyker §II-E.1, Eq. 2).
 //
-// Direct form: one thread per output neuron (b, o, y, x) walks the time steps,
-// sums the weights of the inputs of its window that have fired by step t
-// (the cumulative frame S_t = [time <= t]) and records the first step whose
+// Shapes the matrix-core kernels cover (spk_conv_mfma.hip) go there.  The
+// rest (firing layers with more than 1536 taps) take the direct form below:
+// one thread per output neuron (b, o, y, x) walks the time steps, sums the
+// weights of the inputs of its window that have fired by step t (the
+// cumulative frame S_t = [time <= t]) and records the first step whose
 // potential exceeds theta.  Kernel o's weights are staged in LDS as float.
 #include <hip/hip_fp16.h>
 
@@ -69,12 +71,16 @@ __global__ __launch_bounds__(kThreads) void k_conv_fire_direct(
 
 }  // namespace
 
+static bool is_readout(float theta, bool potentials) { return !(theta <= 3.4e38f) && !potentials; }
+
 extern "C" size_t spk_conv_fire_workspace_size(int B, int T, int Ci, int Hi, int Wi, int Co,
-                                               int Kh, int Kw, int stride, int pad)
+                                               int Kh, int Kw, int stride, int pad, float theta,
+                                               int potentials)
 {
-    (void)B; (void)T; (void)Ci; (void)Hi; (void)Wi; (void)Co; (void)Kh; (void)Kw;
-    (void)stride; (void)pad;
-    return 0;
+    (void)T;
+    const int Ho = spk_out_extent(Hi, Kh, stride, pad), Wo = spk_out_extent(Wi, Kw, stride, pad);
+    if (B <= 0 || Ci <= 0 || Co <= 0 || Ho <= 0 || Wo <= 0) return 0;
+    return spk::conv_mfma_workspace(B, Ho, Wo, Co, Ci * Kh * Kw, is_readout(theta, potentials != 0));
 }
 
 extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int Hi, int Wi,
@@ -83,7 +89,6 @@ extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int C
                                     float *out_vkey, float *potentials, void *ws, size_t ws_bytes,
                                     spk_stream stream)
 {
-    (void)ws; (void)ws_bytes;
     spk::clear_error();
     SPK_REQUIRE(in_times && w && out_times && out_vkey, SPK_E_ARG, "spk_conv_fire: NULL pointer");
     SPK_REQUIRE(B > 0 && Ci > 0 && Hi > 0 && Wi > 0 && Co > 0 && Kh > 0 && Kw > 0 && stride > 0 &&
@@ -100,6 +105,18 @@ extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int C
     const long long taps = (long long)Ci * Kh * Kw;
     SPK_REQUIRE(taps <= kMaxTaps, SPK_E_SHAPE, "spk_conv_fire: Ci*Kh*Kw=%lld > %d", taps, kMaxTaps);
     SPK_REQUIRE(Co <= 65535 && B <= 65535, SPK_E_SHAPE, "spk_conv_fire: Co or B > 65535");
+    const bool half_w = w_dtype == SPK_F16;
+    const bool readout = is_readout(theta, potentials != nullptr);
+    const size_t need = spk_conv_fire_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, theta,
+                                                     potentials != nullptr);
+    SPK_REQUIRE(ws_bytes >= need && (need == 0 || ws), SPK_E_WORKSPACE,
+                "spk_conv_fire: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+    SPK_REQUIRE((long long)B * Ho * Wo < (1LL << 31) && (long long)Ci * Hi * Wi < (1LL << 31),
+                SPK_E_SHAPE, "spk_conv_fire: layer too large");
+    if (spk::conv_mfma_supported(Ci, Kh, Kw, Co, half_w, readout))
+        return spk::conv_fire_mfma(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho,
+                                   Wo, theta, out_times, out_vkey, potentials, ws,
+                                   spk::stream_of(stream));
     ConvGeom g{B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo};
     dim3 grid(spk::ceil_div((long long)Ho * Wo, kThreads), Co, B);
     size_t lds = (size_t)taps * sizeof(float);

@@ -24,6 +24,15 @@ inline size_t align_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
 
 inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 
+// Matrix-core spiking convolution (spk_conv_mfma.hip).  A readout call is a
+// call with theta = +inf and no dense potentials.
+bool conv_mfma_supported(int Ci, int Kh, int Kw, int Co, bool half_w, bool readout);
+size_t conv_mfma_workspace(int B, int Ho, int Wo, int Co, int K, bool readout);
+spk_status conv_fire_mfma(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
+                          bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
+                          float theta, uint8_t *out_t, float *out_v, float *pot, void *ws,
+                          hipStream_t s);
+
 }  // namespace spk
 
 #define SPK_REQUIRE(cond, code, ...)        \

@@ -13,7 +13,7 @@
 
 namespace {
 
-constexpr int kThreads = 1024;
+constexpr int kThreads = 256;
 constexpr int kMaxPos = 1 << 19;      // H*W per sample (64 KB location bit set)
 constexpr int kMaxMaps = 1 << 16;     // C (8 KB map bit set)
 constexpr int kMaxK = 4096;
@@ -31,29 +31,70 @@ __device__ __forceinline__ uint32_t order_desc(float v)
     return ~asc;
 }
 
-__global__ void k_pointwise(const uint8_t *times, const float *__restrict__ vkey, int C, int HW,
-                            long long total, Rec *__restrict__ recs, uint8_t *inhibited)
+// Block = 64 consecutive locations x kGroups waves; wave g walks the maps
+// c = g, g + kGroups, ... for its 64 locations (coalesced loads per map), and
+// the kGroups partial winners meet in LDS.
+constexpr int kGroups = 16;
+
+__device__ __forceinline__ bool earlier(int ta, float va, int ca, int tb, float vb, int cb)
 {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;  // b*HW + p
-    if (i >= total) return;
-    const long long b = i / HW, p = i - b * HW;
+    if (ta != tb) return ta < tb;
+    if (va != vb) return va > vb;
+    return ca < cb;
+}
+
+__global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times,
+                                                            const float *__restrict__ vkey, int C,
+                                                            int HW, long long total,
+                                                            Rec *__restrict__ recs,
+                                                            uint8_t *inhibited)
+{
+    __shared__ int s_t[kGroups][64], s_c[kGroups][64];
+    __shared__ float s_v[kGroups][64];
+    const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
+    const long long i = (long long)blockIdx.x * 64 + lane;  // b*HW + p
+    const bool ok = i < total;
+    const long long b = ok ? i / HW : 0, p = i - b * HW;
     const size_t base = (size_t)b * C * HW + p;
     int bt = spk::kNever, bc = -1;
     float bv = 0.0f;
-    for (int c = 0; c < C; c++) {
-        int t = times[base + (size_t)c * HW];
-        if (t == spk::kNever || t > bt) continue;
-        float v = vkey[base + (size_t)c * HW];
-        if (t < bt || v > bv) {
-            bt = t;
-            bv = v;
-            bc = c;
+    if (ok) {
+        for (int c = grp; c < C; c += kGroups) {
+            const int t = times[base + (size_t)c * HW];
+            if (t == spk::kNever || t > bt) continue;
+            const float v = vkey[base + (size_t)c * HW];
+            if (t < bt || v > bv) {
+                bt = t;
+                bv = v;
+                bc = c;
+            }
         }
     }
-    recs[i] = Rec{((uint32_t)bt << 24) | (uint32_t)(bc < 0 ? 0 : bc), bv};
-    if (inhibited)
-        for (int c = 0; c < C; c++)
-            inhibited[base + (size_t)c * HW] = (c == bc) ? (uint8_t)bt : (uint8_t)spk::kNever;
+    s_t[grp][lane] = bt;
+    s_v[grp][lane] = bv;
+    s_c[grp][lane] = bc;
+    __syncthreads();
+    if (grp == 0) {
+        for (int q = 1; q < kGroups; q++) {
+            const int t = s_t[q][lane], c = s_c[q][lane];
+            const float v = s_v[q][lane];
+            if (c >= 0 && (bc < 0 || earlier(t, v, c, bt, bv, bc))) {
+                bt = t;
+                bv = v;
+                bc = c;
+            }
+        }
+        s_t[0][lane] = bt;
+        s_c[0][lane] = bc;
+        if (ok) recs[i] = Rec{((uint32_t)bt << 24) | (uint32_t)(bc < 0 ? 0 : bc), bv};
+    }
+    if (inhibited) {
+        __syncthreads();
+        const int wt = s_t[0][lane], wc = s_c[0][lane];
+        if (ok)
+            for (int c = grp; c < C; c += kGroups)
+                inhibited[base + (size_t)c * HW] = (c == wc) ? (uint8_t)wt : (uint8_t)spk::kNever;
+    }
 }
 
 // Lexicographic (hi, lo) minimum across the block; returns the winner to all.
@@ -93,17 +134,23 @@ struct WtaArgs {
 __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__ times,
                                                      const float *__restrict__ vkey,
                                                      const Rec *__restrict__ recs, WtaArgs a,
-                                                     spk_winner *__restrict__ winners,
+                                                     int stage_recs, spk_winner *__restrict__ winners,
                                                      int32_t *__restrict__ n_winners)
 {
-    extern __shared__ uint32_t bits[];  // [positions][maps]
+    extern __shared__ uint32_t bits[];  // [positions][maps] dead bits, then staged records
     __shared__ uint64_t s_hi[kThreads / 64];
     __shared__ uint32_t s_lo[kThreads / 64];
     const int b = blockIdx.x;
     const int HW = a.H * a.W;
     const int pw = (HW + 31) / 32, cw = (a.C + 31) / 32;
     uint32_t *pos_dead = bits, *map_dead = bits + pw;
+    Rec *srec = reinterpret_cast<Rec *>(bits + ((pw + cw + 1) & ~1));
     for (int i = threadIdx.x; i < pw + cw; i += blockDim.x) bits[i] = 0;
+    const Rec *rb = recs + (size_t)b * HW;
+    if (a.by_record && stage_recs) {
+        for (int p = threadIdx.x; p < HW; p += blockDim.x) srec[p] = rb[p];
+        rb = srec;
+    }
     __syncthreads();
     const uint64_t kNone = ~0ull;
     int count = 0;
@@ -111,14 +158,13 @@ __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__
         uint64_t hi = kNone;
         uint32_t lo = ~0u;
         if (a.by_record) {
-            const Rec *rb = recs + (size_t)b * HW;
             for (int p = threadIdx.x; p < HW; p += blockDim.x) {
                 if (pos_dead[p >> 5] & (1u << (p & 31))) continue;
-                Rec r = rb[p];
-                uint32_t t = r.tc >> 24, c = r.tc & 0xFFFFFFu;
+                const Rec r = rb[p];
+                const uint32_t t = r.tc >> 24, c = r.tc & 0xFFFFFFu;
                 if (t == (uint32_t)spk::kNever || (map_dead[c >> 5] & (1u << (c & 31)))) continue;
-                uint64_t h = ((uint64_t)t << 32) | order_desc(r.v);
-                uint32_t l = c * (uint32_t)HW + (uint32_t)p;
+                const uint64_t h = ((uint64_t)t << 32) | order_desc(r.v);
+                const uint32_t l = c * (uint32_t)HW + (uint32_t)p;
                 if (h < hi || (h == hi && l < lo)) {
                     hi = h;
                     lo = l;
@@ -128,12 +174,12 @@ __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__
             const size_t base = (size_t)b * a.C * HW;
             const int n = a.C * HW;
             for (int i = threadIdx.x; i < n; i += blockDim.x) {
-                int c = i / HW, p = i - c * HW;
+                const int c = i / HW, p = i - c * HW;
                 if (pos_dead[p >> 5] & (1u << (p & 31))) continue;
                 if (map_dead[c >> 5] & (1u << (c & 31))) continue;
-                uint32_t t = times[base + i];
+                const uint32_t t = times[base + i];
                 if (!a.readout && t == (uint32_t)spk::kNever) continue;
-                uint64_t h = ((uint64_t)(a.readout ? 0u : t) << 32) | order_desc(vkey[base + i]);
+                const uint64_t h = ((uint64_t)(a.readout ? 0u : t) << 32) | order_desc(vkey[base + i]);
                 if (h < hi || (h == hi && (uint32_t)i < lo)) {
                     hi = h;
                     lo = (uint32_t)i;
@@ -156,9 +202,9 @@ __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__
         }
         const int r = a.radius, side = 2 * r + 1;
         for (int i = threadIdx.x; i < side * side; i += blockDim.x) {
-            int yy = y - r + i / side, xx = x - r + i % side;
+            const int yy = y - r + i / side, xx = x - r + i % side;
             if (yy >= 0 && yy < a.H && xx >= 0 && xx < a.W) {
-                int q = yy * a.W + xx;
+                const int q = yy * a.W + xx;
                 atomicOr(&pos_dead[q >> 5], 1u << (q & 31));
             }
         }
@@ -207,8 +253,8 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     Rec *recs = (Rec *)ws;
     if (pointwise) {
         const long long total = (long long)B * HW;
-        hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 256)), dim3(256), 0, s, times,
-                           vkey, C, HW, total, recs, inhibited);
+        hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 64)), dim3(64 * kGroups), 0, s,
+                           times, vkey, C, HW, total, recs, inhibited);
         SPK_LAUNCHED("spk_inhibit_winners");
     } else if (inhibited && inhibited != times) {
         SPK_REQUIRE(hipMemcpyAsync(inhibited, times, (size_t)B * C * HW, hipMemcpyDeviceToDevice,
@@ -216,14 +262,15 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
                     SPK_E_HIP, "spk_inhibit_winners: copy of the time map failed");
     }
     WtaArgs a{C, H, W, T, k, radius, readout, pointwise};
-    const size_t lds = ((size_t)(HW + 31) / 32 + (C + 31) / 32) * sizeof(uint32_t);
-    if (k > 0) {
-        hipLaunchKernelGGL(k_select, dim3(B), dim3(kThreads), lds, s, times, vkey, recs, a,
-                           winners, n_winners);
-    } else {
-        hipLaunchKernelGGL(k_select, dim3(B), dim3(64), lds, s, times, vkey, recs, a, winners,
-                           n_winners);
-    }
+    size_t lds = (((size_t)(HW + 31) / 32 + (C + 31) / 32 + 1) & ~(size_t)1) * sizeof(uint32_t);
+    // records re-read every round are staged in LDS when there are several rounds
+    const int stage = pointwise && k > 1 && lds + (size_t)HW * sizeof(Rec) <= 96 * 1024;
+    if (stage) lds += (size_t)HW * sizeof(Rec);
+    if (lds > 64 * 1024)
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_select),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(k_select, dim3(B), dim3(k > 0 ? kThreads : 64), lds, s, times, vkey, recs, a,
+                       stage, winners, n_winners);
     SPK_LAUNCHED("spk_inhibit_winners");
     return SPK_OK;
 }

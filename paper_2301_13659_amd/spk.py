@@ -53,7 +53,7 @@ _SIGNATURES = {
     "spk_dog_filter": ([_P, _I, _I, _I, _I, _P, _I, _I, _P, _P], _I),
     "spk_latency_code_workspace_size": ([_I, _I, _I, _I], _Z),
     "spk_latency_code": ([_P, _I, _I, _I, _I, _I, _F, _I, _P, _P, _P, _Z, _P], _I),
-    "spk_conv_fire_workspace_size": ([_I] * 10, _Z),
+    "spk_conv_fire_workspace_size": ([_I] * 10 + [_F, _I], _Z),
     "spk_conv_fire": ([_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P,
                        _Z, _P], _I),
     "spk_pool": ([_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P], _I),
@@ -191,7 +191,8 @@ def spk_conv_fire(in_times, w, T: int, stride: int = 1, pad: int = 0, theta: flo
         V = torch.empty((B, T, Co, Ho, Wo), dtype=torch.float32, device=dev)
     elif isinstance(potentials, torch.Tensor):
         V = _dev(potentials, torch.float32, "potentials", 5)
-    nbytes = L.spk_conv_fire_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad)
+    nbytes = L.spk_conv_fire_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, float(theta),
+                                            int(V is not None))
     ws = _workspace(nbytes, dev)
     dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
     _check(L.spk_conv_fire(_ptr(in_times), B, T, Ci, Hi, Wi, _ptr(w), dt, Co, Kh, Kw, stride, pad,

@@ -113,3 +113,20 @@ def test_binding_rejects_host_tensors():
     import torch
     with pytest.raises(ValueError):
         spk.spk_pool(torch.zeros((1, 1, 4, 4), dtype=torch.uint8), 2)
+
+
+@pytest.mark.skipif(__import__("torch").cuda.is_available(),
+                    reason="launches with placeholder pointers: only meaningful without a GPU")
+def test_conv_fire_planning_survives_every_layer_shape():
+    # Valid arguments reach the launch (which fails without a device): the
+    # host-side tile planning must not trap on any workload shape.
+    L = spk.load()
+    shapes = [(8, 15, 2, 28, 28, 32, 5, 2, 15.0), (64, 15, 6, 28, 28, 30, 5, 2, 15.0),
+              (64, 15, 30, 14, 14, 250, 3, 1, 10.0), (64, 15, 250, 5, 5, 200, 5, 2, math.inf),
+              (32, 30, 6, 160, 250, 4, 5, 2, 15.0), (32, 30, 4, 26, 41, 20, 17, 0, 42.0),
+              (128, 30, 64, 64, 64, 128, 3, 1, 20.0), (1, 1, 1, 1, 1, 1, 1, 0, 0.5)]
+    for B, T, Ci, H, W, Co, K, pad, theta in shapes:
+        ws = L.spk_conv_fire_workspace_size(B, T, Ci, H, W, Co, K, K, 1, pad, theta, 0)
+        st = L.spk_conv_fire(P1, B, T, Ci, H, W, P1, 0, Co, K, K, 1, pad, theta, P1, P1, None,
+                             P1 if ws else None, ws, None)
+        assert st == spk.SPK_E_HIP, spk.load().spk_last_error()
