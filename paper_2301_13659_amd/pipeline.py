@@ -131,6 +131,17 @@ class Pipeline:
 
 def conv_flops(wl: wls.Workload) -> list:
     """Dense-interface work per conv layer and batch: 2*B*T*Ho*Wo*Co*Ci*Kh*Kw."""
+    return [f for f, _ in conv_work(wl, dense=True)]
+
+
+def conv_work(wl: wls.Workload, dense: bool = False) -> list:
+    """Algorithmic flop per conv layer and batch, with a label.
+
+    A firing layer needs every step's potential to find the first crossing:
+    T dense convolutions of the cumulative frames, 2*B*T*Ho*Wo*Co*Ci*Kh*Kw.
+    A readout layer (infinite threshold) needs only the last step's potential,
+    one dense convolution of the final frame, 2*B*Ho*Wo*Co*Ci*Kh*Kw, unless
+    `dense` asks for the per-step figure of every layer."""
     C, H, W = wl.input_chw()
     res = []
     for kind, s in wl.stages:
@@ -140,6 +151,10 @@ def conv_flops(wl: wls.Workload) -> list:
             continue
         Ho = (H + 2 * s.pad - s.k) // s.stride + 1
         Wo = (W + 2 * s.pad - s.k) // s.stride + 1
-        res.append(2 * wl.batch * wl.T * Ho * Wo * s.co * s.ci * s.k * s.k)
+        one = 2 * wl.batch * Ho * Wo * s.co * s.ci * s.k * s.k
+        if s.readout and not dense:
+            res.append((one, "2*B*Ho*Wo*Co*Ci*Kh*Kw (readout: last step only)"))
+        else:
+            res.append((one * wl.T, "2*B*T*Ho*Wo*Co*Ci*Kh*Kw"))
         C, H, W = s.co, Ho, Wo
     return res
