@@ -2,9 +2,10 @@
 //
 // The filter bank is tiny (at most 8 kernels, K <= 21), so its coefficients
 // are computed on the host and travel by value in the kernel arguments, where
-// every lane reads them as uniform scalar loads.  A 32 x 8 output tile stages
-// the scaled input pixels (u / 255) of its halo in LDS once and evaluates all
-// filters of the launch from there.  Accumulation is float, window row-major,
+// every lane reads them as uniform scalar loads.  A block evaluates one filter
+// on a 32 x 8 output tile: it stages the scaled input pixels (u / 255) of the
+// tile and its halo in LDS, then runs the fully unrolled window of that
+// kernel size.  Accumulation is float, window row-major,
 // no contraction, so every output is reproducible bit for bit (the rank-order
 // coder downstream turns last-bit differences into different spike times).
 #include <cmath>
@@ -47,43 +48,67 @@ void dog_coefficients(int K, double s1, double s2, float *k)
     for (int at = 0; at < K * K; at++) k[at] = (float)(g1[at] / n1 - g2[at] / n2);
 }
 
+// One K x K window, fully unrolled, coefficients and pixels from LDS (the
+// coefficient reads are broadcasts); the sum keeps the row-major order.
+template <int K>
+__device__ __forceinline__ float window(const float *__restrict__ cf, const float *tile, int tw)
+{
+#pragma clang fp contract(off)
+    float acc = 0.0f;
+#pragma unroll
+    for (int i = 0; i < K; i++)
+#pragma unroll
+        for (int j = 0; j < K; j++) {
+            const float prod = cf[i * K + j] * tile[i * tw + j];
+            acc = acc + prod;
+        }
+    return acc;
+}
+
+// Block = one filter on one 32 x 8 output tile of one (sample, channel).
 __global__ __launch_bounds__(kTX *kTY) void k_dog(const uint8_t *__restrict__ img, int C, int H,
                                                   int W, int F, int Ho, int Wo, DogParams p,
                                                   float *__restrict__ out)
 {
 #pragma clang fp contract(off)
     __shared__ float tile[(kTY + kMaxSpan) * (kTX + kMaxSpan)];
+    __shared__ float coef[kMaxK * kMaxK];
     const int bc = blockIdx.z;  // b * C + c
-    const int x0 = blockIdx.x * kTX, y0 = blockIdx.y * kTY;
-    const int span = p.hi - p.lo;
-    const int tw = kTX + span, th = kTY + span;
+    const int fi = blockIdx.y % p.nf, ty = blockIdx.y / p.nf;
+    const int K = p.ks[fi], off = p.off[fi], cbase = p.cbase[fi];
+    const int x0 = blockIdx.x * kTX, y0 = ty * kTY;
+    const int tw = kTX + K - 1, th = kTY + K - 1;
     const uint8_t *src = img + (size_t)bc * H * W;
     const int tid = threadIdx.y * kTX + threadIdx.x;
+    for (int i = tid; i < K * K; i += kTX * kTY) coef[i] = p.coef[cbase + i];
     for (int i = tid; i < tw * th; i += kTX * kTY) {
-        int r = i / tw, q = i - r * tw;
-        int iy = y0 + p.lo + r, ix = x0 + p.lo + q;
-        float v = 0.0f;
-        if (iy >= 0 && iy < H && ix >= 0 && ix < W) v = (float)src[(size_t)iy * W + ix] / 255.0f;
-        tile[i] = v;
+        const int r = i / tw, q = i - r * tw;
+        const int iy = y0 + off + r, ix = x0 + off + q;
+        const bool inside = (unsigned)iy < (unsigned)H && (unsigned)ix < (unsigned)W;
+        const float u = (float)src[inside ? (size_t)iy * W + ix : 0];
+        tile[i] = inside ? u / 255.0f : 0.0f;
     }
     __syncthreads();
     const int x = x0 + threadIdx.x, y = y0 + threadIdx.y;
     if (x >= Wo || y >= Ho) return;
     const int b = bc / C, c = bc - b * C;
-    for (int f = 0; f < p.nf; f++) {
-        const int K = p.ks[f];
-        const float *cf = p.coef + p.cbase[f];
-        const int r0 = threadIdx.y + p.off[f] - p.lo, q0 = threadIdx.x + p.off[f] - p.lo;
-        float acc = 0.0f;
-        for (int i = 0; i < K; i++) {
-            const float *row = tile + (r0 + i) * tw + q0;
-            for (int j = 0; j < K; j++) {
-                float prod = cf[i * K + j] * row[j];
-                acc = acc + prod;
-            }
-        }
-        out[(((size_t)b * C + c) * F + p.fidx[f]) * Ho * Wo + (size_t)y * Wo + x] = acc;
+    const float *cf = coef;
+    const float *t0 = tile + threadIdx.y * tw + threadIdx.x;
+    float acc;
+    switch (K) {
+    case 1: acc = window<1>(cf, t0, tw); break;
+    case 3: acc = window<3>(cf, t0, tw); break;
+    case 5: acc = window<5>(cf, t0, tw); break;
+    case 7: acc = window<7>(cf, t0, tw); break;
+    case 9: acc = window<9>(cf, t0, tw); break;
+    case 11: acc = window<11>(cf, t0, tw); break;
+    case 13: acc = window<13>(cf, t0, tw); break;
+    case 15: acc = window<15>(cf, t0, tw); break;
+    case 17: acc = window<17>(cf, t0, tw); break;
+    case 19: acc = window<19>(cf, t0, tw); break;
+    default: acc = window<21>(cf, t0, tw); break;
     }
+    out[(((size_t)b * C + c) * F + p.fidx[fi]) * Ho * Wo + (size_t)y * Wo + x] = acc;
 }
 
 }  // namespace
@@ -112,6 +137,8 @@ extern "C" spk_status spk_dog_filter(const uint8_t *img, int B, int C, int H, in
     const int Ho = pad < 0 ? H : H + 2 * pad - filters[0].ksize + 1;
     const int Wo = pad < 0 ? W : W + 2 * pad - filters[0].ksize + 1;
     SPK_REQUIRE(Ho > 0 && Wo > 0, SPK_E_SHAPE, "spk_dog_filter: output %dx%d is empty", Ho, Wo);
+    SPK_REQUIRE((long long)spk::ceil_div(Ho, kTY) * kMaxF <= 65535, SPK_E_SHAPE,
+                "spk_dog_filter: output height %d too large", Ho);
     SPK_REQUIRE((long long)B * C <= 65535, SPK_E_SHAPE, "spk_dog_filter: B*C=%lld > 65535",
                 (long long)B * C);
 
@@ -137,7 +164,7 @@ extern "C" spk_status spk_dog_filter(const uint8_t *img, int B, int C, int H, in
             p.nf++;
             f++;
         }
-        dim3 grid(spk::ceil_div(Wo, kTX), spk::ceil_div(Ho, kTY), B * C);
+        dim3 grid(spk::ceil_div(Wo, kTX), spk::ceil_div(Ho, kTY) * p.nf, B * C);
         hipLaunchKernelGGL(k_dog, grid, dim3(kTX, kTY), 0, spk::stream_of(stream), img, C, H, W, F,
                            Ho, Wo, p, out);
         SPK_LAUNCHED("spk_dog_filter");

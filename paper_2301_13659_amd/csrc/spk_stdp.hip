@@ -2,7 +2,7 @@
 // (Spyker §II-F.1 Eq. 4-6, §II-F.2 Eq. 7).
 //
 // Scatter-free: one workgroup owns kernel o.  It gathers, in (sample, slot)
-// order, the winners of map o (a block-wide ordered compaction into LDS), and
+// order, the winners of map o (an ordered ballot compaction into LDS), and
 // every thread accumulates the changes of its synapses over that list in a
 // fixed order, so the float sums are reproducible.  The clamp and the
 // optional half refresh happen once at the end.  At most one winner per
@@ -13,7 +13,7 @@
 
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 1024;
 constexpr int kMaxTaps = 16384;
 constexpr int kMaxCfg = 16;
 
@@ -30,6 +30,36 @@ struct Entry {
     int b, y, x, t, q;
 };
 
+// Sum, from `init`, of the changes of synapse j of map o over the winners
+// first, first + step, ... of the list.  The pre-spike loads do not depend on
+// each other: they are unconditional (clamped index) so several overlap.
+__device__ __forceinline__ float patch_sum(const float *__restrict__ w,
+                                           const uint8_t *__restrict__ in_times, const Entry *list,
+                                           const StdpGeom &g, int o, int taps, int KK, int j,
+                                           int first, int step, int n, float L, float U,
+                                           const float (*rate)[2], const int *stab, float init)
+{
+#pragma clang fp contract(off)
+    const int c = j / KK, r = j - c * KK;
+    const int ky = r / g.Kw, kx = r - ky * g.Kw;
+    const float w0 = w[(size_t)o * taps + j];
+    const float wl = w0 - L, wu = U - w0;
+    float acc = init;
+#pragma unroll 8
+    for (int m = first; m < n; m += step) {
+        const Entry en = list[m];
+        const int iy = en.y * g.stride + ky - g.pad, ix = en.x * g.stride + kx - g.pad;
+        const bool inside = (unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi;
+        const size_t at = inside ? (((size_t)en.b * g.Ci + c) * g.Hi + iy) * g.Wi + ix : 0;
+        const int t_pre = inside ? (int)in_times[at] : spk::kNever;
+        const float a = rate[en.q][t_pre <= en.t ? 0 : 1];
+        float d = a * wl;
+        d = d * wu;
+        acc = acc + (stab[en.q] ? d : a);
+    }
+    return acc;
+}
+
 __global__ __launch_bounds__(kThreads) void k_stdp(float *__restrict__ w, uint16_t *__restrict__ w16,
                                                    const uint8_t *__restrict__ in_times,
                                                    const spk_winner *__restrict__ winners,
@@ -40,61 +70,71 @@ __global__ __launch_bounds__(kThreads) void k_stdp(float *__restrict__ w, uint16
 #pragma clang fp contract(off)
     extern __shared__ float D[];                   // [taps]
     __shared__ Entry list[kThreads];
-    __shared__ int s_scan[kThreads];
+    __shared__ float part[kThreads];
+    __shared__ int wave_cnt[kThreads / 64];
+    __shared__ float s_rate[kMaxCfg][2];           // a_causal, a_anticausal
+    __shared__ int s_stab[kMaxCfg];
     const int o = blockIdx.x;
-    const int taps = g.Ci * g.Kh * g.Kw;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int taps = g.Ci * g.Kh * g.Kw, KK = g.Kh * g.Kw;
     const float L = cfg.c[0].lower, U = cfg.c[0].upper;
+    if (threadIdx.x < cfg.n) {
+        s_rate[threadIdx.x][0] = cfg.c[threadIdx.x].a_causal;
+        s_rate[threadIdx.x][1] = cfg.c[threadIdx.x].a_anticausal;
+        s_stab[threadIdx.x] = cfg.c[threadIdx.x].stabilize;
+    }
     for (int j = threadIdx.x; j < taps; j += blockDim.x) D[j] = 0.0f;
     const int total = g.B * g.k;
     int n_total = 0;
     for (int base = 0; base < total; base += blockDim.x) {
-        // ordered compaction of this chunk's winners of map o
+        // ordered compaction of this chunk's winners of map o: ballot rank
+        // within the wave, wave counts through LDS
         const int i = base + threadIdx.x;
         Entry e{0, 0, 0, 0, 0};
-        int keep = 0;
+        bool keep = false;
         if (i < total) {
-            const int b = i / g.k, s = i - b * g.k;
+            const int b = i / g.k, slot = i - b * g.k;
             const spk_winner wn = winners[i];
             const int q = winner_cfg ? winner_cfg[i] : 0;
-            if (s < n_winners[b] && wn.c == o && q >= 0 && q < cfg.n) {
-                keep = 1;
-                e = Entry{b, wn.y, wn.x, wn.t, q};
-            }
+            keep = slot < n_winners[b] && wn.c == o && q >= 0 && q < cfg.n;
+            e = Entry{b, wn.y, wn.x, wn.t, q};
         }
-        s_scan[threadIdx.x] = keep;
+        const uint64_t m = __ballot(keep);
+        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        if (lane == 0) wave_cnt[wave] = __popcll(m);
         __syncthreads();
-        for (int off = 1; off < (int)blockDim.x; off <<= 1) {
-            int v = threadIdx.x >= off ? s_scan[threadIdx.x - off] : 0;
-            __syncthreads();
-            s_scan[threadIdx.x] += v;
-            __syncthreads();
+        int before = 0, n_chunk = 0;
+#pragma unroll
+        for (int v = 0; v < kThreads / 64; v++) {
+            const int c = wave_cnt[v];
+            before += v < wave ? c : 0;
+            n_chunk += c;
         }
-        const int n_chunk = s_scan[blockDim.x - 1];
-        if (keep) list[s_scan[threadIdx.x] - 1] = e;
+        if (keep) list[before + rank] = e;
         __syncthreads();
-        for (int j = threadIdx.x; j < taps; j += blockDim.x) {
-            const int c = j / (g.Kh * g.Kw), r = j - c * g.Kh * g.Kw;
-            const int ky = r / g.Kw, kx = r - ky * g.Kw;
-            const float w0 = w[(size_t)o * taps + j];
-            float acc = D[j];
-            for (int m = 0; m < n_chunk; m++) {
-                const Entry en = list[m];
-                const int iy = en.y * g.stride + ky - g.pad, ix = en.x * g.stride + kx - g.pad;
-                int t_pre = spk::kNever;
-                if (iy >= 0 && iy < g.Hi && ix >= 0 && ix < g.Wi)
-                    t_pre = in_times[(((size_t)en.b * g.Ci + c) * g.Hi + iy) * g.Wi + ix];
-                const spk_stdp_config &q = cfg.c[en.q];
-                const float a = (t_pre <= en.t) ? q.a_causal : q.a_anticausal;
-                float d;
-                if (q.stabilize) {
-                    float lo = a * (w0 - L);
-                    d = lo * (U - w0);
-                } else {
-                    d = a;
+        if (n_chunk > 0) {
+            // G groups of `taps` threads share the winners (group g takes
+            // winners g, g + G, ...); the G partial sums are added to D in
+            // group order, so the result is the same on every run.
+            const int G = taps <= kThreads / 2 ? min(n_chunk, kThreads / taps) : 1;
+            if (G > 1) {
+                if (threadIdx.x < G * taps) {
+                    const int grp = threadIdx.x / taps, j = threadIdx.x - grp * taps;
+                    part[threadIdx.x] = patch_sum(w, in_times, list, g, o, taps, KK, j, grp, G,
+                                                  n_chunk, L, U, s_rate, s_stab, 0.0f);
                 }
-                acc = acc + d;
+                __syncthreads();
+                for (int j = threadIdx.x; j < taps; j += blockDim.x) {
+                    float acc = D[j];
+                    for (int q = 0; q < G; q++) acc = acc + part[q * taps + j];
+                    D[j] = acc;
+                }
+            } else {
+                for (int j = threadIdx.x; j < taps; j += blockDim.x)
+                    D[j] = patch_sum(w, in_times, list, g, o, taps, KK, j, 0, 1, n_chunk, L, U, s_rate,
+                                     s_stab, D[j]);
             }
-            D[j] = acc;
         }
         n_total += n_chunk;
         __syncthreads();

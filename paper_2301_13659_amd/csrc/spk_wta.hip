@@ -5,10 +5,12 @@
 // keeps the earliest neuron (then the higher potential, then the lower map).
 // Its survivor is written as an 8-byte record (time|map, potential) to the
 // workspace, and optionally the inhibited time map.  Winner selection then
-// runs one workgroup per sample: up to k rounds of a block-wide arg-min over
-// the surviving records, with the suppressed maps and locations kept as bit
-// sets in LDS.  Readout layers (no threshold) and calls without pointwise
-// inhibition rank the neurons themselves instead of per-location records.
+// runs one workgroup per sample: up to k greedy rounds of an arg-min over the
+// surviving records.  Up to 8192 candidates per sample stay in registers;
+// larger maps keep the suppressed maps and locations as bit sets in LDS and
+// sweep the records each round.  Readout layers (no threshold) and calls
+// without pointwise inhibition rank the neurons themselves instead of
+// per-location records.
 #include "spk_internal.h"
 
 namespace {
@@ -59,11 +61,12 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
     int bt = spk::kNever, bc = -1;
     float bv = 0.0f;
     if (ok) {
+        // unconditional loads, so that the unrolled iterations overlap
+#pragma unroll 4
         for (int c = grp; c < C; c += kGroups) {
             const int t = times[base + (size_t)c * HW];
-            if (t == spk::kNever || t > bt) continue;
             const float v = vkey[base + (size_t)c * HW];
-            if (t < bt || v > bv) {
+            if (t != spk::kNever && (t < bt || (t == bt && v > bv))) {
                 bt = t;
                 bv = v;
                 bc = c;
@@ -216,6 +219,128 @@ __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__
     if (threadIdx.x == 0) n_winners[b] = count;
 }
 
+// Winner selection with the candidates of one sample held in registers: NW
+// waves, NPL candidates per thread (candidate i at thread i % (64*NW), slot
+// i / (64*NW)).  A round is a register arg-min, a wave shuffle reduction and,
+// with several waves, one exchange through LDS; the lane that owns the
+// winner writes it, and every lane retires its own candidates that share the
+// winner's map or lie in its window.
+template <int NPL, int NW>
+__global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restrict__ times,
+                                                        const float *__restrict__ vkey,
+                                                        const Rec *__restrict__ recs, WtaArgs a,
+                                                        spk_winner *__restrict__ winners,
+                                                        int32_t *__restrict__ n_winners)
+{
+    __shared__ uint64_t s_hi[2][NW];
+    __shared__ uint32_t s_lo[2][NW];
+    const int b = blockIdx.x;
+    const int HW = a.H * a.W;
+    const int n = a.by_record ? HW : a.C * HW;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint64_t kNone = ~0ull;
+    uint64_t kh[NPL];
+    uint32_t kl[NPL];
+    int cc[NPL], yx[NPL];
+    float vv[NPL];
+#pragma unroll
+    for (int j = 0; j < NPL; j++) {
+        const int i = tid + j * 64 * NW;
+        const bool in = i < n;
+        const int ii = in ? i : 0;
+        int t, c, pos;
+        float v;
+        if (a.by_record) {
+            const Rec r = recs[(size_t)b * HW + ii];
+            t = (int)(r.tc >> 24);
+            c = (int)(r.tc & 0xFFFFFFu);
+            pos = ii;
+            v = r.v;
+        } else {
+            const size_t at = (size_t)b * a.C * HW + ii;
+            t = times[at];
+            v = vkey[at];
+            c = ii / HW;
+            pos = ii - c * HW;
+        }
+        const bool alive = in && (a.readout || t != spk::kNever);
+        const uint32_t tk = a.readout ? 0u : (uint32_t)t;
+        kh[j] = alive ? (((uint64_t)tk << 32) | order_desc(v)) : kNone;
+        kl[j] = (uint32_t)c * (uint32_t)HW + (uint32_t)pos;
+        cc[j] = c;
+        const int y = pos / a.W;
+        yx[j] = (y << 16) | (pos - y * a.W);
+        vv[j] = v;
+    }
+    int count = 0;
+    for (int round = 0; round < a.k; round++) {
+        uint64_t bh = kNone;
+        uint32_t bl = ~0u;
+#pragma unroll
+        for (int j = 0; j < NPL; j++)
+            if (kh[j] < bh || (kh[j] == bh && kl[j] < bl)) {
+                bh = kh[j];
+                bl = kl[j];
+            }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const uint64_t h2 = __shfl_xor(bh, o, 64);
+            const uint32_t l2 = __shfl_xor(bl, o, 64);
+            if (h2 < bh || (h2 == bh && l2 < bl)) {
+                bh = h2;
+                bl = l2;
+            }
+        }
+        if (NW > 1) {
+            const int slot = round & 1;
+            if (lane == 0) {
+                s_hi[slot][wave] = bh;
+                s_lo[slot][wave] = bl;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int w = 0; w < NW; w++) {
+                const uint64_t h2 = s_hi[slot][w];
+                const uint32_t l2 = s_lo[slot][w];
+                if (h2 < bh || (h2 == bh && l2 < bl)) {
+                    bh = h2;
+                    bl = l2;
+                }
+            }
+        }
+        if (bh == kNone) break;
+        const int wc = (int)(bl / (uint32_t)HW), wp = (int)(bl - (uint32_t)wc * (uint32_t)HW);
+        const int wy = wp / a.W, wx = wp - wy * a.W;
+#pragma unroll
+        for (int j = 0; j < NPL; j++) {
+            if (kh[j] == bh && kl[j] == bl) {
+                spk_winner wn;
+                wn.c = wc;
+                wn.y = wy;
+                wn.x = wx;
+                wn.t = a.readout ? a.T - 1 : (int)(bh >> 32);
+                wn.v = vv[j];
+                winners[(size_t)b * a.k + count] = wn;
+            }
+            const int dy = (yx[j] >> 16) - wy, dx = (yx[j] & 0xFFFF) - wx;
+            const bool near = dy <= a.radius && -dy <= a.radius && dx <= a.radius && -dx <= a.radius;
+            if (cc[j] == wc || near) kh[j] = kNone;
+        }
+        count++;
+    }
+    for (int s = count + tid; s < a.k; s += 64 * NW)
+        winners[(size_t)b * a.k + s] = spk_winner{-1, -1, -1, -1, 0.0f};
+    if (tid == 0) n_winners[b] = count;
+}
+
+template <int NPL, int NW>
+void launch_select_reg(int B, hipStream_t s, const uint8_t *times, const float *vkey,
+                       const Rec *recs, const WtaArgs &a, spk_winner *winners, int32_t *n_winners)
+{
+    hipLaunchKernelGGL((k_select_reg<NPL, NW>), dim3(B), dim3(64 * NW), 0, s, times, vkey, recs, a,
+                       winners, n_winners);
+}
+
 }  // namespace
 
 extern "C" size_t spk_inhibit_winners_workspace_size(int B, int C, int H, int W)
@@ -262,6 +387,24 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
                     SPK_E_HIP, "spk_inhibit_winners: copy of the time map failed");
     }
     WtaArgs a{C, H, W, T, k, radius, readout, pointwise};
+    // candidates per sample: one record per location after pointwise
+    // inhibition, else every neuron
+    const long long n_cand = pointwise ? (long long)HW : (long long)C * HW;
+    if (k > 0 && n_cand <= 64 * 4) {
+        launch_select_reg<4, 1>(B, s, times, vkey, recs, a, winners, n_winners);
+    } else if (k > 0 && n_cand <= 64 * 16) {
+        launch_select_reg<16, 1>(B, s, times, vkey, recs, a, winners, n_winners);
+    } else if (k > 0 && n_cand <= 256 * 16) {
+        launch_select_reg<16, 4>(B, s, times, vkey, recs, a, winners, n_winners);
+    } else if (k > 0 && n_cand <= 256 * 20) {
+        launch_select_reg<20, 4>(B, s, times, vkey, recs, a, winners, n_winners);
+    } else if (k > 0 && n_cand <= 512 * 16) {
+        launch_select_reg<16, 8>(B, s, times, vkey, recs, a, winners, n_winners);
+    }
+    if (k > 0 && n_cand <= 512 * 16) {
+        SPK_LAUNCHED("spk_inhibit_winners");
+        return SPK_OK;
+    }
     size_t lds = (((size_t)(HW + 31) / 32 + (C + 31) / 32 + 1) & ~(size_t)1) * sizeof(uint32_t);
     // records re-read every round are staged in LDS when there are several rounds
     const int stage = pointwise && k > 1 && lds + (size_t)HW * sizeof(Rec) <= 96 * 1024;

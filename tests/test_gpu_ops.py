@@ -198,6 +198,8 @@ def test_inhibit_wta_hand_example():
     (3, 30, 9, 11, 40, 0, 0.3, "pointwise"), (3, 6, 7, 5, 4, 1, 0.3, "fired"),
     (4, 200, 5, 5, 1, 0, 0.0, "readout"), (2, 20, 6, 6, 5, 1, 0.0, "readout"),
     (2, 8, 8, 8, 0, 1, 0.3, "pointwise"), (2, 5, 6, 6, 3, 1, 0.0, "pointwise"),
+    (2, 6, 80, 90, 6, 2, 0.05, "pointwise"), (2, 12, 20, 30, 7, 1, 0.2, "fired"),
+    (2, 40, 16, 16, 3, 1, 0.0, "readout"),
 ])
 def test_inhibit_wta_matches_oracle(B, C, H, W, k, r, dens, mode):
     dev = gpu()
@@ -253,6 +255,7 @@ def test_stdp_hand_example():
     (32, 2, 5, 1, 2, 8, 28, 5, 1, 1), (250, 30, 3, 1, 1, 16, 14, 8, 1, 1),
     (200, 250, 5, 1, 2, 64, 5, 1, 1, 2), (20, 4, 17, 1, 0, 6, 26, 1, 1, 1),
     (128, 64, 3, 1, 1, 8, 64, 16, 1, 1), (7, 3, 3, 2, 1, 300, 9, 3, 0, 2),
+    (5, 8, 3, 1, 1, 400, 12, 3, 1, 2), (3, 30, 5, 1, 2, 200, 10, 2, 1, 1),
 ])
 def test_stdp_matches_oracle(Co, Ci, K, s, p, B, H, k, stab, ncfg):
     dev = gpu()
