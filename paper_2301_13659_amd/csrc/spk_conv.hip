@@ -1,12 +1,17 @@
 // spk_conv_fire: spiking convolution + integrate-and-fire (Spyker §II-E.1, Eq. 2).
 //
-// Shapes the matrix-core kernels cover (spk_conv_mfma.hip) go there.  The
-// rest (firing layers with more than 1536 taps) take the direct form below:
+// Dispatch: firing layers whose weights fit the registers of a wave (see
+// spk_conv_fast.hip), with T <= 32 and no dense potentials requested, run the
+// register-resident kernels there; other shapes the matrix-core kernels of
+// spk_conv_mfma.hip cover (readout layers and the dense-potential mode among
+// them) go there; the rest take the direct form below:
 // one thread per output neuron (b, o, y, x) walks the time steps, sums the
 // weights of the inputs of its window that have fired by step t (the
 // cumulative frame S_t = [time <= t]) and records the first step whose
 // potential exceeds theta.  Kernel o's weights are staged in LDS as float.
 #include <hip/hip_fp16.h>
+
+#include <algorithm>
 
 #include "spk_internal.h"
 
@@ -77,10 +82,16 @@ extern "C" size_t spk_conv_fire_workspace_size(int B, int T, int Ci, int Hi, int
                                                int Kh, int Kw, int stride, int pad, float theta,
                                                int potentials)
 {
-    (void)T;
     const int Ho = spk_out_extent(Hi, Kh, stride, pad), Wo = spk_out_extent(Wi, Kw, stride, pad);
     if (B <= 0 || Ci <= 0 || Co <= 0 || Ho <= 0 || Wo <= 0) return 0;
-    return spk::conv_mfma_workspace(B, Ho, Wo, Co, Ci * Kh * Kw, is_readout(theta, potentials != 0));
+    const bool readout = is_readout(theta, potentials != 0);
+    size_t need = spk::conv_mfma_workspace(B, Ho, Wo, Co, Ci * Kh * Kw, readout);
+    // the channels-last path is open to half weights on more shapes than to
+    // float ones, and its workspace does not depend on the weight type
+    if (spk::conv_fast_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, true, readout,
+                                 potentials != 0))
+        need = std::max(need, spk::conv_fast_workspace(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo));
+    return need;
 }
 
 extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int Hi, int Wi,
@@ -113,6 +124,10 @@ extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int C
                 "spk_conv_fire: workspace of %zu bytes needed, %zu given", need, ws_bytes);
     SPK_REQUIRE((long long)B * Ho * Wo < (1LL << 31) && (long long)Ci * Hi * Wi < (1LL << 31),
                 SPK_E_SHAPE, "spk_conv_fire: layer too large");
+    if (spk::conv_fast_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, half_w, readout,
+                                 potentials != nullptr))
+        return spk::conv_fire_fast(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho,
+                                   Wo, theta, out_times, out_vkey, ws, spk::stream_of(stream));
     if (spk::conv_mfma_supported(Ci, Kh, Kw, Co, half_w, readout))
         return spk::conv_fire_mfma(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho,
                                    Wo, theta, out_times, out_vkey, potentials, ws,

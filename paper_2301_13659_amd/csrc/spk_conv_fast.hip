@@ -1,0 +1,868 @@
+// spk_conv_fire, firing layers on the matrix cores with register-resident
+// operands (Spyker §II-E.1 Eq. 2, first-spike firing of §II-D.3).
+//
+// Two small passes first rewrite the operands into the order the MFMA
+// fragments consume (both in the caller's workspace):
+//
+//  - the time map becomes padded channels-last: Xp[b][iy][ix][c] over the
+//    zero-padded extent (Hi + 2 pad) x (Wi + 2 pad), padding = 255 (never
+//    fires).  For a fixed kernel row ky, the taps (kx, c) of an output
+//    position are then one contiguous run of Kw*Ci bytes;
+//  - the depth K is ordered (ky, j) with j = kx*Ci + c, each run padded to a
+//    multiple of 8 (R8), so the 8 taps of a fragment lane are 8 consecutive
+//    bytes of Xp.  The weights are packed in that order as ready B fragments
+//    (hi/lo halves of the float master, or the half weights), zero on the
+//    padding taps, so padding bytes never matter.
+//
+// The firing kernel: a block of 4 waves owns one column tile (16 maps); each
+// wave keeps the B fragments of all its K subtiles in registers for the whole
+// block.  The block walks row groups (4 waves x R row tiles of 16 positions):
+// it stages the contiguous Xp byte range of the group in LDS, every wave pulls
+// the 8 time bytes of each of its A fragments into registers, then runs the
+// T steps on registers only.  A step either recomputes the potential from the
+// cumulative frame, V_t = W * [time <= t] (two packed-half operations per pair
+// of taps), or, when the wave's inputs arrive sparsely, adds the newly
+// arriving spikes, V_t = V_{t-1} + W * [time == t], skipping subtiles with no
+// arrival.  After each step the crossings of theta are recorded in registers;
+// times and potentials are written once at the end.
+#include <hip/hip_fp16.h>
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <tuple>
+
+#include "spk_internal.h"
+
+namespace {
+
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kSlack = 64;                  // readable bytes past the end of Xp / the halo
+constexpr int kHaloMax = 48 * 1024;         // LDS bytes for a staged row group
+constexpr uint32_t kSelLo = 0x04010400u;    // bytes 0,1 -> halves 1024 + b
+constexpr uint32_t kSelHi = 0x04030402u;    // bytes 2,3 -> halves 1024 + b
+
+struct FGeom {
+    int B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo;
+    int Hp, Wp;  // padded input extent
+    int run;     // Kw*Ci: bytes of one kernel row's taps
+    int R8;      // run rounded up to a multiple of 8
+    int K;       // Kh*R8: packed depth
+    int S;       // ceil(K / 32): MFMA subtiles
+    int P;       // B*Ho*Wo: output positions
+    int NT;      // ceil(Co / 16): column tiles
+    int rowb;    // Wp*Ci: bytes of one padded input row
+    int S16;     // ceil(K / 16): subtiles of the 32x32x16 kernel
+    int NT32;    // ceil(Co / 32): its column tiles
+};
+
+FGeom make_geom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride, int pad,
+                int Ho, int Wo)
+{
+    FGeom g{};
+    g.B = B; g.T = T; g.Ci = Ci; g.Hi = Hi; g.Wi = Wi; g.Co = Co; g.Kh = Kh; g.Kw = Kw;
+    g.stride = stride; g.pad = pad; g.Ho = Ho; g.Wo = Wo;
+    g.Hp = Hi + 2 * pad;
+    g.Wp = Wi + 2 * pad;
+    g.run = Kw * Ci;
+    g.R8 = (g.run + 7) / 8 * 8;
+    g.K = Kh * g.R8;
+    g.S = (g.K + 31) / 32;
+    g.P = B * Ho * Wo;
+    g.NT = (Co + 15) / 16;
+    g.rowb = g.Wp * Ci;
+    g.S16 = (g.K + 15) / 16;
+    g.NT32 = (Co + 31) / 32;
+    return g;
+}
+
+size_t xp_bytes(const FGeom &g)
+{
+    return spk::align_up((size_t)g.B * g.Hp * g.rowb + kSlack, 256);
+}
+
+// B fragment bytes for either fragment shape (the larger of the two).
+size_t bp_bytes(const FGeom &g, int np)
+{
+    const size_t a = (size_t)g.NT * g.S, b = (size_t)g.NT32 * g.S16;
+    return (a > b ? a : b) * np * 64 * sizeof(h8);
+}
+
+__device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
+__device__ __forceinline__ uint32_t as_u(h2 h) { return __builtin_bit_cast(uint32_t, h); }
+
+// [t <= last] for two time bytes, as halves (c = 1025 + last in both halves):
+// c - (1024 + t) is a small exact integer, >= 1 iff t <= last.
+__device__ __forceinline__ uint32_t upto2(uint32_t x, uint32_t sel, h2 c)
+{
+    const h2 one = {(_Float16)1.0f, (_Float16)1.0f}, zero = {(_Float16)0.0f, (_Float16)0.0f};
+    h2 a = c - as_h2(__builtin_amdgcn_perm(0x64646464u, x, sel));
+    return as_u(__builtin_elementwise_min(__builtin_elementwise_max(a, zero), one));
+}
+
+// [t == tau] for two time bytes (c = 1024 + tau): 1 - d^2 is 1 at d == 0 and
+// <= 0 elsewhere.
+__device__ __forceinline__ uint32_t arrive2(uint32_t x, uint32_t sel, h2 c)
+{
+    const h2 one = {(_Float16)1.0f, (_Float16)1.0f}, zero = {(_Float16)0.0f, (_Float16)0.0f};
+    h2 d = as_h2(__builtin_amdgcn_perm(0x64646464u, x, sel)) - c;
+    h2 a = one - d * d;
+    return as_u(__builtin_elementwise_min(__builtin_elementwise_max(a, zero), one));
+}
+
+__device__ __forceinline__ h8 frag_upto(uint2 x, h2 c)
+{
+    u4 v = {upto2(x.x, kSelLo, c), upto2(x.x, kSelHi, c), upto2(x.y, kSelLo, c), upto2(x.y, kSelHi, c)};
+    return __builtin_bit_cast(h8, v);
+}
+
+__device__ __forceinline__ h8 frag_arrive(uint2 x, h2 c)
+{
+    u4 v = {arrive2(x.x, kSelLo, c), arrive2(x.x, kSelHi, c), arrive2(x.y, kSelLo, c),
+            arrive2(x.y, kSelHi, c)};
+    return __builtin_bit_cast(h8, v);
+}
+
+// 8 bytes at any byte offset of LDS, from three aligned dwords.
+__device__ __forceinline__ uint2 lds_read8(const uint8_t *base, int at)
+{
+    const uint32_t *w = reinterpret_cast<const uint32_t *>(base + (at & ~3));
+    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2];
+    const uint32_t sh = (uint32_t)(at & 3);
+    return make_uint2(__builtin_amdgcn_alignbyte(w1, w0, sh), __builtin_amdgcn_alignbyte(w2, w1, sh));
+}
+
+// OR over the 64 lanes of a wave, with row shifts and row broadcasts (DPP)
+// rather than LDS permutes; every lane gets the result.
+__device__ __forceinline__ uint32_t wave_or(uint32_t x)
+{
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+// Sum over the 64 lanes of a wave (DPP, as wave_or).
+__device__ __forceinline__ int wave_sum(int x)
+{
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);
+    return __builtin_amdgcn_readlane(x, 63);
+}
+
+// Number of the 4 time bytes of x below T.
+__device__ __forceinline__ int spikes4(uint32_t x, int T)
+{
+    int n = 0;
+#pragma unroll
+    for (int e = 0; e < 4; e++) n += ((x >> (8 * e)) & 0xFFu) < (uint32_t)T ? 1 : 0;
+    return n;
+}
+
+// Bit t for each of the 8 time bytes, with every time >= 31 (late or never)
+// folded onto bit 31; the caller keeps bits below T.
+__device__ __forceinline__ uint32_t time_bits(uint2 x)
+{
+    uint32_t m = 0u;
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+        const uint32_t t = ((e < 4 ? x.x : x.y) >> (8 * (e & 3))) & 0xFFu;
+        m |= 1u << min(t, 31u);
+    }
+    return m;
+}
+
+// ------------------------------------------------------------------ packing
+
+// Blocks [0, nb_in): padded channels-last time map, one thread per Xp byte.
+// Blocks [nb_in, ...): B fragments, one thread per (column tile, subtile,
+// lane), 8 taps each, as hi/lo halves (NP = 2) or halves (NP = 1).
+// kBig: fragments of the 32x32x16 shape (lane: map l % 32, taps 8*(l/32)..+7
+// of a 16-tap subtile), else of the 16x16x32 shape (map l % 16, taps
+// 8*(l/16)..+7 of a 32-tap subtile).
+template <int NP, bool kHalfW, bool kBig>
+__global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
+                                              const void *__restrict__ wv, FGeom g, int nb_in,
+                                              uint8_t *__restrict__ xp, h8 *__restrict__ bp)
+{
+    if ((int)blockIdx.x < nb_in) {
+        // sizes below 2^31 (checked on the host)
+        const uint32_t n = (uint32_t)g.B * g.Hp * g.rowb;
+        const uint32_t e = blockIdx.x * 256u + threadIdx.x;
+        if (e >= n + kSlack) return;
+        uint8_t v = (uint8_t)spk::kNever;
+        if (e < n) {
+            const uint32_t pix = e / g.Ci, c = e - pix * g.Ci;
+            const uint32_t prow = pix / g.Wp, px = pix - prow * g.Wp;
+            const uint32_t b = prow / g.Hp, py = prow - b * g.Hp;
+            const int iy = (int)py - g.pad, ix = (int)px - g.pad;
+            if ((unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi)
+                v = in[(((size_t)b * g.Ci + c) * g.Hi + iy) * g.Wi + ix];
+        }
+        xp[e] = v;
+        return;
+    }
+    const int NS = kBig ? g.S16 : g.S;
+    const long long f = (long long)(blockIdx.x - nb_in) * 256 + threadIdx.x;
+    if (f >= (long long)(kBig ? g.NT32 : g.NT) * NS * 64) return;
+    const int lane = (int)(f & 63);
+    const long long ts = f >> 6;
+    const int s = (int)(ts % NS), nt = (int)(ts / NS);
+    const int o = kBig ? nt * 32 + (lane & 31) : nt * 16 + (lane & 15);
+    const int kb = kBig ? (s * 2 + (lane >> 5)) * 8 : (s * 4 + (lane >> 4)) * 8;
+    h8 hi, lo;
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+        const int k = kb + e, ky = k / g.R8, j = k - ky * g.R8;
+        float w = 0.0f;
+        if (o < g.Co && ky < g.Kh && j < g.run) {
+            const int kx = j / g.Ci, c = j - kx * g.Ci;
+            const size_t at = (((size_t)o * g.Ci + c) * g.Kh + ky) * g.Kw + kx;
+            w = kHalfW ? (float)reinterpret_cast<const _Float16 *>(wv)[at]
+                       : reinterpret_cast<const float *>(wv)[at];
+        }
+        const _Float16 h = (_Float16)w;
+        hi[e] = h;
+        lo[e] = (_Float16)(w - (float)h);
+    }
+    bp[(size_t)(ts * NP) * 64 + lane] = hi;
+    if (NP == 2) bp[(size_t)(ts * NP + 1) * 64 + lane] = lo;
+}
+
+// -------------------------------------------------------------------- firing
+
+// Byte range of Xp holding the input rows of output positions [p0, p1].
+__host__ __device__ inline void group_range(const FGeom &g, int p0, int p1, long long &h0,
+                                            long long &h1)
+{
+    const int HoWo = g.Ho * g.Wo;
+    const int b0 = p0 / HoWo, y0 = (p0 - b0 * HoWo) / g.Wo;
+    const int b1 = p1 / HoWo, y1 = (p1 - b1 * HoWo) / g.Wo;
+    h0 = ((long long)b0 * g.Hp + (long long)y0 * g.stride) * g.rowb;
+    h1 = ((long long)b1 * g.Hp + (long long)y1 * g.stride + g.Kh) * g.rowb;
+}
+
+// SM: the layer's subtile count (exact); kR: row tiles per wave.
+template <int SM, int NP, int kR>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void k_fire_fast(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g, float theta,
+                 int iters, int vec_store, uint8_t *__restrict__ out_t, float *__restrict__ out_v)
+{
+    constexpr int kRows = kWaves * kR * 16;  // positions per block iteration
+    extern __shared__ __align__(16) uint8_t halo[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nt = blockIdx.y;
+    const int o = nt * 16 + (lane & 15);
+    const int HoWo = g.Ho * g.Wo;
+    const int Q8 = g.R8 / 8;  // fragment octets per kernel row
+
+    // Xp offset of each lane group's octet in each subtile (relative to the
+    // row's window origin), once per block: kernel row ky, byte j0 of its run
+    __shared__ int s_off[SM * 4];
+    __shared__ uint32_t s_bits[kWaves];
+    __shared__ int s_count[kWaves];
+    if (threadIdx.x < SM * 4) {
+        const int q = threadIdx.x;  // = s * 4 + lane group
+        const int ky = q / Q8, jq = q - ky * Q8;
+        s_off[q] = (ky < g.Kh ? ky : 0) * g.rowb + jq * 8;  // octets past K: any byte (B is zero)
+    }
+
+    // B fragments of the column tile, all subtiles, in registers
+    h8 bw[SM][NP];
+#pragma unroll
+    for (int s = 0; s < SM; s++) {
+#pragma unroll
+        for (int q = 0; q < NP; q++) bw[s][q] = bp[((size_t)(nt * SM + s) * NP + q) * 64 + lane];
+    }
+
+    for (int it = 0; it < iters; it++) {
+        const int pb0 = (blockIdx.x * iters + it) * kRows;
+        if (pb0 >= g.P) break;
+        const int pb1 = min(g.P, pb0 + kRows) - 1;
+        long long h0, h1;
+        group_range(g, pb0, pb1, h0, h1);
+        const long long a0 = h0 & ~15ll;
+        const int nvec = (int)((h1 - a0 + 15) >> 4) + 1;  // 16-byte words, one past the end
+        __syncthreads();  // the previous group's halo is no longer read
+        // copy the group's Xp bytes, noting which steps they fire at and how
+        // many of them fire at all (over a superset of the group's taps)
+        const uint32_t tmask = g.T >= 32 ? ~0u : ((1u << g.T) - 1u);
+        {
+            const uint4 *src = reinterpret_cast<const uint4 *>(xp + a0);
+            uint4 *dst = reinterpret_cast<uint4 *>(halo);
+            uint32_t hb = 0u;
+            int hc = 0;
+            for (int i = threadIdx.x; i < nvec; i += kThreads) {
+                const uint4 v = src[i];
+                dst[i] = v;
+                hb |= time_bits(make_uint2(v.x, v.y)) | time_bits(make_uint2(v.z, v.w));
+                hc += spikes4(v.x, g.T);  // density from a quarter of the bytes
+            }
+            hb = wave_or(hb);
+            hc = wave_sum(hc);
+            if (lane == 0) {
+                s_bits[wave] = hb;
+                s_count[wave] = hc;
+            }
+        }
+        __syncthreads();
+        uint32_t all = 0u;
+        int spikes = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; w++) {
+            all |= s_bits[w];
+            spikes += s_count[w];
+        }
+        all &= tmask;
+        const int tmin = all ? __builtin_ctz(all) : g.T;
+        const int tmax = all ? 31 - __builtin_clz(all) : -1;
+        const int span = tmax >= tmin ? tmax - tmin + 1 : 1;
+        // Expected arrivals per (step, subtile) of a wave: 16*kR rows x 32 taps
+        // at the group's spike density, spread over the active steps.  Below
+        // about one, enough subtiles are empty at a step for the arrival form
+        // (1.5x the work of a cumulative step per computed subtile) to win.
+        const float lambda = (float)(16 * kR * 32) * (float)spikes / ((float)nvec * 4.0f * (float)span);
+        const bool delta = lambda < 1.1f;
+
+        // ---- A side: 8 time bytes per (row tile, subtile) into registers
+        uint2 ab[kR][SM];
+#pragma unroll
+        for (int r = 0; r < kR; r++) {
+            const int p = pb0 + (wave * kR + r) * 16 + (lane & 15);
+            const int pc = min(p, g.P - 1);
+            const int b = pc / HoWo, rem = pc - b * HoWo;
+            const int y = rem / g.Wo, x = rem - y * g.Wo;
+            const int base = (int)(((long long)b * g.Hp + (long long)y * g.stride) * g.rowb +
+                                   (long long)x * g.stride * g.Ci - a0);
+#pragma unroll
+            for (int s = 0; s < SM; s++) ab[r][s] = lds_read8(halo, base + s_off[s * 4 + (lane >> 4)]);
+        }
+        // Arrival-time masks per subtile, OR over the wave, for the arrival
+        // form only.  A mask may hold extra bits (padding taps, late times
+        // folded onto bit 31 when T == 32): an extra subtile adds zeros.
+        uint32_t ms[SM];
+#pragma unroll
+        for (int s = 0; s < SM; s++) ms[s] = 0u;
+        if (delta) {
+#pragma unroll
+            for (int s = 0; s < SM; s++) {
+                uint32_t m = 0u;
+#pragma unroll
+                for (int r = 0; r < kR; r++) m |= time_bits(ab[r][s]);
+                ms[s] = wave_or(m) & tmask;
+            }
+        }
+
+        uint32_t valid = 0u;
+#pragma unroll
+        for (int r = 0; r < kR; r++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int p = pb0 + (wave * kR + r) * 16 + (lane >> 4) * 4 + i;
+                if (p < g.P && o < g.Co) valid |= 1u << (r * 4 + i);
+            }
+        // Fired and valid neurons, as lane masks per accumulator element
+        // (scalar registers); the per-lane times and key potentials are only
+        // touched at steps where something new fires.
+        uint64_t vmask[kR * 4], fmask[kR * 4];
+#pragma unroll
+        for (int e = 0; e < kR * 4; e++) {
+            vmask[e] = __ballot((valid >> e) & 1u);
+            fmask[e] = 0ull;
+        }
+        uint32_t tf[kR] = {};
+        float vk[kR][4] = {};
+        f4 acc[kR];
+#pragma unroll
+        for (int r = 0; r < kR; r++) acc[r] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        for (int tau = 0; tau < g.T; tau++) {
+            if (delta) {
+                const uint32_t cb = 0x6400u + (uint32_t)tau;  // half 1024 + tau
+                const h2 cc = as_h2(cb | (cb << 16));
+#pragma unroll
+                for (int s = 0; s < SM; s++) {
+                    if ((ms[s] >> tau) & 1u) {
+                        h8 a[kR];
+#pragma unroll
+                        for (int r = 0; r < kR; r++) a[r] = frag_arrive(ab[r][s], cc);
+#pragma unroll
+                        for (int q = 0; q < NP; q++)
+#pragma unroll
+                            for (int r = 0; r < kR; r++)
+                                acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[r], bw[s][q], acc[r], 0, 0, 0);
+                    }
+                }
+            } else if (tau >= tmin && tau <= tmax) {
+                const uint32_t cb = 0x6401u + (uint32_t)tau;  // half 1025 + tau
+                const h2 cc = as_h2(cb | (cb << 16));
+#pragma unroll
+                for (int r = 0; r < kR; r++) acc[r] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int s = 0; s < SM; s++) {
+                    h8 a[kR];
+#pragma unroll
+                    for (int r = 0; r < kR; r++) a[r] = frag_upto(ab[r][s], cc);
+#pragma unroll
+                    for (int q = 0; q < NP; q++)
+#pragma unroll
+                        for (int r = 0; r < kR; r++)
+                            acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[r], bw[s][q], acc[r], 0, 0, 0);
+                }
+            }
+            // crossings of theta at this step (first crossing only)
+            uint64_t any = 0ull, nm[kR * 4];
+#pragma unroll
+            for (int r = 0; r < kR; r++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const int e = r * 4 + i;
+                    nm[e] = __ballot(acc[r][i] > theta) & vmask[e] & ~fmask[e];
+                    any |= nm[e];
+                }
+            if (any) {
+                const uint64_t me = 1ull << lane;
+#pragma unroll
+                for (int r = 0; r < kR; r++)
+#pragma unroll
+                    for (int i = 0; i < 4; i++) {
+                        const int e = r * 4 + i;
+                        if (nm[e] & me) {
+                            vk[r][i] = acc[r][i];
+                            tf[r] = (tf[r] & ~(0xFFu << (8 * i))) | ((uint32_t)tau << (8 * i));
+                        }
+                        fmask[e] |= nm[e];
+                    }
+            }
+            if (tau >= tmax) break;  // no later arrival: the potentials stay as they are
+        }
+        uint32_t fired = 0u;
+#pragma unroll
+        for (int e = 0; e < kR * 4; e++) fired |= ((fmask[e] >> lane) & 1ull) ? (1u << e) : 0u;
+
+        // times and key potentials: t_f and V[t_f], or NEVER and V[T-1]
+#pragma unroll
+        for (int r = 0; r < kR; r++) {
+            uint32_t tb = 0u;
+            float v[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const bool f = (fired >> (r * 4 + i)) & 1u;
+                v[i] = f ? vk[r][i] : acc[r][i];
+                tb |= (f ? ((tf[r] >> (8 * i)) & 0xFFu) : (uint32_t)spk::kNever) << (8 * i);
+            }
+            const int p0 = pb0 + (wave * kR + r) * 16 + (lane >> 4) * 4;
+            if (vec_store) {
+                // 4 positions of one sample, 4-aligned (Ho*Wo % 4 == 0)
+                if ((valid >> (r * 4)) & 1u) {
+                    const int b = p0 / HoWo, rem = p0 - b * HoWo;
+                    const size_t n = ((size_t)b * g.Co + o) * HoWo + rem;
+                    *reinterpret_cast<uint32_t *>(out_t + n) = tb;
+                    *reinterpret_cast<float4 *>(out_v + n) = make_float4(v[0], v[1], v[2], v[3]);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+                    if ((valid >> (r * 4 + i)) & 1u) {
+                        const int p = p0 + i;
+                        const int b = p / HoWo, rem = p - b * HoWo;
+                        const size_t n = ((size_t)b * g.Co + o) * HoWo + rem;
+                        out_t[n] = (uint8_t)(tb >> (8 * i));
+                        out_v[n] = v[i];
+                    }
+            }
+        }
+    }
+}
+
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+// The 32x32x16 form of the firing kernel (the 16x16x32 instruction runs at
+// half the rate on this chip): a wave owns 32 positions x 32 maps, B
+// fragments of all SK subtiles (16 taps each) stay in registers, and so do
+// the 8 time bytes per subtile of the wave's A fragments; their conversion to
+// halves is redone at each step rather than kept, which saves registers.
+// Accumulator element e of lane l is position row 8*(e/4) + 4*(l/32) + e%4,
+// map l % 32.
+template <int SK, int NP>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void k_fire32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g, float theta,
+              int iters, int vec_store, uint8_t *__restrict__ out_t, float *__restrict__ out_v)
+{
+    constexpr int kRows = kWaves * 32;  // positions per block iteration
+    // LDS: [time bytes of every wave's A fragments: wave][subtile][lane] | halo]
+    extern __shared__ __align__(16) uint8_t lds[];
+    uint2 *astage = reinterpret_cast<uint2 *>(lds) + (size_t)(threadIdx.x >> 6) * SK * 64;
+    uint8_t *halo = lds + (size_t)kWaves * SK * 64 * sizeof(uint2);
+    __shared__ int s_off[SK * 2];
+    __shared__ uint32_t s_bits[kWaves];
+    __shared__ int s_count[kWaves];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nt = blockIdx.y;
+    const int o = nt * 32 + (lane & 31);
+    const int HoWo = g.Ho * g.Wo;
+    const int Q8 = g.R8 / 8;
+    if (threadIdx.x < SK * 2) {
+        const int q = threadIdx.x;  // = s * 2 + lane half
+        const int ky = q / Q8, jq = q - ky * Q8;
+        s_off[q] = (ky < g.Kh ? ky : 0) * g.rowb + jq * 8;  // octets past K: any byte (B is zero)
+    }
+    h8 bw[SK][NP];
+#pragma unroll
+    for (int s = 0; s < SK; s++)
+#pragma unroll
+        for (int q = 0; q < NP; q++) bw[s][q] = bp[((size_t)(nt * SK + s) * NP + q) * 64 + lane];
+
+    for (int it = 0; it < iters; it++) {
+        const int pb0 = (blockIdx.x * iters + it) * kRows;
+        if (pb0 >= g.P) break;
+        const int pb1 = min(g.P, pb0 + kRows) - 1;
+        long long h0, h1;
+        group_range(g, pb0, pb1, h0, h1);
+        const long long a0 = h0 & ~15ll;
+        const int nvec = (int)((h1 - a0 + 15) >> 4) + 1;  // 16-byte words, one past the end
+        const uint32_t tmask = g.T >= 32 ? ~0u : ((1u << g.T) - 1u);
+        __syncthreads();  // the previous group's halo is no longer read
+        {
+            const uint4 *src = reinterpret_cast<const uint4 *>(xp + a0);
+            uint4 *dst = reinterpret_cast<uint4 *>(halo);
+            uint32_t hb = 0u;
+            int hc = 0;
+            for (int i = threadIdx.x; i < nvec; i += kThreads) {
+                const uint4 v = src[i];
+                dst[i] = v;
+                hb |= time_bits(make_uint2(v.x, v.y)) | time_bits(make_uint2(v.z, v.w));
+                hc += spikes4(v.x, g.T);  // density from a quarter of the bytes
+            }
+            hb = wave_or(hb);
+            hc = wave_sum(hc);
+            if (lane == 0) {
+                s_bits[wave] = hb;
+                s_count[wave] = hc;
+            }
+        }
+        __syncthreads();
+        uint32_t all = 0u;
+        int spikes = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; w++) {
+            all |= s_bits[w];
+            spikes += s_count[w];
+        }
+        all &= tmask;
+        const int tmin = all ? __builtin_ctz(all) : g.T;
+        const int tmax = all ? 31 - __builtin_clz(all) : -1;
+        const int span = tmax >= tmin ? tmax - tmin + 1 : 1;
+        // expected arrivals per (step, subtile): 32 rows x 16 taps
+        const float lambda = 512.0f * (float)spikes / ((float)nvec * 4.0f * (float)span);
+        const bool delta = lambda < 1.1f;
+
+        uint32_t ms[SK];
+        {
+            uint2 ab[SK];
+            const int p = pb0 + wave * 32 + (lane & 31);
+            const int pc = min(p, g.P - 1);
+            const int b = pc / HoWo, rem = pc - b * HoWo;
+            const int y = rem / g.Wo, x = rem - y * g.Wo;
+            const int base = (int)(((long long)b * g.Hp + (long long)y * g.stride) * g.rowb +
+                                   (long long)x * g.stride * g.Ci - a0);
+#pragma unroll
+            for (int s = 0; s < SK; s++) ab[s] = lds_read8(halo, base + s_off[s * 2 + (lane >> 5)]);
+#pragma unroll
+            for (int s = 0; s < SK; s++) ms[s] = 0u;
+            if (delta) {
+#pragma unroll
+                for (int s = 0; s < SK; s++) ms[s] = wave_or(time_bits(ab[s])) & tmask;
+            }
+            // each lane reads back only what it wrote: no barrier needed
+#pragma unroll
+            for (int s = 0; s < SK; s++) astage[s * 64 + lane] = ab[s];
+        }
+
+        uint32_t valid = 0u;
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int p = pb0 + wave * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            valid |= (p < g.P && o < g.Co) ? (1u << e) : 0u;
+        }
+        uint32_t fired = 0u;
+        uint32_t tf[4] = {0u, 0u, 0u, 0u};
+        float vk[16];
+#pragma unroll
+        for (int e = 0; e < 16; e++) vk[e] = 0.0f;
+        f16v acc;
+#pragma unroll
+        for (int e = 0; e < 16; e++) acc[e] = 0.0f;
+
+        for (int tau = 0; tau < g.T; tau++) {
+            // keeps the staged bytes in LDS: they are read again at every step
+            asm volatile("" ::: "memory");
+            if (delta) {
+                const uint32_t cb = 0x6400u + (uint32_t)tau;  // half 1024 + tau
+                const h2 cc = as_h2(cb | (cb << 16));
+#pragma unroll
+                for (int s = 0; s < SK; s++) {
+                    if ((ms[s] >> tau) & 1u) {
+                        const h8 a = frag_arrive(astage[s * 64 + lane], cc);
+#pragma unroll
+                        for (int q = 0; q < NP; q++)
+                            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bw[s][q], acc, 0, 0, 0);
+                    }
+                }
+            } else if (tau >= tmin && tau <= tmax) {
+                const uint32_t cb = 0x6401u + (uint32_t)tau;  // half 1025 + tau
+                const h2 cc = as_h2(cb | (cb << 16));
+#pragma unroll
+                for (int e = 0; e < 16; e++) acc[e] = 0.0f;
+#pragma unroll
+                for (int s = 0; s < SK; s++) {
+                    const h8 a = frag_upto(astage[s * 64 + lane], cc);
+#pragma unroll
+                    for (int q = 0; q < NP; q++)
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bw[s][q], acc, 0, 0, 0);
+                }
+            }
+            // crossings of theta at this step (first crossing only)
+            uint32_t now = 0u;
+#pragma unroll
+            for (int e = 0; e < 16; e++) now |= (acc[e] > theta) ? (1u << e) : 0u;
+            now &= valid & ~fired;
+            if (__ballot(now != 0u)) {
+#pragma unroll
+                for (int e = 0; e < 16; e++)
+                    if ((now >> e) & 1u) {
+                        vk[e] = acc[e];
+                        tf[e >> 2] = (tf[e >> 2] & ~(0xFFu << (8 * (e & 3)))) | ((uint32_t)tau << (8 * (e & 3)));
+                    }
+                fired |= now;
+            }
+            if (tau >= tmax) break;  // no later arrival: the potentials stay as they are
+        }
+
+        // times and key potentials: t_f and V[t_f], or NEVER and V[T-1]
+#pragma unroll
+        for (int g4 = 0; g4 < 4; g4++) {
+            uint32_t tb = 0u;
+            float v[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int e = g4 * 4 + i;
+                const bool f = (fired >> e) & 1u;
+                v[i] = f ? vk[e] : acc[e];
+                tb |= (f ? ((tf[g4] >> (8 * i)) & 0xFFu) : (uint32_t)spk::kNever) << (8 * i);
+            }
+            const int p0 = pb0 + wave * 32 + 8 * g4 + 4 * (lane >> 5);
+            if (vec_store) {
+                // 4 positions of one sample, 4-aligned (Ho*Wo % 4 == 0)
+                if (p0 < g.P && o < g.Co) {
+                    const int b = p0 / HoWo, rem = p0 - b * HoWo;
+                    const size_t n = ((size_t)b * g.Co + o) * HoWo + rem;
+                    *reinterpret_cast<uint32_t *>(out_t + n) = tb;
+                    *reinterpret_cast<float4 *>(out_v + n) = make_float4(v[0], v[1], v[2], v[3]);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const int p = p0 + i;
+                    if (p < g.P && o < g.Co) {
+                        const int b = p / HoWo, rem = p - b * HoWo;
+                        const size_t n = ((size_t)b * g.Co + o) * HoWo + rem;
+                        out_t[n] = (uint8_t)(tb >> (8 * i));
+                        out_v[n] = v[i];
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Kernel variants.  Both keep the B fragments of all subtiles in registers:
+// the 32x32x16 one (S16 subtiles: 2*S16 + 4*NP*S16 registers of operands) up
+// to 19 float or 31 half subtiles, else the 16x16x32 one (R*S*4 + NP*S*4,
+// R = 2 row tiles per wave, or 1 for deeper layers) up to 15 float or 24 half
+// subtiles.
+enum Variant { kNone = 0, kV32 = 1, kV16 = 2 };
+
+Variant variant_of(const FGeom &g, bool half_w)
+{
+    if (g.S16 <= (half_w ? 31 : 19)) return kV32;
+    if (g.S <= (half_w ? 24 : 15)) return kV16;
+    return kNone;
+}
+
+constexpr int rows_per_wave(int S, int NP) { return S <= (NP == 2 ? 9 : 12) ? 2 : 1; }
+
+int group_rows(const FGeom &g, bool half_w)
+{
+    if (variant_of(g, half_w) == kV32) return kWaves * 32;
+    return kWaves * rows_per_wave(g.S, half_w ? 1 : 2) * 16;
+}
+
+long long max_group_bytes(const FGeom &g, bool half_w)
+{
+    const int rows = group_rows(g, half_w);
+    long long best = 0;
+    for (long long p0 = 0; p0 < g.P; p0 += rows) {
+        const int p1 = (int)std::min<long long>(g.P, p0 + rows) - 1;
+        long long h0, h1;
+        group_range(g, (int)p0, p1, h0, h1);
+        best = std::max(best, h1 - (h0 & ~15ll));
+    }
+    return best;
+}
+
+size_t halo_lds(long long group_bytes) { return spk::align_up((size_t)group_bytes + 32, 16); }
+
+// LDS bytes of the largest row group of a geometry, remembered per geometry
+// (the exact maximum walks every group once).
+size_t group_lds(const FGeom &g, bool half_w)
+{
+    typedef std::tuple<int, int, int, int, int, int, int, int, int, int> Key;
+    static std::mutex mu;
+    static std::map<Key, size_t> memo;
+    const Key key{g.B, g.Ci, g.Hi, g.Wi, g.Kh, g.Kw, g.stride, g.pad, g.Ho, (int)half_w};
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = memo.find(key);
+        if (it != memo.end()) return it->second;
+    }
+    const size_t v = halo_lds(max_group_bytes(g, half_w));
+    std::lock_guard<std::mutex> lock(mu);
+    if (memo.size() > 4096) memo.clear();
+    memo[key] = v;
+    return v;
+}
+
+template <int SM, int NP>
+void launch_fire(const uint8_t *xp, const h8 *bp, const FGeom &g, float theta, int iters,
+                 int vec_store, size_t lds, uint8_t *ot, float *ov, hipStream_t s)
+{
+    constexpr int R = rows_per_wave(SM, NP);
+    const int groups = spk::ceil_div(g.P, kWaves * R * 16);
+    dim3 grid(spk::ceil_div(groups, iters), g.NT);
+    hipLaunchKernelGGL((k_fire_fast<SM, NP, R>), grid, dim3(kThreads), lds, s, xp, bp, g, theta,
+                       iters, vec_store, ot, ov);
+}
+
+typedef void (*FireLauncher)(const uint8_t *, const h8 *, const FGeom &, float, int, int, size_t,
+                             uint8_t *, float *, hipStream_t);
+
+#define SPK_FIRE_2(S) &launch_fire<S, 2>
+#define SPK_FIRE_1(S) &launch_fire<S, 1>
+const FireLauncher kFireF32[16] = {
+    nullptr,        SPK_FIRE_2(1),  SPK_FIRE_2(2),  SPK_FIRE_2(3),  SPK_FIRE_2(4),  SPK_FIRE_2(5),
+    SPK_FIRE_2(6),  SPK_FIRE_2(7),  SPK_FIRE_2(8),  SPK_FIRE_2(9),  SPK_FIRE_2(10), SPK_FIRE_2(11),
+    SPK_FIRE_2(12), SPK_FIRE_2(13), SPK_FIRE_2(14), SPK_FIRE_2(15)};
+const FireLauncher kFireF16[25] = {
+    nullptr,        SPK_FIRE_1(1),  SPK_FIRE_1(2),  SPK_FIRE_1(3),  SPK_FIRE_1(4),  SPK_FIRE_1(5),
+    SPK_FIRE_1(6),  SPK_FIRE_1(7),  SPK_FIRE_1(8),  SPK_FIRE_1(9),  SPK_FIRE_1(10), SPK_FIRE_1(11),
+    SPK_FIRE_1(12), SPK_FIRE_1(13), SPK_FIRE_1(14), SPK_FIRE_1(15), SPK_FIRE_1(16), SPK_FIRE_1(17),
+    SPK_FIRE_1(18), SPK_FIRE_1(19), SPK_FIRE_1(20), SPK_FIRE_1(21), SPK_FIRE_1(22), SPK_FIRE_1(23),
+    SPK_FIRE_1(24)};
+#undef SPK_FIRE_2
+#undef SPK_FIRE_1
+
+template <int SK, int NP>
+void launch_fire32(const uint8_t *xp, const h8 *bp, const FGeom &g, float theta, int iters,
+                   int vec_store, size_t lds, uint8_t *ot, float *ov, hipStream_t s)
+{
+    const int groups = spk::ceil_div(g.P, kWaves * 32);
+    dim3 grid(spk::ceil_div(groups, iters), g.NT32);
+    hipLaunchKernelGGL((k_fire32<SK, NP>), grid, dim3(kThreads), lds, s, xp, bp, g, theta, iters,
+                       vec_store, ot, ov);
+}
+
+#define SPK_F32_2(S) &launch_fire32<S, 2>
+#define SPK_F32_1(S) &launch_fire32<S, 1>
+const FireLauncher kFire32F32[20] = {
+    nullptr,        SPK_F32_2(1),  SPK_F32_2(2),  SPK_F32_2(3),  SPK_F32_2(4),  SPK_F32_2(5),
+    SPK_F32_2(6),   SPK_F32_2(7),  SPK_F32_2(8),  SPK_F32_2(9),  SPK_F32_2(10), SPK_F32_2(11),
+    SPK_F32_2(12),  SPK_F32_2(13), SPK_F32_2(14), SPK_F32_2(15), SPK_F32_2(16), SPK_F32_2(17),
+    SPK_F32_2(18),  SPK_F32_2(19)};
+const FireLauncher kFire32F16[32] = {
+    nullptr,        SPK_F32_1(1),  SPK_F32_1(2),  SPK_F32_1(3),  SPK_F32_1(4),  SPK_F32_1(5),
+    SPK_F32_1(6),   SPK_F32_1(7),  SPK_F32_1(8),  SPK_F32_1(9),  SPK_F32_1(10), SPK_F32_1(11),
+    SPK_F32_1(12),  SPK_F32_1(13), SPK_F32_1(14), SPK_F32_1(15), SPK_F32_1(16), SPK_F32_1(17),
+    SPK_F32_1(18),  SPK_F32_1(19), SPK_F32_1(20), SPK_F32_1(21), SPK_F32_1(22), SPK_F32_1(23),
+    SPK_F32_1(24),  SPK_F32_1(25), SPK_F32_1(26), SPK_F32_1(27), SPK_F32_1(28), SPK_F32_1(29),
+    SPK_F32_1(30),  SPK_F32_1(31)};
+#undef SPK_F32_2
+#undef SPK_F32_1
+
+}  // namespace
+
+namespace spk {
+
+bool conv_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                         int pad, int Ho, int Wo, bool half_w, bool readout, bool potentials)
+{
+    if (readout || potentials || T < 1 || T > 32 || B < 1 || Ci < 1 || Co < 1 || Ho < 1 || Wo < 1) return false;
+    const long long Hp = Hi + 2ll * pad, Wp = Wi + 2ll * pad;
+    if ((long long)B * Ho * Wo >= (1ll << 31) || (long long)B * Hp * Wp * Ci + kSlack >= (1ll << 31))
+        return false;
+    if ((long long)Kw * Ci > (1 << 16) || Kh > (1 << 12)) return false;
+    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    if (variant_of(g, half_w) == kNone) return false;
+    if ((long long)g.rowb * g.Kh > kHaloMax) return false;  // cheap pre-check
+    return group_lds(g, half_w) <= (size_t)kHaloMax;  // + at most 31 KB of staged bytes
+}
+
+size_t conv_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                           int pad, int Ho, int Wo)
+{
+    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    return xp_bytes(g) + bp_bytes(g, 2);
+}
+
+spk_status conv_fire_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
+                          bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
+                          float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
+{
+    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
+    h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
+    const Variant v = variant_of(g, half_w);
+    const long long nx = (long long)g.B * g.Hp * g.rowb + kSlack;
+    const int nb_in = spk::ceil_div(nx, 256);
+    const int nb_w = v == kV32 ? spk::ceil_div((long long)g.NT32 * g.S16 * 64, 256)
+                               : spk::ceil_div((long long)g.NT * g.S * 64, 256);
+    const dim3 pg(nb_in + nb_w);
+    if (v == kV32) {
+        if (half_w) hipLaunchKernelGGL((k_pack<1, true, true>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
+        else hipLaunchKernelGGL((k_pack<2, false, true>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
+    } else {
+        if (half_w) hipLaunchKernelGGL((k_pack<1, true, false>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
+        else hipLaunchKernelGGL((k_pack<2, false, false>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
+    }
+    SPK_LAUNCHED("spk_conv_fire");
+
+    // Row groups per block: keep about 640 blocks in flight (two per CU with
+    // some slack) so that each wave's register B fragments serve several groups.
+    const int groups = spk::ceil_div(g.P, group_rows(g, half_w));
+    const int col_tiles = v == kV32 ? g.NT32 : g.NT;
+    int iters = (int)std::max<long long>(1, (long long)groups * col_tiles / 640);
+    iters = std::min(iters, groups);
+    size_t lds = group_lds(g, half_w);
+    if (v == kV32) lds += (size_t)kWaves * g.S16 * 64 * sizeof(uint2);
+    const int vec_store = (g.Ho * g.Wo) % 4 == 0 && ((uintptr_t)out_t & 3) == 0 &&
+                          ((uintptr_t)out_v & 15) == 0;
+    const FireLauncher launch = v == kV32 ? (half_w ? kFire32F16[g.S16] : kFire32F32[g.S16])
+                                          : (half_w ? kFireF16[g.S] : kFireF32[g.S]);
+    launch(xp, bp, g, theta, iters, vec_store, lds, out_t, out_v, s);
+    return check_launch("spk_conv_fire");
+}
+
+}  // namespace spk

@@ -33,6 +33,16 @@ spk_status conv_fire_mfma(const uint8_t *in, int B, int T, int Ci, int Hi, int W
                           float theta, uint8_t *out_t, float *out_v, float *pot, void *ws,
                           hipStream_t s);
 
+// Register-resident firing kernels on a channels-last copy of the input
+// (spk_conv_fast.hip): firing layers without the dense potentials.
+bool conv_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                         int pad, int Ho, int Wo, bool half_w, bool readout, bool potentials);
+size_t conv_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                           int pad, int Ho, int Wo);
+spk_status conv_fire_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
+                          bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
+                          float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s);
+
 }  // namespace spk
 
 #define SPK_REQUIRE(cond, code, ...)        \

@@ -110,6 +110,12 @@ CONV_CASES = [
     (3, 250, 5, 5, 200, 5, 1, 2, 15, math.inf, 0.3, "f32"),
     (2, 40, 6, 7, 24, 3, 1, 1, 9, math.inf, 0.5, "f16"),
     (1, 1, 3, 3, 1, 3, 3, 0, 1, 0.5, 1.0, "f32"),
+    (2, 16, 11, 13, 40, 5, 1, 2, 10, 12.0, 0.3, "f32"),     # 13 subtiles: one row tile per wave
+    (4, 2, 170, 250, 8, 3, 1, 1, 8, 2.5, 0.2, "f32"),       # several row groups per block, ragged
+    (2, 8, 10, 10, 20, 3, 1, 1, 32, 5.0, 0.3, "f32"),       # T = 32
+    (2, 8, 10, 10, 20, 3, 1, 1, 33, 5.0, 0.3, "f32"),       # T = 33
+    (2, 30, 14, 14, 37, 3, 1, 1, 15, 3.0, 0.02, "f32"),     # sparse arrivals
+    (2, 5, 9, 9, 7, 3, 1, 1, 5, -0.5, 0.3, "f32"),          # negative threshold
 ]
 
 
@@ -128,15 +134,14 @@ def test_conv_fire_matches_oracle(case):
     check_potentials(np_(g_V), o_V)
     exc = excused_from_potentials(o_V, theta)
     check_fire(np_(g_tf), np_(g_vk), o_tf, o_vk, exc)
-    # without the dense potentials: firing layers give the same outputs bit for bit;
-    # readout layers take the single-frame GEMM, equal to the oracle within tolerance
+    # without the dense potentials the call takes the firing kernels (or, for a
+    # readout layer, the single-frame GEMM): same rules against the oracle
     g_tf2, g_vk2 = spk.spk_conv_fire(_t(times, dev), w_dev, T, s, p, theta)
     if math.isinf(theta):
         assert np.all(np_(g_tf2) == NEVER)
         check_potentials(np_(g_vk2), o_vk, "readout v_key")
     else:
-        np.testing.assert_array_equal(np_(g_tf2), np_(g_tf))
-        np.testing.assert_array_equal(np_(g_vk2), np_(g_vk))
+        check_fire(np_(g_tf2), np_(g_vk2), o_tf, o_vk, exc)
 
 
 def test_conv_fire_hand_example():
@@ -149,6 +154,10 @@ def test_conv_fire_hand_example():
     np.testing.assert_array_equal(np_(V)[0, :, 0], np.array(g["potentials_by_t"], np.float32))
     np.testing.assert_array_equal(np_(tf)[0, 0], np.array(g["t_f"], np.uint8))
     np.testing.assert_array_equal(np_(vk)[0, 0], np.array(g["v_key"], np.float32))
+    # the firing kernels (no dense potentials): dyadic values, exact in any order
+    tf2, vk2 = spk.spk_conv_fire(_t(times, dev), _t(w, dev), g["T"], 1, 0, g["theta"])
+    np.testing.assert_array_equal(np_(tf2)[0, 0], np.array(g["t_f"], np.uint8))
+    np.testing.assert_array_equal(np_(vk2)[0, 0], np.array(g["v_key"], np.float32))
 
 
 def test_conv_fire_silent_input_and_negative_weights():
@@ -162,6 +171,9 @@ def test_conv_fire_silent_input_and_negative_weights():
     assert np.all(np_(g_tf)[0] == NEVER) and not np_(g_V)[0].any()
     check_potentials(np_(g_V), o_V)
     check_fire(np_(g_tf), np_(g_vk), o_tf, o_vk, excused_from_potentials(o_V, 0.5))
+    g_tf2, g_vk2 = spk.spk_conv_fire(_t(times, dev), _t(w, dev), 6, 1, 1, 0.5)
+    assert np.all(np_(g_tf2)[0] == NEVER) and not np_(g_vk2)[0].any()
+    check_fire(np_(g_tf2), np_(g_vk2), o_tf, o_vk, excused_from_potentials(o_V, 0.5))
 
 
 # --------------------------------------------------------------------- pool
