@@ -112,12 +112,15 @@ __global__ __launch_bounds__(kThreads) void k_code_small(const float *__restrict
     uint64_t k8[8];
     int mine = 0;
     const int first = threadIdx.x * 8;
+    float xv[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) xv[j] = xs[min(first + j, n - 1)];  // all loads first
 #pragma unroll
     for (int j = 0; j < 8; j++) {
         const int i = first + j;
         uint64_t key = kDead;
         if (i < n) {
-            key = make_key(xs[i], min_value, (uint32_t)i);
+            key = make_key(xv[j], min_value, (uint32_t)i);
             if (key == kDead) ts[i] = spk::kNever;
             else mine++;
         }

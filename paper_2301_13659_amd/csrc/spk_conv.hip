@@ -91,6 +91,9 @@ extern "C" size_t spk_conv_fire_workspace_size(int B, int T, int Ci, int Hi, int
     if (spk::conv_fast_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, true, readout,
                                  potentials != 0))
         need = std::max(need, spk::conv_fast_workspace(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo));
+    if (readout && spk::readout_fast_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo))
+        need = std::max(need,
+                        spk::readout_fast_workspace(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo));
     return need;
 }
 
@@ -128,6 +131,9 @@ extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int C
                                  potentials != nullptr))
         return spk::conv_fire_fast(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho,
                                    Wo, theta, out_times, out_vkey, ws, spk::stream_of(stream));
+    if (readout && spk::readout_fast_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo))
+        return spk::readout_fast(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho,
+                                 Wo, out_times, out_vkey, ws, spk::stream_of(stream));
     if (spk::conv_mfma_supported(Ci, Kh, Kw, Co, half_w, readout))
         return spk::conv_fire_mfma(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho,
                                    Wo, theta, out_times, out_vkey, potentials, ws,

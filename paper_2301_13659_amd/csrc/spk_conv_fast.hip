@@ -185,61 +185,147 @@ __device__ __forceinline__ uint32_t time_bits(uint2 x)
     return m;
 }
 
+// Copy n 16-byte words from global memory to LDS with the whole block, four
+// loads per thread in flight before their stores.
+__device__ __forceinline__ void copy_to_lds(uint4 *__restrict__ dst, const uint4 *__restrict__ src,
+                                            int n)
+{
+    const int step = (int)blockDim.x;
+    int i = threadIdx.x;
+    for (; i + 3 * step < n; i += 4 * step) {
+        const uint4 a = src[i], b = src[i + step], c = src[i + 2 * step], d = src[i + 3 * step];
+        dst[i] = a;
+        dst[i + step] = b;
+        dst[i + 2 * step] = c;
+        dst[i + 3 * step] = d;
+    }
+    for (; i < n; i += step) dst[i] = src[i];
+}
+
 // ------------------------------------------------------------------ packing
 
-// Blocks [0, nb_in): padded channels-last time map, one thread per Xp byte.
-// Blocks [nb_in, ...): B fragments, one thread per (column tile, subtile,
-// lane), 8 taps each, as hi/lo halves (NP = 2) or halves (NP = 1).
-// kBig: fragments of the 32x32x16 shape (lane: map l % 32, taps 8*(l/32)..+7
-// of a 16-tap subtile), else of the 16x16x32 shape (map l % 16, taps
-// 8*(l/16)..+7 of a 32-tap subtile).
+// Blocks [0, B*Hp): one padded input row each, (b, py): the row's time bytes
+// go through LDS from channel rows (coalesced reads) to channels-last order
+// (coalesced writes); the last block also fills the readable slack.
+// Blocks [B*Hp, B*Hp + maps): one output map o each (maps = the column tiles'
+// width, the padding maps written as zeros): its weights are staged in LDS
+// and written as B fragments in the packed tap order, as hi/lo halves
+// (NP = 2) or halves (NP = 1).  kBig: fragments of the 32x32x16 shape (lane:
+// map l % 32, taps 8*(l/32)..+7 of a 16-tap subtile), else of the 16x16x32
+// shape (map l % 16, taps 8*(l/16)..+7 of a 32-tap subtile).
 template <int NP, bool kHalfW, bool kBig>
 __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
                                               const void *__restrict__ wv, FGeom g, int nb_in,
                                               uint8_t *__restrict__ xp, h8 *__restrict__ bp)
 {
+    extern __shared__ __align__(16) uint8_t sm[];
     if ((int)blockIdx.x < nb_in) {
-        // sizes below 2^31 (checked on the host)
-        const uint32_t n = (uint32_t)g.B * g.Hp * g.rowb;
-        const uint32_t e = blockIdx.x * 256u + threadIdx.x;
-        if (e >= n + kSlack) return;
-        uint8_t v = (uint8_t)spk::kNever;
-        if (e < n) {
-            const uint32_t pix = e / g.Ci, c = e - pix * g.Ci;
-            const uint32_t prow = pix / g.Wp, px = pix - prow * g.Wp;
-            const uint32_t b = prow / g.Hp, py = prow - b * g.Hp;
-            const int iy = (int)py - g.pad, ix = (int)px - g.pad;
-            if ((unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi)
-                v = in[(((size_t)b * g.Ci + c) * g.Hi + iy) * g.Wi + ix];
+        const int b = blockIdx.x / g.Hp, py = blockIdx.x - b * g.Hp;
+        const int iy = py - g.pad;
+        uint8_t *row = xp + ((size_t)b * g.Hp + py) * g.rowb;
+        if ((unsigned)iy < (unsigned)g.Hi) {
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = (uint8_t)spk::kNever;
+            __syncthreads();
+            const uint8_t *src = in + (size_t)b * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi;
+            const int n = g.Ci * g.Wi, step = (int)blockDim.x;
+            auto put = [&](int e, uint8_t v) {
+                const int c = e / g.Wi, x = e - c * g.Wi;
+                sm[(x + g.pad) * g.Ci + c] = v;
+            };
+            auto get = [&](int e) {
+                const int c = e / g.Wi, x = e - c * g.Wi;
+                return src[(size_t)c * g.Hi * g.Wi + x];
+            };
+            int e = threadIdx.x;
+            for (; e + 3 * step < n; e += 4 * step) {
+                const uint8_t a = get(e), bb = get(e + step), c = get(e + 2 * step), d = get(e + 3 * step);
+                put(e, a);
+                put(e + step, bb);
+                put(e + 2 * step, c);
+                put(e + 3 * step, d);
+            }
+            for (; e < n; e += step) put(e, get(e));
+            __syncthreads();
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = sm[e];
+        } else {
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = (uint8_t)spk::kNever;
         }
-        xp[e] = v;
+        if ((int)blockIdx.x == nb_in - 1)
+            for (int e = threadIdx.x; e < kSlack; e += blockDim.x) row[g.rowb + e] = (uint8_t)spk::kNever;
         return;
     }
-    const int NS = kBig ? g.S16 : g.S;
-    const long long f = (long long)(blockIdx.x - nb_in) * 256 + threadIdx.x;
-    if (f >= (long long)(kBig ? g.NT32 : g.NT) * NS * 64) return;
-    const int lane = (int)(f & 63);
-    const long long ts = f >> 6;
-    const int s = (int)(ts % NS), nt = (int)(ts / NS);
-    const int o = kBig ? nt * 32 + (lane & 31) : nt * 16 + (lane & 15);
-    const int kb = kBig ? (s * 2 + (lane >> 5)) * 8 : (s * 4 + (lane >> 4)) * 8;
-    h8 hi, lo;
-#pragma unroll
-    for (int e = 0; e < 8; e++) {
-        const int k = kb + e, ky = k / g.R8, j = k - ky * g.R8;
-        float w = 0.0f;
-        if (o < g.Co && ky < g.Kh && j < g.run) {
-            const int kx = j / g.Ci, c = j - kx * g.Ci;
-            const size_t at = (((size_t)o * g.Ci + c) * g.Kh + ky) * g.Kw + kx;
-            w = kHalfW ? (float)reinterpret_cast<const _Float16 *>(wv)[at]
-                       : reinterpret_cast<const float *>(wv)[at];
+    const int o = blockIdx.x - nb_in;
+    const int taps = g.Ci * g.Kh * g.Kw;
+    float *wl = reinterpret_cast<float *>(sm);
+    {
+        const int oc = min(o, g.Co - 1);
+        auto wget = [&](int e) {
+            const size_t at = (size_t)oc * taps + e;
+            return kHalfW ? (float)reinterpret_cast<const _Float16 *>(wv)[at]
+                          : reinterpret_cast<const float *>(wv)[at];
+        };
+        const bool real = o < g.Co;  // padding maps: zeros
+        const int step = (int)blockDim.x;
+        int e = threadIdx.x;
+        for (; e + 3 * step < taps; e += 4 * step) {
+            const float a = wget(e), b = wget(e + step), c = wget(e + 2 * step), d = wget(e + 3 * step);
+            wl[e] = real ? a : 0.0f;
+            wl[e + step] = real ? b : 0.0f;
+            wl[e + 2 * step] = real ? c : 0.0f;
+            wl[e + 3 * step] = real ? d : 0.0f;
         }
-        const _Float16 h = (_Float16)w;
-        hi[e] = h;
-        lo[e] = (_Float16)(w - (float)h);
+        for (; e < taps; e += step) wl[e] = real ? wget(e) : 0.0f;
     }
-    bp[(size_t)(ts * NP) * 64 + lane] = hi;
-    if (NP == 2) bp[(size_t)(ts * NP + 1) * 64 + lane] = lo;
+    __syncthreads();
+    // this map's lanes: kBig 2 per 16-tap subtile, else 4 per 32-tap subtile
+    const int per = kBig ? 2 : 4, NS = kBig ? g.S16 : g.S;
+    const int nt = kBig ? o / 32 : o / 16, col = kBig ? o & 31 : o & 15;
+    for (int f = threadIdx.x; f < NS * per; f += blockDim.x) {
+        const int s = f / per, h = f - s * per;
+        const int lane = col + (kBig ? 32 : 16) * h;
+        const int kb = (s * per + h) * 8;
+        h8 hi, lo;
+        // tap kb = ky*R8 + j, j = kx*Ci + c; the 8 taps step through (ky, j, kx, c)
+        int ky = kb / g.R8, j = kb - ky * g.R8;
+        int kx = j / g.Ci, c = j - kx * g.Ci;
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            float w = 0.0f;
+            if (ky < g.Kh && j < g.run) w = wl[(c * g.Kh + ky) * g.Kw + kx];
+            const _Float16 hw = (_Float16)w;
+            hi[e] = hw;
+            lo[e] = (_Float16)(w - (float)hw);
+            if (++j == g.R8) {
+                j = 0;
+                ky++;
+                kx = 0;
+                c = 0;
+            } else if (++c == g.Ci) {
+                c = 0;
+                kx++;
+            }
+        }
+        const size_t ts = (size_t)nt * NS + s;
+        bp[(ts * NP) * 64 + lane] = hi;
+        if (NP == 2) bp[(ts * NP + 1) * 64 + lane] = lo;
+    }
+}
+
+// Launch of the packing pass for a fragment shape.
+void launch_pack(const uint8_t *in, const void *w, bool half_w, bool big, const FGeom &g,
+                 uint8_t *xp, h8 *bp, hipStream_t s)
+{
+    const int nb_in = g.B * g.Hp;
+    const int maps = big ? g.NT32 * 32 : g.NT * 16;
+    const size_t lds = std::max((size_t)g.rowb, (size_t)g.Ci * g.Kh * g.Kw * sizeof(float));
+    const dim3 grid(nb_in + maps), blk(256);
+    if (big) {
+        if (half_w) hipLaunchKernelGGL((k_pack<1, true, true>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
+        else hipLaunchKernelGGL((k_pack<2, false, true>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
+    } else {
+        if (half_w) hipLaunchKernelGGL((k_pack<1, true, false>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
+        else hipLaunchKernelGGL((k_pack<2, false, false>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
+    }
 }
 
 // -------------------------------------------------------------------- firing
@@ -305,11 +391,20 @@ void k_fire_fast(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeo
             uint4 *dst = reinterpret_cast<uint4 *>(halo);
             uint32_t hb = 0u;
             int hc = 0;
-            for (int i = threadIdx.x; i < nvec; i += kThreads) {
+            int i = threadIdx.x;
+            for (; i + kThreads < nvec; i += 2 * kThreads) {
+                const uint4 v = src[i], u = src[i + kThreads];
+                dst[i] = v;
+                dst[i + kThreads] = u;
+                hb |= time_bits(make_uint2(v.x, v.y)) | time_bits(make_uint2(v.z, v.w)) |
+                      time_bits(make_uint2(u.x, u.y)) | time_bits(make_uint2(u.z, u.w));
+                hc += spikes4(v.x, g.T) + spikes4(u.x, g.T);  // density from a quarter of the bytes
+            }
+            for (; i < nvec; i += kThreads) {
                 const uint4 v = src[i];
                 dst[i] = v;
                 hb |= time_bits(make_uint2(v.x, v.y)) | time_bits(make_uint2(v.z, v.w));
-                hc += spikes4(v.x, g.T);  // density from a quarter of the bytes
+                hc += spikes4(v.x, g.T);
             }
             hb = wave_or(hb);
             hc = wave_sum(hc);
@@ -541,11 +636,20 @@ void k_fire32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g
             uint4 *dst = reinterpret_cast<uint4 *>(halo);
             uint32_t hb = 0u;
             int hc = 0;
-            for (int i = threadIdx.x; i < nvec; i += kThreads) {
+            int i = threadIdx.x;
+            for (; i + kThreads < nvec; i += 2 * kThreads) {
+                const uint4 v = src[i], u = src[i + kThreads];
+                dst[i] = v;
+                dst[i + kThreads] = u;
+                hb |= time_bits(make_uint2(v.x, v.y)) | time_bits(make_uint2(v.z, v.w)) |
+                      time_bits(make_uint2(u.x, u.y)) | time_bits(make_uint2(u.z, u.w));
+                hc += spikes4(v.x, g.T) + spikes4(u.x, g.T);  // density from a quarter of the bytes
+            }
+            for (; i < nvec; i += kThreads) {
                 const uint4 v = src[i];
                 dst[i] = v;
                 hb |= time_bits(make_uint2(v.x, v.y)) | time_bits(make_uint2(v.z, v.w));
-                hc += spikes4(v.x, g.T);  // density from a quarter of the bytes
+                hc += spikes4(v.x, g.T);
             }
             hb = wave_or(hb);
             hc = wave_sum(hc);
@@ -689,6 +793,130 @@ void k_fire32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g
     }
 }
 
+// ------------------------------------------------------------------ readout
+//
+// Readout layers (theta = +inf) need only V at the last step: one GEMM on the
+// final frame [time <= T-1], split over K.  A block of 4 waves owns a column
+// tile (32 maps) and a run of 4*kRoKC subtiles; wave w keeps the B fragments
+// of subtiles w*kRoKC.. in registers.  The block walks row groups of 32
+// positions: it stages the Xp rows that group and its K run touch, each wave
+// accumulates its subtiles, and the four partial tiles are added in LDS in
+// wave order and written to part[split][map][position].  k_readout_sum adds
+// the splits in order.
+constexpr int kRoKC = 16;
+constexpr int kRoSteps = kWaves * kRoKC;
+constexpr int kRoRed = kWaves * 1024 * (int)sizeof(float);  // LDS of the partial tiles
+
+__host__ __device__ inline void ro_range(const FGeom &g, int p0, int p1, int sp, long long &h0,
+                                         long long &h1)
+{
+    const int HoWo = g.Ho * g.Wo;
+    const int kb0 = sp * kRoSteps * 16, kb1 = min(g.K, (sp + 1) * kRoSteps * 16);
+    const int ky_lo = min(kb0 / g.R8, g.Kh - 1), ky_hi = min((kb1 - 1) / g.R8, g.Kh - 1);
+    const int b0 = p0 / HoWo, y0 = (p0 - b0 * HoWo) / g.Wo;
+    const int b1 = p1 / HoWo, y1 = (p1 - b1 * HoWo) / g.Wo;
+    h0 = ((long long)b0 * g.Hp + (long long)y0 * g.stride + ky_lo) * g.rowb;
+    h1 = ((long long)b1 * g.Hp + (long long)y1 * g.stride + ky_hi + 1) * g.rowb;
+}
+
+template <int NP>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g, int iters,
+                 int n_groups, int halo_cap, float *__restrict__ part)
+{
+    // LDS: [partial tiles: wave][element][lane] | halo]
+    extern __shared__ __align__(16) uint8_t lds[];
+    float *red = reinterpret_cast<float *>(lds);
+    uint8_t *halo = lds + kRoRed;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nt = blockIdx.y, sp = blockIdx.z;
+    const int sw0 = sp * kRoSteps + wave * kRoKC;            // this wave's first subtile
+    const int nsw = max(0, min(kRoKC, g.S16 - sw0));          // and how many it has
+    const int HoWo = g.Ho * g.Wo;
+    const int Q8 = g.R8 / 8;
+    const int kb0 = sp * kRoSteps * 16;
+    const int ky_lo = min(kb0 / g.R8, g.Kh - 1);
+
+    h8 bw[kRoKC][NP];
+#pragma unroll
+    for (int s = 0; s < kRoKC; s++) {
+        const int sc = min(sw0 + s, g.S16 - 1);
+#pragma unroll
+        for (int q = 0; q < NP; q++) bw[s][q] = bp[((size_t)(nt * g.S16 + sc) * NP + q) * 64 + lane];
+    }
+    const uint32_t cb = 0x6401u + (uint32_t)(g.T - 1);  // half 1025 + (T - 1)
+    const h2 cc = as_h2(cb | (cb << 16));
+
+    for (int it = 0; it < iters; it++) {
+        const int rg = blockIdx.x * iters + it;
+        if (rg >= n_groups) break;
+        const int p0 = rg * 32, p1 = min(g.P, p0 + 32) - 1;
+        long long h0, h1;
+        ro_range(g, p0, p1, sp, h0, h1);
+        const long long a0 = h0 & ~15ll;
+        const int nvec = (int)((h1 - a0 + 15) >> 4) + 1;
+        __syncthreads();  // the previous group's halo and partial tiles are no longer read
+        copy_to_lds(reinterpret_cast<uint4 *>(halo), reinterpret_cast<const uint4 *>(xp + a0), nvec);
+        __syncthreads();
+
+        f16v acc;
+#pragma unroll
+        for (int e = 0; e < 16; e++) acc[e] = 0.0f;
+        {
+            const int p = p0 + (lane & 31);
+            const int pc = min(p, g.P - 1);
+            const int b = pc / HoWo, rem = pc - b * HoWo;
+            const int y = rem / g.Wo, x = rem - y * g.Wo;
+            const int base = (int)(((long long)b * g.Hp + (long long)y * g.stride) * g.rowb +
+                                   (long long)x * g.stride * g.Ci - a0);
+            const int q0 = 2 * sw0 + (lane >> 5);
+            int ky = q0 / Q8, jq = q0 - ky * Q8;
+#pragma unroll
+            for (int s = 0; s < kRoKC; s++) {
+                if (s < nsw) {
+                    // octets past K read a row of the halo (their weights are zero)
+                    const int off = ky < g.Kh ? ky * g.rowb + jq * 8 : ky_lo * g.rowb;
+                    const h8 a = frag_upto(lds_read8(halo, base + off), cc);
+#pragma unroll
+                    for (int q = 0; q < NP; q++)
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bw[s][q], acc, 0, 0, 0);
+                }
+                jq += 2;
+                while (jq >= Q8) {
+                    jq -= Q8;
+                    ky++;
+                }
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < 16; e++) red[(wave * 16 + e) * 64 + lane] = acc[e];
+        __syncthreads();
+        // element (e, l): position row 8*(e/4) + 4*(l/32) + e%4, map l % 32
+        for (int i = threadIdx.x; i < 1024; i += kThreads) {
+            const int e = i >> 6, l = i & 63;
+            const float v = ((red[i] + red[1024 + i]) + red[2048 + i]) + red[3072 + i];
+            const int p = p0 + 8 * (e >> 2) + 4 * (l >> 5) + (e & 3), o = nt * 32 + (l & 31);
+            if (p < g.P && o < g.Co) part[((size_t)sp * g.Co + o) * g.P + p] = v;
+        }
+    }
+}
+
+// V = sum of the splits in order; readout neurons never fire.
+__global__ void k_readout_sum(const float *__restrict__ part, FGeom g, int splits,
+                              uint8_t *__restrict__ out_t, float *__restrict__ out_v)
+{
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;  // o * P + p
+    const long long n = (long long)g.Co * g.P;
+    if (i >= n) return;
+    float v = 0.0f;
+    for (int s = 0; s < splits; s++) v += part[(size_t)s * n + i];
+    const int o = (int)(i / g.P), p = (int)(i - (long long)o * g.P);
+    const int HoWo = g.Ho * g.Wo, b = p / HoWo, rem = p - b * HoWo;
+    const size_t at = ((size_t)b * g.Co + o) * HoWo + rem;
+    out_t[at] = (uint8_t)spk::kNever;
+    out_v[at] = v;
+}
+
 // Kernel variants.  Both keep the B fragments of all subtiles in registers:
 // the 32x32x16 one (S16 subtiles: 2*S16 + 4*NP*S16 registers of operands) up
 // to 19 float or 31 half subtiles, else the 16x16x32 one (R*S*4 + NP*S*4,
@@ -802,6 +1030,45 @@ const FireLauncher kFire32F16[32] = {
 #undef SPK_F32_2
 #undef SPK_F32_1
 
+int ro_splits(const FGeom &g) { return (g.S16 + kRoSteps - 1) / kRoSteps; }
+
+// Largest staged byte range of any (row group, split), remembered per geometry.
+size_t ro_halo(const FGeom &g)
+{
+    typedef std::tuple<int, int, int, int, int, int, int, int, int> Key;
+    static std::mutex mu;
+    static std::map<Key, size_t> memo;
+    const Key key{g.B, g.Ci, g.Hi, g.Wi, g.Kh, g.Kw, g.stride, g.pad, g.Ho};
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = memo.find(key);
+        if (it != memo.end()) return it->second;
+    }
+    long long best = 0;
+    const int splits = ro_splits(g);
+    for (long long p0 = 0; p0 < g.P; p0 += 32) {
+        const int p1 = (int)std::min<long long>(g.P, p0 + 32) - 1;
+        for (int sp = 0; sp < splits; sp++) {
+            long long h0, h1;
+            ro_range(g, (int)p0, p1, sp, h0, h1);
+            best = std::max(best, h1 - (h0 & ~15ll));
+        }
+    }
+    const size_t v = halo_lds(best);
+    std::lock_guard<std::mutex> lock(mu);
+    if (memo.size() > 4096) memo.clear();
+    memo[key] = v;
+    return v;
+}
+
+constexpr size_t kRoLdsMax = 96 * 1024;
+
+// The packing pass stages one padded input row or one map's weights in LDS.
+bool pack_fits(const FGeom &g)
+{
+    return (long long)g.rowb <= 64 * 1024 && (long long)g.Ci * g.Kh * g.Kw * 4 <= 64 * 1024;
+}
+
 }  // namespace
 
 namespace spk {
@@ -815,7 +1082,7 @@ bool conv_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, i
         return false;
     if ((long long)Kw * Ci > (1 << 16) || Kh > (1 << 12)) return false;
     const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
-    if (variant_of(g, half_w) == kNone) return false;
+    if (variant_of(g, half_w) == kNone || !pack_fits(g)) return false;
     if ((long long)g.rowb * g.Kh > kHaloMax) return false;  // cheap pre-check
     return group_lds(g, half_w) <= (size_t)kHaloMax;  // + at most 31 KB of staged bytes
 }
@@ -827,6 +1094,68 @@ size_t conv_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh,
     return xp_bytes(g) + bp_bytes(g, 2);
 }
 
+bool readout_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw,
+                            int stride, int pad, int Ho, int Wo)
+{
+    if (T < 1 || T > SPK_MAX_T || B < 1 || Ci < 1 || Co < 1 || Ho < 1 || Wo < 1) return false;
+    const long long Hp = Hi + 2ll * pad, Wp = Wi + 2ll * pad;
+    if ((long long)B * Ho * Wo >= (1ll << 31) || (long long)B * Hp * Wp * Ci + kSlack >= (1ll << 31))
+        return false;
+    if ((long long)Kw * Ci > (1 << 16) || Kh > (1 << 12)) return false;
+    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    if (!pack_fits(g) || (long long)ro_splits(g) * Co * g.P >= (1ll << 31)) return false;
+    if ((long long)g.rowb * (g.Kh + 2) * 2 > (long long)kRoLdsMax) return false;  // cheap pre-check
+    return ro_halo(g) + kRoRed <= kRoLdsMax;
+}
+
+size_t readout_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw,
+                              int stride, int pad, int Ho, int Wo)
+{
+    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    return xp_bytes(g) + spk::align_up(bp_bytes(g, 2), 256) +
+           (size_t)ro_splits(g) * Co * g.P * sizeof(float);
+}
+
+spk_status readout_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
+                        bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
+                        uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
+{
+    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
+    h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
+    float *part = reinterpret_cast<float *>(reinterpret_cast<char *>(ws) + xp_bytes(g) +
+                                            spk::align_up(bp_bytes(g, 2), 256));
+    launch_pack(in, w, half_w, true, g, xp, bp, s);
+    SPK_LAUNCHED("spk_conv_fire");
+
+    const int splits = ro_splits(g);
+    const int n_groups = spk::ceil_div(g.P, 32);
+    // about 512 blocks: one round at two blocks per CU, B fragments reused
+    // over several row groups
+    int iters = (int)std::max<long long>(1, spk::ceil_div((long long)n_groups * g.NT32 * splits, 512));
+    iters = std::min(iters, n_groups);
+    const size_t lds = ro_halo(g) + kRoRed;
+    dim3 grid(spk::ceil_div(n_groups, iters), g.NT32, splits);
+    if (half_w) {
+        if (lds > 64 * 1024)
+            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_readout32<1>),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_readout32<1>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups,
+                           (int)ro_halo(g), part);
+    } else {
+        if (lds > 64 * 1024)
+            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_readout32<2>),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_readout32<2>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups,
+                           (int)ro_halo(g), part);
+    }
+    SPK_LAUNCHED("spk_conv_fire");
+    const long long n = (long long)g.Co * g.P;
+    hipLaunchKernelGGL(k_readout_sum, dim3(spk::ceil_div(n, 256)), dim3(256), 0, s, part, g, splits,
+                       out_t, out_v);
+    return check_launch("spk_conv_fire");
+}
+
 spk_status conv_fire_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
                           bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
                           float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
@@ -835,18 +1164,7 @@ spk_status conv_fire_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int W
     uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
     h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
     const Variant v = variant_of(g, half_w);
-    const long long nx = (long long)g.B * g.Hp * g.rowb + kSlack;
-    const int nb_in = spk::ceil_div(nx, 256);
-    const int nb_w = v == kV32 ? spk::ceil_div((long long)g.NT32 * g.S16 * 64, 256)
-                               : spk::ceil_div((long long)g.NT * g.S * 64, 256);
-    const dim3 pg(nb_in + nb_w);
-    if (v == kV32) {
-        if (half_w) hipLaunchKernelGGL((k_pack<1, true, true>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
-        else hipLaunchKernelGGL((k_pack<2, false, true>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
-    } else {
-        if (half_w) hipLaunchKernelGGL((k_pack<1, true, false>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
-        else hipLaunchKernelGGL((k_pack<2, false, false>), pg, dim3(256), 0, s, in, w, g, nb_in, xp, bp);
-    }
+    launch_pack(in, w, half_w, v == kV32, g, xp, bp, s);
     SPK_LAUNCHED("spk_conv_fire");
 
     // Row groups per block: keep about 640 blocks in flight (two per CU with

@@ -42,6 +42,15 @@ size_t conv_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh,
 spk_status conv_fire_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
                           bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
                           float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s);
+// Readout layers (theta = +inf, no dense potentials): the split-K GEMM of the
+// last frame on the same channels-last copy (spk_conv_fast.hip).
+bool readout_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw,
+                            int stride, int pad, int Ho, int Wo);
+size_t readout_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw,
+                              int stride, int pad, int Ho, int Wo);
+spk_status readout_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
+                        bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
+                        uint8_t *out_t, float *out_v, void *ws, hipStream_t s);
 
 }  // namespace spk
 

@@ -45,17 +45,35 @@ __device__ __forceinline__ float patch_sum(const float *__restrict__ w,
     const float w0 = w[(size_t)o * taps + j];
     const float wl = w0 - L, wu = U - w0;
     float acc = init;
-#pragma unroll 8
-    for (int m = first; m < n; m += step) {
-        const Entry en = list[m];
+    auto pre_time = [&](const Entry &en) {
         const int iy = en.y * g.stride + ky - g.pad, ix = en.x * g.stride + kx - g.pad;
         const bool inside = (unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi;
         const size_t at = inside ? (((size_t)en.b * g.Ci + c) * g.Hi + iy) * g.Wi + ix : 0;
-        const int t_pre = inside ? (int)in_times[at] : spk::kNever;
+        const int t = in_times[at];
+        return inside ? t : spk::kNever;
+    };
+    auto add = [&](const Entry &en, int t_pre) {
         const float a = rate[en.q][t_pre <= en.t ? 0 : 1];
         float d = a * wl;
         d = d * wu;
         acc = acc + (stab[en.q] ? d : a);
+    };
+    // winners in batches of 8: the pre-spike loads of a batch are issued
+    // before any is used; the sum keeps the winners' order
+    int m = first;
+    for (; m + 7 * step < n; m += 8 * step) {
+        Entry en[8];
+        int tp[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) en[u] = list[m + u * step];
+#pragma unroll
+        for (int u = 0; u < 8; u++) tp[u] = pre_time(en[u]);
+#pragma unroll
+        for (int u = 0; u < 8; u++) add(en[u], tp[u]);
+    }
+    for (; m < n; m += step) {
+        const Entry en = list[m];
+        add(en, pre_time(en));
     }
     return acc;
 }

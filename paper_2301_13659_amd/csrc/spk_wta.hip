@@ -61,17 +61,27 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
     int bt = spk::kNever, bc = -1;
     float bv = 0.0f;
     if (ok) {
-        // unconditional loads, so that the unrolled iterations overlap
-#pragma unroll 4
-        for (int c = grp; c < C; c += kGroups) {
-            const int t = times[base + (size_t)c * HW];
-            const float v = vkey[base + (size_t)c * HW];
+        // maps in batches of 4: the loads of a batch are issued before any is used
+        auto take = [&](int c, int t, float v) {
             if (t != spk::kNever && (t < bt || (t == bt && v > bv))) {
                 bt = t;
                 bv = v;
                 bc = c;
             }
+        };
+        int c = grp;
+        for (; c + 3 * kGroups < C; c += 4 * kGroups) {
+            int t[4];
+            float v[4];
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                t[u] = times[base + (size_t)(c + u * kGroups) * HW];
+                v[u] = vkey[base + (size_t)(c + u * kGroups) * HW];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u++) take(c + u * kGroups, t[u], v[u]);
         }
+        for (; c < C; c += kGroups) take(c, times[base + (size_t)c * HW], vkey[base + (size_t)c * HW]);
     }
     s_t[grp][lane] = bt;
     s_v[grp][lane] = bv;
@@ -98,6 +108,47 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
             for (int c = grp; c < C; c += kGroups)
                 inhibited[base + (size_t)c * HW] = (c == wc) ? (uint8_t)wt : (uint8_t)spk::kNever;
     }
+}
+
+// Wave-wide minima with row shifts and row broadcasts (DPP) instead of LDS
+// permutes.  Lanes without a source keep the identity (all ones); every lane
+// gets the result.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_or_ones(uint32_t x)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)0xFFFFFFFF, (int)x, CTRL, ROWS, 0xf, false);
+}
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t dpp_or_ones64(uint64_t x)
+{
+    const uint32_t lo = dpp_or_ones<CTRL, ROWS>((uint32_t)x);
+    const uint32_t hi = dpp_or_ones<CTRL, ROWS>((uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x)
+{
+    x = min(x, dpp_or_ones64<0x111, 0xf>(x));  // row_shr:1
+    x = min(x, dpp_or_ones64<0x112, 0xf>(x));  // row_shr:2
+    x = min(x, dpp_or_ones64<0x114, 0xf>(x));  // row_shr:4
+    x = min(x, dpp_or_ones64<0x118, 0xf>(x));  // row_shr:8
+    x = min(x, dpp_or_ones64<0x142, 0xa>(x));  // row_bcast:15
+    x = min(x, dpp_or_ones64<0x143, 0xc>(x));  // row_bcast:31
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x)
+{
+    x = min(x, dpp_or_ones<0x111, 0xf>(x));
+    x = min(x, dpp_or_ones<0x112, 0xf>(x));
+    x = min(x, dpp_or_ones<0x114, 0xf>(x));
+    x = min(x, dpp_or_ones<0x118, 0xf>(x));
+    x = min(x, dpp_or_ones<0x142, 0xa>(x));
+    x = min(x, dpp_or_ones<0x143, 0xc>(x));
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
 // Lexicographic (hi, lo) minimum across the block; returns the winner to all.
@@ -221,11 +272,11 @@ __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__
 
 // Winner selection with the candidates of one sample held in registers: NW
 // waves, NPL candidates per thread (candidate i at thread i % (64*NW), slot
-// i / (64*NW)).  A round is a register arg-min, a wave shuffle reduction and,
+// i / (64*NW)).  A round is a register arg-min, a wave reduction (DPP) and,
 // with several waves, one exchange through LDS; the lane that owns the
 // winner writes it, and every lane retires its own candidates that share the
 // winner's map or lie in its window.
-template <int NPL, int NW>
+template <int NPL, int NW, bool kRec>
 __global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restrict__ times,
                                                         const float *__restrict__ vkey,
                                                         const Rec *__restrict__ recs, WtaArgs a,
@@ -236,41 +287,49 @@ __global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restric
     __shared__ uint32_t s_lo[2][NW];
     const int b = blockIdx.x;
     const int HW = a.H * a.W;
-    const int n = a.by_record ? HW : a.C * HW;
+    const int n = kRec ? HW : a.C * HW;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint64_t kNone = ~0ull;
     uint64_t kh[NPL];
     uint32_t kl[NPL];
     int cc[NPL], yx[NPL];
     float vv[NPL];
+    // every candidate load first (clamped index, no branch), then the keys
+    uint32_t tq[NPL];
+#pragma unroll
+    for (int j = 0; j < NPL; j++) {
+        const int ii = min(tid + j * 64 * NW, n - 1);
+        if (kRec) {
+            const Rec r = recs[(size_t)b * HW + ii];
+            tq[j] = r.tc;
+            vv[j] = r.v;
+        } else {
+            const size_t at = (size_t)b * a.C * HW + ii;
+            tq[j] = times[at];
+            vv[j] = vkey[at];
+        }
+    }
 #pragma unroll
     for (int j = 0; j < NPL; j++) {
         const int i = tid + j * 64 * NW;
-        const bool in = i < n;
-        const int ii = in ? i : 0;
+        const int ii = min(i, n - 1);
         int t, c, pos;
-        float v;
-        if (a.by_record) {
-            const Rec r = recs[(size_t)b * HW + ii];
-            t = (int)(r.tc >> 24);
-            c = (int)(r.tc & 0xFFFFFFu);
+        if (kRec) {
+            t = (int)(tq[j] >> 24);
+            c = (int)(tq[j] & 0xFFFFFFu);
             pos = ii;
-            v = r.v;
         } else {
-            const size_t at = (size_t)b * a.C * HW + ii;
-            t = times[at];
-            v = vkey[at];
+            t = (int)tq[j];
             c = ii / HW;
             pos = ii - c * HW;
         }
-        const bool alive = in && (a.readout || t != spk::kNever);
+        const bool alive = i < n && (a.readout || t != spk::kNever);
         const uint32_t tk = a.readout ? 0u : (uint32_t)t;
-        kh[j] = alive ? (((uint64_t)tk << 32) | order_desc(v)) : kNone;
+        kh[j] = alive ? (((uint64_t)tk << 32) | order_desc(vv[j])) : kNone;
         kl[j] = (uint32_t)c * (uint32_t)HW + (uint32_t)pos;
         cc[j] = c;
         const int y = pos / a.W;
         yx[j] = (y << 16) | (pos - y * a.W);
-        vv[j] = v;
     }
     int count = 0;
     for (int round = 0; round < a.k; round++) {
@@ -282,14 +341,11 @@ __global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restric
                 bh = kh[j];
                 bl = kl[j];
             }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            const uint64_t h2 = __shfl_xor(bh, o, 64);
-            const uint32_t l2 = __shfl_xor(bl, o, 64);
-            if (h2 < bh || (h2 == bh && l2 < bl)) {
-                bh = h2;
-                bl = l2;
-            }
+        {
+            // the smallest key, then the smallest index among the lanes holding it
+            const uint64_t wh = wave_min_u64(bh);
+            bl = wave_min_u32(bh == wh ? bl : ~0u);
+            bh = wh;
         }
         if (NW > 1) {
             const int slot = round & 1;
@@ -337,8 +393,12 @@ template <int NPL, int NW>
 void launch_select_reg(int B, hipStream_t s, const uint8_t *times, const float *vkey,
                        const Rec *recs, const WtaArgs &a, spk_winner *winners, int32_t *n_winners)
 {
-    hipLaunchKernelGGL((k_select_reg<NPL, NW>), dim3(B), dim3(64 * NW), 0, s, times, vkey, recs, a,
-                       winners, n_winners);
+    if (a.by_record)
+        hipLaunchKernelGGL((k_select_reg<NPL, NW, true>), dim3(B), dim3(64 * NW), 0, s, times, vkey,
+                           recs, a, winners, n_winners);
+    else
+        hipLaunchKernelGGL((k_select_reg<NPL, NW, false>), dim3(B), dim3(64 * NW), 0, s, times, vkey,
+                           recs, a, winners, n_winners);
 }
 
 }  // namespace
