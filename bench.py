@@ -31,7 +31,16 @@ PEAK_F16_MFMA_TFLOPS = 2500.0
 # scaled by a plain copy of known size; valid only while the kernel source
 # hashes to the value recorded with the counters.
 PROFILES = os.path.join(ROOT, "profiles")
-CONV_SOURCE = os.path.join(ROOT, "paper_2301_13659_amd", "csrc", "spk_conv_mfma.hip")
+CONV_SOURCES = [os.path.join(ROOT, "paper_2301_13659_amd", "csrc", f)
+                for f in ("spk_conv.hip", "spk_conv_fast.hip", "spk_conv_mfma.hip")]
+
+
+def conv_source_hash():
+    h = hashlib.sha256()
+    for f in CONV_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def parse():
@@ -61,9 +70,7 @@ def measured_traffic(wl, layer):
         if ":" in line:
             k, v = line.split(":", 1)
             rec[k.strip()] = v.strip()
-    with open(CONV_SOURCE, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()
-    if rec.get("kernel_source_sha256") != sha:
+    if rec.get("kernel_source_sha256") != conv_source_hash():
         return None
     try:
         return float(rec["fetch_bytes_per_launch"]) + float(rec["write_bytes_per_launch"])
