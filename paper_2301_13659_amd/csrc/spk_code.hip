@@ -8,9 +8,10 @@
 // values (<= min_value, NaN) get the all-ones key, sort to the end and are
 // written as never firing up front.
 //
-//  - Samples of up to kSmall values are ranked by one workgroup each: every
-//    thread sorts 8 keys in registers, then merge-path levels in LDS merge
-//    the runs (no padding to a power of two).
+//  - Samples of up to kSmall values are ranked by one workgroup each: the
+//    eligible keys are compacted, every thread sorts 8 of them in registers,
+//    then merge-path levels in LDS merge the runs (no padding to a power of
+//    two).
 //  - Larger samples: workgroups sort kSmall-key chunks in LDS, then merge
 //    passes double the sorted runs (merge-path split per thread) until each
 //    sample is one run; the ping-pong buffers live in the caller workspace.
@@ -53,6 +54,28 @@ __device__ __forceinline__ int block_sum(int v, int *red)
     tot = red[0];
     __syncthreads();
     return tot;
+}
+
+// Exclusive prefix sum of v over the block in thread order; total gets the sum.
+__device__ __forceinline__ int block_exclusive_scan(int v, int *red, int &total)
+{
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    int s = v;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(s, o, 64);
+        if (lane >= o) s += t;
+    }
+    if (lane == 63) red[wid] = s;
+    __syncthreads();
+    int before = 0, tot = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); w++) {
+        const int c = red[w];
+        before += w < wid ? c : 0;
+        tot += c;
+    }
+    __syncthreads();
+    total = tot;
+    return before + s - v;
 }
 
 // Sort 8 keys held by one thread (ascending), a fixed compare-exchange network.
@@ -98,8 +121,33 @@ __device__ void merge_level(const uint64_t *src, uint64_t *dst, int n, int width
     }
 }
 
-// Whole sample in one workgroup: keys -> register sort of 8 -> LDS merge
-// levels -> times.  n <= 8 * blockDim.
+// Merge runs of `width` sorted keys pairwise (src -> dst, n keys), one key
+// per thread at a time: a key's place in the merged run is its place in its
+// own run plus the number of keys below it in the other run (keys are unique),
+// found by binary search.
+__device__ void merge_level_rank(const uint64_t *src, uint64_t *dst, int n, int width)
+{
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+        const int lo = (e / (2 * width)) * 2 * width;
+        const int na = min(width, n - lo), nb = max(0, min(width, n - lo - width));
+        const uint64_t key = src[e];
+        const bool in_a = e < lo + na;
+        const uint64_t *other = in_a ? src + lo + na : src + lo;
+        int l = 0, h = in_a ? nb : na;
+        while (l < h) {
+            const int mid = (l + h) >> 1;
+            if (other[mid] < key) l = mid + 1;
+            else h = mid;
+        }
+        dst[lo + (in_a ? e - lo : e - lo - na) + l] = key;
+    }
+}
+
+// Whole sample in one workgroup.  The eligible keys are compacted first (in
+// index order, by a block prefix sum), then only those are sorted: register
+// sort of 8, LDS merge levels by rank; rank r of the N sorted keys fires at
+// r*T/N.
+// n <= 8 * blockDim.
 __global__ __launch_bounds__(kThreads) void k_code_small(const float *__restrict__ x, int n, int T,
                                                          float min_value,
                                                          uint8_t *__restrict__ times)
@@ -126,15 +174,25 @@ __global__ __launch_bounds__(kThreads) void k_code_small(const float *__restrict
         }
         k8[j] = key;
     }
-    const int N = block_sum(mine, red);
-    sort8(k8);
+    int N;
+    int w = block_exclusive_scan(mine, red, N);
     uint64_t *src = keys, *dst = keys + n;
 #pragma unroll
     for (int j = 0; j < 8; j++)
-        if (first + j < n) src[first + j] = k8[j];
+        if (k8[j] != kDead) src[w++] = k8[j];
     __syncthreads();
-    for (int width = 8; width < n; width *= 2) {
-        merge_level(src, dst, n, width);
+    if (N == 0) return;
+    if (first < N) {
+#pragma unroll
+        for (int j = 0; j < 8; j++) k8[j] = first + j < N ? src[first + j] : kDead;
+        sort8(k8);
+#pragma unroll
+        for (int j = 0; j < 8; j++)
+            if (first + j < N) src[first + j] = k8[j];
+    }
+    __syncthreads();
+    for (int width = 8; width < N; width *= 2) {
+        merge_level_rank(src, dst, N, width);
         __syncthreads();
         uint64_t *t = src;
         src = dst;
