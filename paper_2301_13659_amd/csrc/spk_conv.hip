@@ -94,6 +94,10 @@ extern "C" size_t spk_conv_fire_workspace_size(int B, int T, int Ci, int Hi, int
     if (readout && spk::readout_fast_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo))
         need = std::max(need,
                         spk::readout_fast_workspace(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo));
+    for (int hw = 0; hw < 2; hw++)
+        if (spk::conv_pt_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, hw != 0, readout,
+                                   potentials != 0))
+            need = std::max(need, spk::conv_pt_workspace(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo));
     return need;
 }
 
@@ -127,6 +131,10 @@ extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int C
                 "spk_conv_fire: workspace of %zu bytes needed, %zu given", need, ws_bytes);
     SPK_REQUIRE((long long)B * Ho * Wo < (1LL << 31) && (long long)Ci * Hi * Wi < (1LL << 31),
                 SPK_E_SHAPE, "spk_conv_fire: layer too large");
+    if (spk::conv_pt_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, half_w, readout,
+                               potentials != nullptr))
+        return spk::conv_fire_pt(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho, Wo,
+                                 theta, out_times, out_vkey, ws, spk::stream_of(stream));
     if (spk::conv_fast_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, half_w, readout,
                                  potentials != nullptr))
         return spk::conv_fire_fast(in_times, B, T, Ci, Hi, Wi, w, half_w, Co, Kh, Kw, stride, pad, Ho,

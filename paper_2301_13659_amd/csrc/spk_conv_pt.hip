@@ -1,0 +1,685 @@
+// spk_conv_fire, firing layers with T <= 32: one matrix-core product per
+// tile computes the potentials of every time step at once (Spyker §II-E.1
+// Eq. 2; first-spike firing of §II-D.3 and §II-E).
+//
+// Under rank-order coding frame t is the cumulative S_t = [time <= t], so
+// V_t = W * S_t for every step independently.  The implicit GEMM here puts
+// (position, step) pairs on the MFMA rows: a 32x32x16 tile holds 32 / TP
+// output positions x TP steps (TP = 8, 16 or 32 >= T; rows past T - 1 repeat
+// step T - 1) against 32 maps, and its 16-tap depth slices walk the kernel
+// window.  The A fragment of row (p, t) is [time <= t] over 8 taps, one
+// packed-half subtraction with clamping per pair of taps.  The first crossing
+// of theta and the potential that goes with it are read off the finished
+// tile, with no state carried across steps.
+//
+// Operands (in the caller's workspace, written by k_pack_pt):
+//  - Xp: the time map as padded channels-last bytes, Xp[b][iy][ix][c] over
+//    (Hi + 2 pad) x (Wi + 2 pad) x Cp, each time clamped to T (T and above
+//    never fire within the window; padding and the channels past Ci hold T).
+//    Cp is Ci rounded up to 8 when that adds no depth, so window runs start
+//    aligned;
+//  - the depth is ordered (ky, j), j = kx*Cp + c, each kernel row's run of
+//    Kw*Cp taps padded to a multiple of 16, so a 16-tap slice never straddles
+//    two kernel rows and its offset from the window origin is
+//    ky*rowbytes + 16*jq for every position;
+//  - the weights as ready B fragments in that order: hi/lo halves of the
+//    float master (two products per slice) or the half weights; zero on
+//    padding taps.
+//
+// Work split: a block (4 waves) keeps the B fragments of one 32-map column
+// tile in registers and walks one contiguous range of positions in groups of
+// 64.  Ranges divide the positions evenly over about two blocks per CU, so
+// every SIMD gets the same work; the blocks of one range sit on one XCD and
+// share its L2 for the input bytes.  A group's input rows are loaded into
+// registers one group ahead and stored to LDS as the halves 1024 + t that the
+// A fragments subtract from (with a flag per 16 bytes that says whether any
+// of them fires).  Results go through LDS so that each map's run of positions
+// is written with coalesced stores.  In a sparse group, the 16-tap slices in
+// which no input of the tile fires are skipped.
+#include <hip/hip_fp16.h>
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <tuple>
+
+#include "spk_internal.h"
+
+namespace {
+
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f16v __attribute__((ext_vector_type(16)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kG = 64;                         // positions per group
+constexpr int kStageStride = kG + 1;           // staged results: [map][position], padded
+constexpr int kRange = 16 * 1024;              // Xp bytes of a group's input rows (at most)
+constexpr int kPf = kRange / 16 / kThreads;    // 16-byte words per thread of a group's input
+constexpr int kSlackPT = 64;                   // readable bytes past the end of Xp
+constexpr uint32_t kSelLo = 0x04010400u;       // bytes 0,1 -> halves 1024 + b
+constexpr uint32_t kSelHi = 0x04030402u;       // bytes 2,3 -> halves 1024 + b
+
+// LDS: [input as halves (2 * kRange) | fire flag per 16 bytes | staged V x 2 |
+// staged t x 2 | position table x 3]
+constexpr size_t kFlagOff = 2 * (size_t)kRange;
+constexpr size_t kStvOff = kFlagOff + kRange / 16;
+constexpr size_t kSttOff = kStvOff + 2 * 32 * kStageStride * sizeof(float);
+constexpr size_t kTabOff = (kSttOff + 2 * 32 * kStageStride + 15) / 16 * 16;
+
+struct PGeom {
+    int B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo;
+    int Cp;    // channels per padded pixel of Xp
+    int Hp, Wp;
+    int rowb;  // Wp * Cp: bytes of one padded input row
+    int run;   // Kw * Cp: taps of one kernel row
+    int Q16;   // ceil(run / 16): 16-tap slices per kernel row
+    int SK;    // Kh * Q16: slices of the layer
+    int SKp;   // slices of the kernel instance (>= SK; the extra ones are zero)
+    int P;     // B * Ho * Wo
+    int NT;    // ceil(Co / 32)
+    int TP;    // steps per position in a tile: 8, 16 or 32
+    int lgTP;
+};
+
+int choose_cp(int Ci, int Kw)
+{
+    const int c8 = (Ci + 7) / 8 * 8;
+    return (Kw * c8 + 15) / 16 == (Kw * Ci + 15) / 16 ? c8 : Ci;
+}
+
+PGeom make_pgeom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride, int pad,
+                 int Ho, int Wo)
+{
+    PGeom g{};
+    g.B = B; g.T = T; g.Ci = Ci; g.Hi = Hi; g.Wi = Wi; g.Co = Co; g.Kh = Kh; g.Kw = Kw;
+    g.stride = stride; g.pad = pad; g.Ho = Ho; g.Wo = Wo;
+    g.Cp = choose_cp(Ci, Kw);
+    g.Hp = Hi + 2 * pad;
+    g.Wp = Wi + 2 * pad;
+    g.rowb = g.Wp * g.Cp;
+    g.run = Kw * g.Cp;
+    g.Q16 = (g.run + 15) / 16;
+    g.SK = Kh * g.Q16;
+    g.SKp = g.SK;
+    g.P = B * Ho * Wo;
+    g.NT = (Co + 31) / 32;
+    g.TP = T <= 8 ? 8 : (T <= 16 ? 16 : 32);
+    g.lgTP = T <= 8 ? 3 : (T <= 16 ? 4 : 5);
+    return g;
+}
+
+// Alignment of every window run in the staged halves: 16, 8, 4 or 2 bytes.
+int read_mode(int Cp) { return Cp % 8 == 0 ? 3 : (Cp % 4 == 0 ? 2 : (Cp % 2 == 0 ? 1 : 0)); }
+
+size_t xp_bytes(const PGeom &g) { return spk::align_up((size_t)g.B * g.Hp * g.rowb + kSlackPT, 256); }
+size_t bp_bytes(const PGeom &g, int np) { return (size_t)g.NT * g.SKp * np * 64 * sizeof(h8); }
+
+__device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
+__device__ __forceinline__ uint32_t as_u(h2 h) { return __builtin_bit_cast(uint32_t, h); }
+
+// [t <= last] for two staged halves 1024 + t (c = 1025 + last in both):
+// c - (1024 + t) is a small exact integer, >= 1 iff t <= last; clamp to [0, 1].
+__device__ __forceinline__ uint32_t upto2(uint32_t x, h2 c)
+{
+    const h2 one = {(_Float16)1.0f, (_Float16)1.0f}, zero = {(_Float16)0.0f, (_Float16)0.0f};
+    h2 a = c - as_h2(x);
+    return as_u(__builtin_elementwise_min(__builtin_elementwise_max(a, zero), one));
+}
+
+__device__ __forceinline__ h8 frag_upto(u4 x, h2 c)
+{
+    u4 v = {upto2(x[0], c), upto2(x[1], c), upto2(x[2], c), upto2(x[3], c)};
+    return __builtin_bit_cast(h8, v);
+}
+
+// 8 staged halves (16 bytes) at byte offset at from base (16-aligned); kMode
+// gives the alignment every window run has: 3 = 16, 2 = 8, 1 = 4, 0 = 2 bytes.
+template <int kMode>
+__device__ __forceinline__ u4 lds_read16(const uint8_t *base, int at)
+{
+    if (kMode == 3) return *reinterpret_cast<const u4 *>(base + at);
+    if (kMode == 2) {
+        const uint2 a = *reinterpret_cast<const uint2 *>(base + at);
+        const uint2 b = *reinterpret_cast<const uint2 *>(base + at + 8);
+        return u4{a.x, a.y, b.x, b.y};
+    }
+    if (kMode == 1) {
+        const uint32_t *w = reinterpret_cast<const uint32_t *>(base + at);
+        return u4{w[0], w[1], w[2], w[3]};
+    }
+    const uint32_t *w = reinterpret_cast<const uint32_t *>(base + (at & ~3));
+    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3], w4 = w[4];
+    const uint32_t sh = (uint32_t)(at & 3);
+    return u4{__builtin_amdgcn_alignbyte(w1, w0, sh), __builtin_amdgcn_alignbyte(w2, w1, sh),
+              __builtin_amdgcn_alignbyte(w3, w2, sh), __builtin_amdgcn_alignbyte(w4, w3, sh)};
+}
+
+// Padded input rows [r0, r1) hold the windows of output positions [p0, p1].
+__host__ __device__ inline void group_rows(const PGeom &g, int p0, int p1, int &r0, int &r1)
+{
+    const int HoWo = g.Ho * g.Wo;
+    const int b0 = p0 / HoWo, y0 = (p0 - b0 * HoWo) / g.Wo;
+    const int b1 = p1 / HoWo, y1 = (p1 - b1 * HoWo) / g.Wo;
+    r0 = b0 * g.Hp + y0 * g.stride;
+    r1 = b1 * g.Hp + y1 * g.stride + g.Kh;
+}
+
+// ------------------------------------------------------------------ packing
+
+// Blocks [0, B*Hp): one padded input row (b, py) each, transposed through LDS
+// from channel rows to channels-last, times clamped to T; the last of them
+// fills the readable slack.  Blocks [B*Hp, B*Hp + 32*NT): one map o each
+// (maps past Co are zero), written as B fragments: lane l holds map o (l % 32)
+// and taps 8*(l/32)..+7 of a slice.
+template <int NP, bool kHalfW>
+__global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
+                                                 const void *__restrict__ wv, PGeom g, int nb_in,
+                                                 uint8_t *__restrict__ xp, h8 *__restrict__ bp)
+{
+    extern __shared__ __align__(16) uint8_t sm[];
+    const uint8_t never = (uint8_t)g.T;
+    if ((int)blockIdx.x < nb_in) {
+        const int b = blockIdx.x / g.Hp, py = blockIdx.x - b * g.Hp;
+        const int iy = py - g.pad;
+        uint8_t *row = xp + ((size_t)b * g.Hp + py) * g.rowb;
+        if ((unsigned)iy < (unsigned)g.Hi) {
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = never;
+            __syncthreads();
+            const uint8_t *src = in + (size_t)b * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi;
+            const int n = g.Ci * g.Wi;
+            for (int e = threadIdx.x; e < n; e += blockDim.x) {
+                const int c = e / g.Wi, x = e - c * g.Wi;
+                const uint8_t v = src[(size_t)c * g.Hi * g.Wi + x];
+                sm[(x + g.pad) * g.Cp + c] = v < never ? v : never;
+            }
+            __syncthreads();
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = sm[e];
+        } else {
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = never;
+        }
+        if ((int)blockIdx.x == nb_in - 1)
+            for (int e = threadIdx.x; e < kSlackPT; e += blockDim.x) row[g.rowb + e] = never;
+        return;
+    }
+    const int o = blockIdx.x - nb_in;
+    const int taps = g.Ci * g.Kh * g.Kw;
+    float *wl = reinterpret_cast<float *>(sm);
+    const bool real = o < g.Co;
+    for (int e = threadIdx.x; e < taps; e += blockDim.x) {
+        float w = 0.0f;
+        if (real) {
+            const size_t at = (size_t)o * taps + e;
+            w = kHalfW ? (float)reinterpret_cast<const _Float16 *>(wv)[at]
+                       : reinterpret_cast<const float *>(wv)[at];
+        }
+        wl[e] = w;
+    }
+    __syncthreads();
+    const int nt = o / 32, col = o & 31;
+    for (int f = threadIdx.x; f < g.SKp * 2; f += blockDim.x) {
+        const int s = f >> 1, half = f & 1;
+        const int ky = s / g.Q16, jq = s - ky * g.Q16;
+        h8 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            const int j = jq * 16 + half * 8 + e;
+            const int kx = j / g.Cp, c = j - kx * g.Cp;
+            float w = 0.0f;
+            if (s < g.SK && j < g.run && c < g.Ci) w = wl[(c * g.Kh + ky) * g.Kw + kx];
+            const _Float16 hw = (_Float16)w;
+            hi[e] = hw;
+            lo[e] = (_Float16)(w - (float)hw);
+        }
+        const size_t ts = (size_t)nt * g.SKp + s;
+        const int lane = col + 32 * half;
+        bp[(ts * NP) * 64 + lane] = hi;
+        if (NP == 2) bp[(ts * NP + 1) * 64 + lane] = lo;
+    }
+}
+
+// -------------------------------------------------------------------- firing
+
+struct Tab {
+    int xoff;   // Xp offset of the position's window origin
+    int obase;  // output offset of the position for map 0: b*Co*Ho*Wo + y*Wo + x
+};
+
+// Per-group position table (threads 0..kG-1; slots past the group repeat its last).
+__device__ __forceinline__ void fill_table(const PGeom &g, int gs, int cnt, Tab *tab)
+{
+    const int i = threadIdx.x;
+    if (i < kG) {
+        const int p = gs + min(i, cnt - 1);
+        const int HoWo = g.Ho * g.Wo;
+        const int b = p / HoWo, rem = p - b * HoWo;
+        const int y = rem / g.Wo, x = rem - y * g.Wo;
+        Tab t;
+        t.xoff = (b * g.Hp + y * g.stride) * g.rowb + x * g.stride * g.Cp;
+        t.obase = b * g.Co * HoWo + rem;
+        tab[i] = t;
+    }
+}
+
+// The Xp bytes [a0, a1 + 32) (a0 16-aligned) as 16-byte words, kPf per
+// thread (word threadIdx.x + 256*i); words past the end of Xp read its last.
+struct Staged {
+    uint4 w[kPf];
+};
+
+__device__ __forceinline__ int range_words(int a0, int a1) { return (a1 - a0 + 32 + 15) / 16; }
+
+__device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words, int a0, int a1)
+{
+    Staged st;
+    const size_t w0 = (size_t)a0 / 16;
+    const int nw = range_words(a0, a1);
+#pragma unroll
+    for (int i = 0; i < kPf; i++) {
+        const int k = (int)threadIdx.x + kThreads * i;
+        size_t w = w0 + (size_t)min(k, nw - 1);
+        w = w < xp_words ? w : xp_words - 1;
+        st.w[i] = k < nw ? reinterpret_cast<const uint4 *>(xp)[w] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    return st;
+}
+
+// Staged words to LDS as halves 1024 + t, plus a flag per word: does any of
+// its 16 times fire within the window (clamped times: any byte below T)?
+// Returns, uniform over the wave, whether under 80% of the wave's words of
+// the range [0, nw) are flagged: a sparse range, worth testing slices in.
+__device__ __forceinline__ bool store_range(const Staged &st, uint8_t *lds, uint32_t never4, int nw)
+{
+    int flagged = 0, words = 0;
+#pragma unroll
+    for (int i = 0; i < kPf; i++) {
+        const int k = (int)threadIdx.x + kThreads * i;
+        const uint4 v = st.w[i];
+        const u4 lo = {__builtin_amdgcn_perm(0x64646464u, v.x, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.x, kSelHi),
+                       __builtin_amdgcn_perm(0x64646464u, v.y, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.y, kSelHi)};
+        const u4 hi = {__builtin_amdgcn_perm(0x64646464u, v.z, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.z, kSelHi),
+                       __builtin_amdgcn_perm(0x64646464u, v.w, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.w, kSelHi)};
+        reinterpret_cast<u4 *>(lds)[2 * k] = lo;
+        reinterpret_cast<u4 *>(lds)[2 * k + 1] = hi;
+        const bool f = ((v.x ^ never4) | (v.y ^ never4) | (v.z ^ never4) | (v.w ^ never4)) != 0u;
+        lds[kFlagOff + k] = f ? 1 : 0;
+        flagged += __builtin_popcountll(__builtin_amdgcn_ballot_w64(f && k < nw));
+        words += __builtin_popcountll(__builtin_amdgcn_ballot_w64(k < nw));
+    }
+    return flagged * 5 < words * 4;
+}
+
+// Staged results of positions [gs, min(gs + 64, p_end)) to the outputs:
+// consecutive threads take consecutive positions of one map.
+__device__ __forceinline__ void write_out(const PGeom &g, int nt, int gs, int p_end, const Tab *tab,
+                                          const float *stv, const uint8_t *stt,
+                                          uint8_t *__restrict__ out_t, float *__restrict__ out_v)
+{
+    const int HoWo = g.Ho * g.Wo;
+    const int cnt = min(p_end, gs + kG) - gs;
+    for (int idx = threadIdx.x; idx < 32 * kG; idx += kThreads) {
+        const int pi = idx & (kG - 1), oc = idx / kG;
+        const int o = nt * 32 + oc;
+        if (pi < cnt && o < g.Co) {
+            const int n = tab[pi].obase + o * HoWo;
+            out_v[n] = stv[oc * kStageStride + pi];
+            out_t[n] = stt[oc * kStageStride + pi];
+        }
+    }
+}
+
+// Merge the two wave halves of one position slot (ft: step or NEVER; last:
+// the potential at step T-1, meaningful in the upper half only).
+__device__ __forceinline__ void merge_halves(uint32_t ft, float fv, float last, int hh, uint32_t &tf,
+                                             float &vk)
+{
+    const auto t2 = __builtin_amdgcn_permlane32_swap(ft, ft, false, false);
+    const uint32_t fb = __builtin_bit_cast(uint32_t, fv);
+    const auto v2 = __builtin_amdgcn_permlane32_swap(fb, fb, false, false);
+    const uint32_t lb = __builtin_bit_cast(uint32_t, hh ? last : 0.0f);
+    const auto l2 = __builtin_amdgcn_permlane32_swap(lb, lb, false, false);
+    // every lane now holds both halves' values (in either order): x + 0 = x
+    const uint32_t t0 = t2[0], t1 = t2[1];
+    const float f0 = __builtin_bit_cast(float, (uint32_t)v2[0]);
+    const float f1 = __builtin_bit_cast(float, (uint32_t)v2[1]);
+    const float vl = __builtin_bit_cast(float, (uint32_t)l2[0]) + __builtin_bit_cast(float, (uint32_t)l2[1]);
+    tf = min(t0, t1);
+    const float fsel = t0 < t1 ? f0 : f1;
+    vk = tf < (uint32_t)spk::kNever ? fsel : vl;
+}
+
+// Epilogue of a tile with TP steps per position: element e of a lane is row
+// 8*(e/4) + 4*hh + e%4 (steps ascend with e), map lane % 32.  Per position
+// slot (TP/2 elements per lane): the first element above theta, then the two
+// wave halves merged into the spike time and key potential.
+template <int TP>
+__device__ __forceinline__ void tile_epilogue(const f16v &acc, float theta, int hh, uint32_t *st, float *sv)
+{
+    constexpr int EP = TP / 2;
+#pragma unroll
+    for (int k = 0; k < 32 / TP; k++) {
+        int fe = 16;
+        float fv = 0.0f;
+#pragma unroll
+        for (int e = (k + 1) * EP - 1; e >= k * EP; e--) {
+            const bool c = acc[e] > theta;
+            fe = c ? e : fe;
+            fv = c ? acc[e] : fv;
+        }
+        const uint32_t ft = fe < 16 ? (uint32_t)((((fe >> 2) << 3) + 4 * hh + (fe & 3)) & (TP - 1))
+                                    : (uint32_t)spk::kNever;
+        merge_halves(ft, fv, acc[(k + 1) * EP - 1], hh, st[k], sv[k]);
+    }
+}
+
+// SK: slices of the instance (all in registers), NP: 2 = hi/lo products of a
+// float master, 1 = half weights; kMode: alignment of the window runs.
+template <int SK, int NP, int kMode>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__restrict__ bp, PGeom g,
+               float theta, int nranges,
+               uint8_t *__restrict__ out_t, float *__restrict__ out_v)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    uint8_t *hal = lds;
+    const uint8_t *flag = lds + kFlagOff;
+    auto stv = [&](int i) { return reinterpret_cast<float *>(lds + kStvOff) + i * 32 * kStageStride; };
+    auto stt = [&](int i) { return lds + kSttOff + i * 32 * kStageStride; };
+    Tab *tabs = reinterpret_cast<Tab *>(lds + kTabOff);
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // block -> (column tile, range); the NT blocks of a range share an XCD
+    const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
+    const int nt = q % g.NT;
+    const int range = xcd + 8 * (q / g.NT);
+    if (range >= nranges) return;
+    const int p_begin = (int)((long long)range * g.P / nranges);
+    const int p_end = (int)((long long)(range + 1) * g.P / nranges);
+    if (p_begin >= p_end) return;
+
+    h8 bw[SK][NP];
+#pragma unroll
+    for (int s = 0; s < SK; s++)
+#pragma unroll
+        for (int k = 0; k < NP; k++) bw[s][k] = bp[((size_t)(nt * SK + s) * NP + k) * 64 + lane];
+
+    // slice offsets from the window origin, in bytes of staged halves
+    // (slices past the layer's read the origin; their B is zero)
+    int off2[SK];
+#pragma unroll
+    for (int s = 0; s < SK; s++) {
+        const int ky = s / g.Q16, jq = s - ky * g.Q16;
+        off2[s] = s < g.SK ? 2 * (ky * g.rowb + jq * 16) : 0;
+    }
+    // this lane's slice for the fire flags of a tile (lanes past SK: none)
+    const int my_off = lane < g.SK ? (lane / g.Q16) * g.rowb + (lane % g.Q16) * 16 : -1;
+
+    // row (p, t) of this lane: slot p = r / TP, step t = r % TP (capped at T - 1)
+    const int r = lane & 31, hh = lane >> 5;
+    const int pl = r >> g.lgTP, tt = r & (g.TP - 1);
+    const uint32_t cbv = 0x6401u + (uint32_t)min(tt, g.T - 1);
+    const h2 cc = as_h2(cbv | (cbv << 16));
+    const int PT = 32 >> g.lgTP;  // positions per tile
+    const uint32_t never4 = 0x01010101u * (uint32_t)g.T;
+
+    bool sparse;
+    {
+        int r0, r1;
+        group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
+        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, never4, range_words(a0, a1));
+        fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
+    }
+
+    // Group it: computed from the staged input and table[it % 3] into
+    // stage[it % 2]; its results are written out during group it + 1 (or
+    // after the loop).  The next group's input is loaded into registers
+    // during this one and stored once every wave is done with this one.
+    int it = 0;
+    for (int gs = p_begin; gs < p_end; gs += kG, it++) {
+        const int cnt = min(p_end, gs + kG) - gs;
+        const int cur = it & 1;
+        const Tab *tab = tabs + (it % 3) * kG;
+        int r0, r1;
+        group_rows(g, gs, gs + cnt - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15;
+        __syncthreads();  // this group's input and table are in LDS; group it-1 is staged
+        const int gn = gs + kG;
+        const bool more = gn < p_end;
+        Staged nxt;
+        int nxt_words = 0;
+        if (more) {
+            int n0, n1;
+            group_rows(g, gn, min(p_end, gn + kG) - 1, n0, n1);
+            const int b0 = (n0 * g.rowb) & ~15, b1 = n1 * g.rowb;
+            nxt = load_range(xp, xp_words, b0, b1);
+            nxt_words = range_words(b0, b1);
+            fill_table(g, gn, min(p_end, gn + kG) - gn, tabs + ((it + 1) % 3) * kG);
+        }
+        if (it > 0)
+            write_out(g, nt, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1), stt(cur ^ 1), out_t, out_v);
+        // tiles of the group go round the waves
+        const int wp0 = gs + wv * PT, wp1 = gs + cnt, wstep = 4 * PT;
+        int xo_next = tab[min(wp0 - gs + pl, cnt - 1)].xoff;
+        for (int tp0 = wp0; tp0 < wp1; tp0 += wstep) {
+            // this lane's window origin (taps from the staged range start)
+            const int org2 = 2 * (xo_next - a0 + 8 * hh);
+            auto rd = [&](int s) -> u4 { return lds_read16<kMode>(hal, org2 + off2[s]); };
+            f16v acc;
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[e] = 0.0f;
+            auto step = [&](int s, u4 x) {
+                const h8 a = frag_upto(x, cc);
+#pragma unroll
+                for (int k = 0; k < NP; k++) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bw[s][k], acc, 0, 0, 0);
+            };
+            // slices to compute: all, or in a sparse group those where an input
+            // of some position of the tile fires (a slice's 16 bytes lie in at
+            // most two flagged words)
+            uint64_t live = ~0ull;
+            if (sparse) {
+                live = 0ull;
+                for (int j = 0; j < PT; j++) {
+                    const int xo = tab[min(tp0 - gs + j, cnt - 1)].xoff - a0;
+                    bool f = false;
+                    if (my_off >= 0) {
+                        const int at = xo + my_off;
+                        f = (flag[at >> 4] | flag[(at + 15) >> 4]) != 0;
+                    }
+                    live |= __builtin_amdgcn_ballot_w64(f);
+                }
+            }
+            // reads run three slices ahead of the products; the dense form
+            // has no branch between slices
+            constexpr int kAhead = 3;
+            u4 win[kAhead];
+#pragma unroll
+            for (int s = 0; s < kAhead && s < SK; s++) win[s] = rd(s);
+            if (!sparse) {
+#pragma unroll
+                for (int s = 0; s < SK; s++) {
+                    const u4 x = win[s % kAhead];
+                    if (s + kAhead < SK) win[s % kAhead] = rd(s + kAhead);
+                    step(s, x);
+                }
+            } else {
+#pragma unroll
+                for (int s = 0; s < SK; s++) {
+                    const u4 x = win[s % kAhead];
+                    if (s + kAhead < SK) win[s % kAhead] = rd(s + kAhead);
+                    if (__builtin_expect((live >> s) & 1ull, 1)) step(s, x);
+                }
+            }
+            // the next tile's window origin, read while this one finishes
+            if (tp0 + wstep < wp1) xo_next = tab[min(tp0 + wstep - gs + pl, cnt - 1)].xoff;
+            uint32_t st[4] = {0u, 0u, 0u, 0u};
+            float sv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (g.lgTP == 3) tile_epilogue<8>(acc, theta, hh, st, sv);
+            else if (g.lgTP == 4) tile_epilogue<16>(acc, theta, hh, st, sv);
+            else tile_epilogue<32>(acc, theta, hh, st, sv);
+            const int o = lane & 31;
+            if (hh == 0) {
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    const int pi = tp0 - gs + k;
+                    if (k < PT && pi < cnt) {
+                        stv(cur)[o * kStageStride + pi] = sv[k];
+                        stt(cur)[o * kStageStride + pi] = (uint8_t)st[k];
+                    }
+                }
+            }
+        }
+        if (more) {
+            __syncthreads();  // every wave is done with this group's input
+            sparse = store_range(nxt, hal, never4, nxt_words);
+        }
+    }
+    __syncthreads();  // the last group is staged
+    write_out(g, nt, p_begin + (it - 1) * kG, p_end, tabs + ((it - 1) % 3) * kG, stv((it - 1) & 1),
+              stt((it - 1) & 1), out_t, out_v);
+}
+
+// Kernel instances: slice counts rounded up to these (the extra slices have
+// zero weights).  Float masters (hi/lo) keep 4*2*SK registers of B fragments,
+// halves 4*SK: both up to 144.
+constexpr int kSK2[] = {2, 4, 6, 8, 10, 12, 14, 16, 18};
+constexpr int kSK1[] = {4, 8, 12, 16, 20, 24, 28, 32, 36};
+
+int instance_sk(int SK, bool half_w)
+{
+    const int *t = half_w ? kSK1 : kSK2;
+    for (int i = 0; i < 9; i++)
+        if (SK <= t[i]) return t[i];
+    return 0;
+}
+
+typedef void (*PtLaunch)(dim3, size_t, hipStream_t, const uint8_t *, size_t, const h8 *, const PGeom &,
+                         float, int, uint8_t *, float *);
+
+template <int SK, int NP, int kMode>
+void launch_pt(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t xw, const h8 *bp,
+               const PGeom &g, float theta, int nranges, uint8_t *ot, float *ov)
+{
+    hipLaunchKernelGGL((k_fire_pt<SK, NP, kMode>), grid, dim3(kThreads), lds, s, xp, xw, bp, g, theta,
+                       nranges, ot, ov);
+}
+
+#define SPK_PT(S, N) {&launch_pt<S, N, 0>, &launch_pt<S, N, 1>, &launch_pt<S, N, 2>, &launch_pt<S, N, 3>}
+const PtLaunch kLaunch2[9][4] = {SPK_PT(2, 2),  SPK_PT(4, 2),  SPK_PT(6, 2),  SPK_PT(8, 2), SPK_PT(10, 2),
+                                 SPK_PT(12, 2), SPK_PT(14, 2), SPK_PT(16, 2), SPK_PT(18, 2)};
+const PtLaunch kLaunch1[9][4] = {SPK_PT(4, 1),  SPK_PT(8, 1),  SPK_PT(12, 1), SPK_PT(16, 1), SPK_PT(20, 1),
+                                 SPK_PT(24, 1), SPK_PT(28, 1), SPK_PT(32, 1), SPK_PT(36, 1)};
+#undef SPK_PT
+
+// Largest staged row range over the groups of every range (exact, per geometry).
+int max_rows(const PGeom &g, int nranges)
+{
+    typedef std::tuple<int, int, int, int, int, int, int, int, int> Key;
+    static std::mutex mu;
+    static std::map<Key, int> memo;
+    const Key key{g.B, g.Hi, g.Wi, g.Kh, g.stride, g.pad, g.Ho, g.Wo, nranges};
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = memo.find(key);
+        if (it != memo.end()) return it->second;
+    }
+    int best = 0;
+    for (int rg = 0; rg < nranges; rg++) {
+        const int pb = (int)((long long)rg * g.P / nranges), pe = (int)((long long)(rg + 1) * g.P / nranges);
+        for (int gs = pb; gs < pe; gs += kG) {
+            int r0, r1;
+            group_rows(g, gs, std::min(pe, gs + kG) - 1, r0, r1);
+            best = std::max(best, r1 - r0);
+        }
+    }
+    std::lock_guard<std::mutex> lock(mu);
+    if (memo.size() > 4096) memo.clear();
+    memo[key] = best;
+    return best;
+}
+
+int cu_count()
+{
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            n = v;
+        else
+            n = 256;
+    }
+    return n;
+}
+
+int n_ranges(const PGeom &g)
+{
+    const int target = 2 * cu_count();
+    int nr = std::max(1, target / g.NT);
+    nr = std::min(nr, std::max(1, g.P / 16));
+    return nr;
+}
+
+size_t fire_lds() { return kTabOff + 3 * kG * sizeof(Tab); }
+
+}  // namespace
+
+namespace spk {
+
+bool conv_pt_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                       int pad, int Ho, int Wo, bool half_w, bool readout, bool potentials)
+{
+    if (readout || potentials || T < 1 || T > 32 || B < 1 || Ci < 1 || Co < 1 || Ho < 1 || Wo < 1)
+        return false;
+    const long long Hp = Hi + 2ll * pad, Wp = Wi + 2ll * pad;
+    const int Cp = choose_cp(Ci, Kw);
+    if ((long long)B * Hp * Wp * Cp + kSlackPT >= (1ll << 30)) return false;
+    if ((long long)B * Co * Ho * Wo >= (1ll << 31)) return false;
+    if (Wp * Cp > 48 * 1024 || (long long)Ci * Kh * Kw * 4 > 64 * 1024) return false;
+    const PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    if (instance_sk(g.SK, half_w) == 0) return false;
+    // a group's rows, with the 16-byte alignment in front and 32 bytes of over-read
+    const long long rows = max_rows(g, n_ranges(g));
+    return rows * g.rowb + 64 <= kRange;
+}
+
+size_t conv_pt_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                         int pad, int Ho, int Wo)
+{
+    PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    g.SKp = std::max(instance_sk(g.SK, false), instance_sk(g.SK, true));
+    if (g.SKp == 0) g.SKp = g.SK;
+    return xp_bytes(g) + bp_bytes(g, 2);
+}
+
+spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
+                        bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
+                        float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
+{
+    PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    g.SKp = instance_sk(g.SK, half_w);
+    uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
+    h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
+    const int nb_in = g.B * g.Hp;
+    const size_t plds = std::max((size_t)g.rowb, (size_t)g.Ci * g.Kh * g.Kw * sizeof(float));
+    const dim3 pgrid(nb_in + g.NT * 32);
+    if (half_w)
+        hipLaunchKernelGGL((k_pack_pt<1, true>), pgrid, dim3(256), plds, s, in, w, g, nb_in, xp, bp);
+    else
+        hipLaunchKernelGGL((k_pack_pt<2, false>), pgrid, dim3(256), plds, s, in, w, g, nb_in, xp, bp);
+    SPK_LAUNCHED("spk_conv_fire");
+
+    const int nranges = n_ranges(g);
+    const int per_xcd = (nranges + 7) / 8;
+    const dim3 grid(8 * g.NT * per_xcd);
+    const size_t xw = ((size_t)g.B * g.Hp * g.rowb + kSlackPT) / 16;
+    int idx = 0;
+    while ((half_w ? kSK1 : kSK2)[idx] != g.SKp) idx++;
+    const PtLaunch launch = (half_w ? kLaunch1 : kLaunch2)[idx][read_mode(g.Cp)];
+    launch(grid, fire_lds(), s, xp, xw, bp, g, theta, nranges, out_t, out_v);
+    return check_launch("spk_conv_fire");
+}
+
+}  // namespace spk

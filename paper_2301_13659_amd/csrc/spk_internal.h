@@ -42,6 +42,15 @@ size_t conv_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh,
 spk_status conv_fire_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
                           bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
                           float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s);
+// Firing layers with T <= 32 whose weights fit a wave's registers: every
+// step of a tile in one matrix-core product (spk_conv_pt.hip).
+bool conv_pt_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                       int pad, int Ho, int Wo, bool half_w, bool readout, bool potentials);
+size_t conv_pt_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                         int pad, int Ho, int Wo);
+spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
+                        bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
+                        float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s);
 // Readout layers (theta = +inf, no dense potentials): the split-K GEMM of the
 // last frame on the same channels-last copy (spk_conv_fast.hip).
 bool readout_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw,

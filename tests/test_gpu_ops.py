@@ -116,6 +116,8 @@ CONV_CASES = [
     (2, 8, 10, 10, 20, 3, 1, 1, 33, 5.0, 0.3, "f32"),       # T = 33
     (2, 30, 14, 14, 37, 3, 1, 1, 15, 3.0, 0.02, "f32"),     # sparse arrivals
     (2, 5, 9, 9, 7, 3, 1, 1, 5, -0.5, 0.3, "f32"),          # negative threshold
+    (2, 6, 40, 40, 33, 5, 1, 2, 20, 6.0, 0.04, "f32"),      # unaligned channels, sparse, two column tiles
+    (2, 3, 21, 19, 40, 3, 1, 0, 16, 1.5, 0.3, "f16"),       # unaligned channels, half weights, T = 16
 ]
 
 
