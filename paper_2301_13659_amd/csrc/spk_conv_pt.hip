@@ -541,6 +541,153 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
               stt((it - 1) & 1), out_t, out_v);
 }
 
+// Layers whose B fragments do not fit a wave's registers: each wave computes
+// kRT tiles at once and streams the B fragments of one slice at a time from
+// the workspace (L2), kD slices ahead, so every fragment read serves kRT
+// products.  Input staging, the epilogue and the write-out are those of
+// k_fire_pt; there is no slice skipping.
+constexpr int kRT = 4, kD = 4;
+
+template <int NP, int kMode>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__restrict__ bp, PGeom g,
+                 float theta, int nranges, uint8_t *__restrict__ out_t, float *__restrict__ out_v)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    uint8_t *hal = lds;
+    auto stv = [&](int i) { return reinterpret_cast<float *>(lds + kStvOff) + i * 32 * kStageStride; };
+    auto stt = [&](int i) { return lds + kSttOff + i * 32 * kStageStride; };
+    Tab *tabs = reinterpret_cast<Tab *>(lds + kTabOff);
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
+    const int nt = q % g.NT;
+    const int range = xcd + 8 * (q / g.NT);
+    if (range >= nranges) return;
+    const int p_begin = (int)((long long)range * g.P / nranges);
+    const int p_end = (int)((long long)(range + 1) * g.P / nranges);
+    if (p_begin >= p_end) return;
+    // B fragment (slice s, part k) of this lane: bcol[(s * NP + k) * 64]
+    const h8 *bcol = bp + (size_t)nt * g.SKp * NP * 64 + lane;
+
+    const int r = lane & 31, hh = lane >> 5;
+    const int pl = r >> g.lgTP, tt = r & (g.TP - 1);
+    const uint32_t cbv = 0x6401u + (uint32_t)min(tt, g.T - 1);
+    const h2 cc = as_h2(cbv | (cbv << 16));
+    const int PT = 32 >> g.lgTP;
+    const uint32_t never4 = 0x01010101u * (uint32_t)g.T;
+
+    {
+        int r0, r1;
+        group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
+        (void)store_range(load_range(xp, xp_words, a0, a1), hal, never4, range_words(a0, a1));
+        fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
+    }
+
+    int it = 0;
+    for (int gs = p_begin; gs < p_end; gs += kG, it++) {
+        const int cnt = min(p_end, gs + kG) - gs;
+        const int cur = it & 1;
+        const Tab *tab = tabs + (it % 3) * kG;
+        int r0, r1;
+        group_rows(g, gs, gs + cnt - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15;
+        __syncthreads();  // this group's input and table are in LDS; group it-1 is staged
+        const int gn = gs + kG;
+        const bool more = gn < p_end;
+        Staged nxt;
+        int nxt_words = 0;
+        if (more) {
+            int n0, n1;
+            group_rows(g, gn, min(p_end, gn + kG) - 1, n0, n1);
+            const int b0 = (n0 * g.rowb) & ~15, b1 = n1 * g.rowb;
+            nxt = load_range(xp, xp_words, b0, b1);
+            nxt_words = range_words(b0, b1);
+            fill_table(g, gn, min(p_end, gn + kG) - gn, tabs + ((it + 1) % 3) * kG);
+        }
+        if (it > 0)
+            write_out(g, nt, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1), stt(cur ^ 1), out_t, out_v);
+
+        // tiles of the group: tile i covers positions gs + i*PT ..; wave w
+        // takes tiles w, w + 4, ..., kRT of them at a time
+        const int ntiles = (cnt + PT - 1) / PT;
+        for (int t0 = wv; t0 < ntiles; t0 += 4 * kRT) {
+            int org2[kRT];
+#pragma unroll
+            for (int j = 0; j < kRT; j++) {
+                const int slot = min((t0 + 4 * j) * PT + pl, cnt - 1);
+                org2[j] = 2 * (tab[slot].xoff - a0 + 8 * hh);
+            }
+            f16v acc[kRT];
+#pragma unroll
+            for (int j = 0; j < kRT; j++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) acc[j][e] = 0.0f;
+            h8 ring[kD][NP];
+#pragma unroll
+            for (int d = 0; d < kD; d++)
+#pragma unroll
+                for (int k = 0; k < NP; k++) ring[d][k] = bcol[(size_t)(d * NP + k) * 64];
+            int ky = 0, jq = 0;
+            for (int s0 = 0; s0 < g.SKp; s0 += kD) {
+#pragma unroll
+                for (int d = 0; d < kD; d++) {
+                    const int sl = s0 + d;
+                    h8 bq[NP];
+#pragma unroll
+                    for (int k = 0; k < NP; k++) bq[k] = ring[d][k];
+                    const int sn = sl + kD;  // this ring slot's next slice
+                    if (sn < g.SKp)
+#pragma unroll
+                        for (int k = 0; k < NP; k++) ring[d][k] = bcol[(size_t)(sn * NP + k) * 64];
+                    const int off = sl < g.SK ? 2 * (ky * g.rowb + jq * 16) : 0;
+#pragma unroll
+                    for (int j = 0; j < kRT; j++) {
+                        const h8 a = frag_upto(lds_read16<kMode>(hal, org2[j] + off), cc);
+#pragma unroll
+                        for (int k = 0; k < NP; k++)
+                            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bq[k], acc[j], 0, 0, 0);
+                    }
+                    if (++jq == g.Q16) {
+                        jq = 0;
+                        ky++;
+                    }
+                }
+            }
+            const int o = lane & 31;
+#pragma unroll
+            for (int j = 0; j < kRT; j++) {
+                const int ti = t0 + 4 * j;
+                if (ti >= ntiles) continue;
+                uint32_t st[4] = {0u, 0u, 0u, 0u};
+                float sv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                if (g.lgTP == 3) tile_epilogue<8>(acc[j], theta, hh, st, sv);
+                else if (g.lgTP == 4) tile_epilogue<16>(acc[j], theta, hh, st, sv);
+                else tile_epilogue<32>(acc[j], theta, hh, st, sv);
+                if (hh == 0) {
+#pragma unroll
+                    for (int k = 0; k < 4; k++) {
+                        const int pi = ti * PT + k;
+                        if (k < PT && pi < cnt) {
+                            stv(cur)[o * kStageStride + pi] = sv[k];
+                            stt(cur)[o * kStageStride + pi] = (uint8_t)st[k];
+                        }
+                    }
+                }
+            }
+        }
+        if (more) {
+            __syncthreads();  // every wave is done with this group's input
+            (void)store_range(nxt, hal, never4, nxt_words);
+        }
+    }
+    __syncthreads();  // the last group is staged
+    write_out(g, nt, p_begin + (it - 1) * kG, p_end, tabs + ((it - 1) % 3) * kG, stv((it - 1) & 1),
+              stt((it - 1) & 1), out_t, out_v);
+}
+
 // Kernel instances: slice counts rounded up to these (the extra slices have
 // zero weights).  Float masters (hi/lo) keep 4*2*SK registers of B fragments,
 // halves 4*SK: both up to 144.
@@ -553,6 +700,22 @@ int instance_sk(int SK, bool half_w)
     for (int i = 0; i < 9; i++)
         if (SK <= t[i]) return t[i];
     return 0;
+}
+
+// Slices packed for a layer: a register-resident instance's count, or (deep
+// layers) the slices rounded up to the prefetch depth.
+int packed_sk(int SK, bool half_w)
+{
+    const int i = instance_sk(SK, half_w);
+    return i ? i : (SK + kD - 1) / kD * kD;
+}
+
+template <int NP, int kMode>
+void launch_deep(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t xw, const h8 *bp,
+                 const PGeom &g, float theta, int nranges, uint8_t *ot, float *ov)
+{
+    hipLaunchKernelGGL((k_fire_deep<NP, kMode>), grid, dim3(kThreads), lds, s, xp, xw, bp, g, theta,
+                       nranges, ot, ov);
 }
 
 typedef void (*PtLaunch)(dim3, size_t, hipStream_t, const uint8_t *, size_t, const h8 *, const PGeom &,
@@ -572,6 +735,8 @@ const PtLaunch kLaunch2[9][4] = {SPK_PT(2, 2),  SPK_PT(4, 2),  SPK_PT(6, 2),  SP
 const PtLaunch kLaunch1[9][4] = {SPK_PT(4, 1),  SPK_PT(8, 1),  SPK_PT(12, 1), SPK_PT(16, 1), SPK_PT(20, 1),
                                  SPK_PT(24, 1), SPK_PT(28, 1), SPK_PT(32, 1), SPK_PT(36, 1)};
 #undef SPK_PT
+const PtLaunch kDeep[2][4] = {{&launch_deep<1, 0>, &launch_deep<1, 1>, &launch_deep<1, 2>, &launch_deep<1, 3>},
+                              {&launch_deep<2, 0>, &launch_deep<2, 1>, &launch_deep<2, 2>, &launch_deep<2, 3>}};
 
 // Largest staged row range over the groups of every range (exact, per geometry).
 int max_rows(const PGeom &g, int nranges)
@@ -639,7 +804,7 @@ bool conv_pt_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int
     if ((long long)B * Co * Ho * Wo >= (1ll << 31)) return false;
     if (Wp * Cp > 48 * 1024 || (long long)Ci * Kh * Kw * 4 > 64 * 1024) return false;
     const PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
-    if (instance_sk(g.SK, half_w) == 0) return false;
+    if (g.SK > 4096) return false;
     // a group's rows, with the 16-byte alignment in front and 32 bytes of over-read
     const long long rows = max_rows(g, n_ranges(g));
     return rows * g.rowb + 64 <= kRange;
@@ -649,8 +814,7 @@ size_t conv_pt_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, i
                          int pad, int Ho, int Wo)
 {
     PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
-    g.SKp = std::max(instance_sk(g.SK, false), instance_sk(g.SK, true));
-    if (g.SKp == 0) g.SKp = g.SK;
+    g.SKp = std::max(packed_sk(g.SK, false), packed_sk(g.SK, true));
     return xp_bytes(g) + bp_bytes(g, 2);
 }
 
@@ -659,7 +823,7 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
                         float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
 {
     PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
-    g.SKp = instance_sk(g.SK, half_w);
+    g.SKp = packed_sk(g.SK, half_w);
     uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
     h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
     const int nb_in = g.B * g.Hp;
@@ -675,9 +839,14 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
     const int per_xcd = (nranges + 7) / 8;
     const dim3 grid(8 * g.NT * per_xcd);
     const size_t xw = ((size_t)g.B * g.Hp * g.rowb + kSlackPT) / 16;
-    int idx = 0;
-    while ((half_w ? kSK1 : kSK2)[idx] != g.SKp) idx++;
-    const PtLaunch launch = (half_w ? kLaunch1 : kLaunch2)[idx][read_mode(g.Cp)];
+    PtLaunch launch;
+    if (instance_sk(g.SK, half_w)) {
+        int idx = 0;
+        while ((half_w ? kSK1 : kSK2)[idx] != g.SKp) idx++;
+        launch = (half_w ? kLaunch1 : kLaunch2)[idx][read_mode(g.Cp)];
+    } else {
+        launch = kDeep[half_w ? 0 : 1][read_mode(g.Cp)];
+    }
     launch(grid, fire_lds(), s, xp, xw, bp, g, theta, nranges, out_t, out_v);
     return check_launch("spk_conv_fire");
 }
