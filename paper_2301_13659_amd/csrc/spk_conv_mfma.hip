@@ -383,7 +383,9 @@ __global__ __launch_bounds__(kThreads) void k_conv_fire_mfma(
             const _Float16 ct = (_Float16)(float)(1024 + tau);
             const h2 cc = {ct, ct};
             uint64_t sm = all_s;
-            if (masks) sm = __builtin_amdgcn_readfirstlane(act[tau]);
+            // (through uint32_t: the int the builtin returns must not sign-extend
+            // subtile 31 into bits 32..63)
+            if (masks) sm = (uint32_t)__builtin_amdgcn_readfirstlane(act[tau]);
             // Walk the active subtiles with the operands of the next one already
             // in flight (two register sets used in turn).
             h8 bh0[C], bl0[C], bh1[C], bl1[C];
