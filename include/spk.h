@@ -257,6 +257,54 @@ spk_status spk_frames_to_times(const uint8_t *frames, int B, int T, int64_t n,
 spk_status spk_times_to_frames(const uint8_t *times, int B, int T, int64_t n,
                                uint8_t *frames, spk_stream stream);
 
+/*
+ * spk_fc_fire -- fully connected layer with integrate-and-fire neurons,
+ * §II-E.2: an I x O kernel over B x T x I input spikes.  For sample b,
+ * neuron o and step t, V_t = sum over i of W[o, i] * [in_times[b, i] <= t];
+ * the neuron fires once, at the first t with V_t > theta (theta = +inf:
+ * readout, never fires).  This is spk_conv_fire with a 1 x 1 kernel over I
+ * input channels on a 1 x 1 image, and has its precision and errors.
+ *   in_times   uint8 B x I (device), e.g. a flattened B x C x H x W time map.
+ *   w          O x I (device): float master weights or IEEE half bits.
+ *   out_times  uint8 B x O; out_vkey float B x O (as spk_conv_fire).
+ *   potentials nullable float B x T x O (device).
+ *   ws         workspace of spk_fc_fire_workspace_size(...) bytes.
+ */
+size_t spk_fc_fire_workspace_size(int B, int T, int I, int O, float theta, int potentials);
+spk_status spk_fc_fire(const uint8_t *in_times, int B, int T, int I, const void *w,
+                       spk_dtype w_dtype, int O, float theta, uint8_t *out_times,
+                       float *out_vkey, float *potentials, void *ws, size_t ws_bytes,
+                       spk_stream stream);
+
+/*
+ * spk_fc_winners -- k-winners-take-all of a fully connected layer (the
+ * paper's fcwta, §II-F.3).  Per sample, up to k rounds: the best remaining
+ * candidate wins (earliest time, then higher vkey, then lower neuron index);
+ * it and every neuron whose index is within `radius` of its index stop being
+ * candidates.  Candidates are the neurons that fired; with readout = 1 every
+ * neuron, ranked by vkey only, reported with t = T-1.
+ *   times, vkey  uint8 / float B x O (device), from spk_fc_fire.
+ *   winners      spk_winner B x k (device): {c = neuron, y = 0, x = 0, t, v};
+ *                slots past n_winners[b] get c = -1.
+ *   n_winners    int32 B (device).
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (T out of range, O > 65536, k > 4096).
+ */
+spk_status spk_fc_winners(const uint8_t *times, const float *vkey, int B, int O, int T,
+                          int k, int radius, int readout, spk_winner *winners,
+                          int32_t *n_winners, spk_stream stream);
+
+/*
+ * spk_fc_stdp_update -- STDP / R-STDP of a fully connected layer (§II-F.1,
+ * §II-F.2): spk_stdp_update with a 1 x 1 kernel over I input channels; the
+ * receptive field of neuron o is the whole input, w is float O x I, w_f16
+ * nullable half O x I, in_times uint8 B x I, winners from spk_fc_winners.
+ */
+size_t spk_fc_stdp_update_workspace_size(int O, int I, int B, int k);
+spk_status spk_fc_stdp_update(float *w, uint16_t *w_f16, int O, int I, const uint8_t *in_times,
+                              int B, const spk_winner *winners, const int32_t *n_winners, int k,
+                              const spk_stdp_config *cfg, int n_cfg, const int32_t *winner_cfg,
+                              void *ws, size_t ws_bytes, spk_stream stream);
+
 /* float -> IEEE half bits, round to nearest even (the SPK_F16 conv operand). */
 spk_status spk_cast_f16(const float *x, uint16_t *y, int64_t n, spk_stream stream);
 

@@ -57,6 +57,7 @@ def lib():
         L.or_stdp_update.argtypes = [P, i, i, i, i, i, i, P, i, i, i, P, P, i, P, i, P]
         L.or_stdp_update.restype = i
         L.or_rstdp_select.argtypes = [P, P, i, i, P, i, P]
+        L.or_fc_wta.argtypes = [P, P, i, i, i, i, i, i, P, P]
         _lib = L
     return _lib
 
@@ -228,3 +229,42 @@ def rstdp_select(winners, n_winners, labels, group) -> np.ndarray:
     out = np.empty((B, k), np.int32)
     lib().or_rstdp_select(_p(winners), _p(n_winners), B, k, _p(labels), group, _p(out))
     return out
+
+
+# --------------------------------------------------------- fully connected
+
+def fc_fire(in_times, w, T, theta, potentials: bool = False):
+    """FC layer with IF neurons (§II-E.2): in_times B x I, w O x I.  The FC
+    product is the convolution of a 1 x 1 kernel over I input channels."""
+    in_times = _c(in_times, np.uint8)
+    w = np.asarray(w)
+    B, I = in_times.shape
+    O = w.shape[0]
+    r = conv_fire(in_times.reshape(B, I, 1, 1), w.reshape(O, I, 1, 1), T, 1, 0, theta,
+                  potentials=potentials)
+    if potentials:
+        tf, vk, V = r
+        return tf.reshape(B, O), vk.reshape(B, O), V.reshape(B, T, O)
+    tf, vk = r
+    return tf.reshape(B, O), vk.reshape(B, O)
+
+
+def fc_wta(times, vkey, T, k, radius, readout=False):
+    times = _c(times, np.uint8)
+    vkey = _c(vkey, np.float32)
+    B, O = times.shape
+    win = np.zeros((B, max(k, 1)), WINNER_DTYPE)[:, :k].copy()
+    nw = np.zeros(B, np.int32)
+    lib().or_fc_wta(_p(times), _p(vkey), B, O, T, k, radius, int(bool(readout)), _p(win), _p(nw))
+    return win, nw
+
+
+def fc_stdp_update(w, in_times, winners, n_winners, cfgs, winner_cfg=None):
+    """STDP / R-STDP of an FC layer: the convolution update with a 1 x 1 kernel."""
+    w = np.asarray(w, np.float32)
+    O, I = w.shape
+    in_times = _c(in_times, np.uint8)
+    B = in_times.shape[0]
+    out = stdp_update(w.reshape(O, I, 1, 1), in_times.reshape(B, I, 1, 1), winners, n_winners,
+                      cfgs, 1, 0, winner_cfg=winner_cfg)
+    return out.reshape(O, I)

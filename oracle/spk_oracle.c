@@ -485,3 +485,57 @@ void or_rstdp_select(const or_winner *winners, const int32_t *n_winners, int B, 
                 (s < n_winners[b] && wn->c / group == labels[b]) ? 0 : 1;
         }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Fully connected layer winners: §II-E.2 (FC layer), §II-F.3 (fcwta).      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * k-winners-take-all for a fully connected layer (the paper's
+ * fcwta(array, radius, count)).  Neurons of a sample are indexed o in [0, O).
+ * Per sample, up to k rounds: the best remaining candidate wins (earliest
+ * spike, then higher potential, then lower index); it and every neuron whose
+ * index lies within `radius` of its index stop being candidates.  Reading:
+ * the radius of fcwta measures distance along the neuron index, the one
+ * dimension an FC layer has.  Candidates are the fired neurons; in readout
+ * mode every neuron, ranked by potential only, reported with t = T-1.
+ * Winners are reported as {c = o, y = 0, x = 0, t, v}; unused slots c = -1.
+ */
+void or_fc_wta(const uint8_t *times, const float *vkey, int B, int O, int T, int k, int radius,
+               int readout, or_winner *winners, int32_t *n_winners)
+{
+    uint8_t *alive = (uint8_t *)malloc(O > 0 ? (size_t)O : 1);
+    for (int b = 0; b < B; b++) {
+        const uint8_t *tb = times + (size_t)b * O;
+        const float *vb = vkey + (size_t)b * O;
+        for (int o = 0; o < O; o++) alive[o] = readout ? 1 : (tb[o] != OR_NEVER);
+        int count = 0;
+        for (int round = 0; round < k; round++) {
+            int best = -1;
+            for (int o = 0; o < O; o++) {
+                if (!alive[o]) continue;
+                if (best < 0) { best = o; continue; }
+                int to = readout ? 0 : tb[o], tm = readout ? 0 : tb[best];
+                if (or_better(to, vb[o], o, tm, vb[best], best)) best = o;
+            }
+            if (best < 0) break;
+            or_winner *wn = &winners[(size_t)b * k + count];
+            wn->c = best;
+            wn->y = 0;
+            wn->x = 0;
+            wn->t = readout ? T - 1 : tb[best];
+            wn->v = vb[best];
+            count++;
+            for (int o = 0; o < O; o++)
+                if (abs(o - best) <= radius) alive[o] = 0;
+        }
+        n_winners[b] = count;
+        for (int s = count; s < k; s++) {
+            or_winner *wn = &winners[(size_t)b * k + s];
+            wn->c = -1;
+            wn->y = wn->x = wn->t = -1;
+            wn->v = 0.0f;
+        }
+    }
+    free(alive);
+}

@@ -67,6 +67,11 @@ _SIGNATURES = {
     "spk_frames_to_times": ([_P, _I, _I, _I64, _P, _P], _I),
     "spk_times_to_frames": ([_P, _I, _I, _I64, _P, _P], _I),
     "spk_cast_f16": ([_P, _P, _I64, _P], _I),
+    "spk_fc_fire_workspace_size": ([_I, _I, _I, _I, _F, _I], _Z),
+    "spk_fc_fire": ([_P, _I, _I, _I, _P, _I, _I, _F, _P, _P, _P, _P, _Z, _P], _I),
+    "spk_fc_winners": ([_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P], _I),
+    "spk_fc_stdp_update_workspace_size": ([_I, _I, _I, _I], _Z),
+    "spk_fc_stdp_update": ([_P, _P, _I, _I, _P, _I, _P, _P, _I, _P, _I, _P, _P, _Z, _P], _I),
 }
 
 _lib = None
@@ -311,6 +316,69 @@ def spk_cast_f16(x, out=None):
         out = torch.empty(x.shape, dtype=torch.float16, device=x.device)
     _check(load().spk_cast_f16(_ptr(x), _ptr(out), x.numel(), _stream(x.device)))
     return out
+
+
+def spk_fc_fire(in_times, w, T: int, theta: float = math.inf, potentials=False):
+    """Fully connected IF layer: in_times uint8 B x I, w float32 / float16 O x I."""
+    _dev(in_times, torch.uint8, "in_times", 2)
+    if w.dtype not in (torch.float32, torch.float16):
+        raise ValueError("w: expected float32 or float16")
+    _dev(w, w.dtype, "w", 2)
+    B, I = in_times.shape
+    O, I2 = w.shape
+    if I != I2:
+        raise ValueError(f"w has {I2} inputs, input has {I}")
+    dev = in_times.device
+    out_times = torch.empty((B, O), dtype=torch.uint8, device=dev)
+    out_vkey = torch.empty((B, O), dtype=torch.float32, device=dev)
+    V = torch.empty((B, T, O), dtype=torch.float32, device=dev) if potentials else None
+    L = load()
+    nbytes = L.spk_fc_fire_workspace_size(B, T, I, O, float(theta), int(V is not None))
+    ws = _workspace(nbytes, dev)
+    dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
+    _check(L.spk_fc_fire(_ptr(in_times), B, T, I, _ptr(w), dt, O, float(theta), _ptr(out_times),
+                         _ptr(out_vkey), _ptr(V), _ptr(ws), nbytes, _stream(dev)))
+    return (out_times, out_vkey, V) if V is not None else (out_times, out_vkey)
+
+
+def spk_fc_winners(times, vkey, T: int, k: int, radius: int, readout: bool = False):
+    """fcwta: returns (winners int32 B x k x 5, n_winners int32 B)."""
+    _dev(times, torch.uint8, "times", 2)
+    _dev(vkey, torch.float32, "vkey", 2)
+    B, O = times.shape
+    dev = times.device
+    winners = torch.empty((B, k, 5), dtype=torch.int32, device=dev)
+    n_winners = torch.empty((B,), dtype=torch.int32, device=dev)
+    _check(load().spk_fc_winners(_ptr(times), _ptr(vkey), B, O, T, k, radius, int(bool(readout)),
+                                 _ptr(winners), _ptr(n_winners), _stream(dev)))
+    return winners, n_winners
+
+
+def spk_fc_stdp_update(w, in_times, winners, n_winners, cfgs, winner_cfg=None, w_f16=None):
+    """In-place STDP of float32 FC weights w (O x I) from in_times (B x I)."""
+    _dev(w, torch.float32, "w", 2)
+    _dev(in_times, torch.uint8, "in_times", 2)
+    _dev(winners, torch.int32, "winners", 3)
+    _dev(n_winners, torch.int32, "n_winners", 1)
+    if w_f16 is not None:
+        _dev(w_f16, torch.float16, "w_f16", 2)
+    if winner_cfg is not None:
+        _dev(winner_cfg, torch.int32, "winner_cfg")
+    O, I = w.shape
+    B, I2 = in_times.shape
+    if I != I2:
+        raise ValueError(f"w has {I} inputs, input has {I2}")
+    k = winners.shape[1]
+    cl = [tuple(c) for c in cfgs]
+    arr = (StdpConfig * len(cl))(*[StdpConfig(float(a), float(b), float(lo), float(up), int(st))
+                                   for a, b, lo, up, st in cl])
+    L = load()
+    nbytes = L.spk_fc_stdp_update_workspace_size(O, I, B, k)
+    ws = _workspace(nbytes, w.device)
+    _check(L.spk_fc_stdp_update(_ptr(w), _ptr(w_f16), O, I, _ptr(in_times), B, _ptr(winners),
+                                _ptr(n_winners), k, arr, len(cl), _ptr(winner_cfg), _ptr(ws), nbytes,
+                                _stream(w.device)))
+    return w
 
 
 def winners_numpy(winners: torch.Tensor) -> np.ndarray:

@@ -130,3 +130,16 @@ def test_conv_fire_planning_survives_every_layer_shape():
         st = L.spk_conv_fire(P1, B, T, Ci, H, W, P1, 0, Co, K, K, 1, pad, theta, P1, P1, None,
                              P1 if ws else None, ws, None)
         assert st == spk.SPK_E_HIP, spk.load().spk_last_error()
+
+
+def test_fc_validation():
+    L = spk.load()
+    _err(L.spk_fc_winners(None, P1, 1, 8, 4, 1, 0, 0, P1, P1, None), spk.SPK_E_ARG, "NULL")
+    _err(L.spk_fc_winners(P1, P1, 1, 8, 4, 1, -1, 0, P1, P1, None), spk.SPK_E_ARG, "radius")
+    _err(L.spk_fc_winners(P1, P1, 1, 1 << 17, 4, 1, 0, 0, P1, P1, None), spk.SPK_E_SHAPE, "O=")
+    _err(L.spk_fc_winners(P1, P1, 1, 8, 0, 1, 0, 0, P1, P1, None), spk.SPK_E_SHAPE, "T=")
+    _err(L.spk_fc_winners(P1, P1, 1, 8, 4, 5000, 0, 0, P1, P1, None), spk.SPK_E_SHAPE, "k=")
+    _err(L.spk_fc_fire(P1, 0, 4, 8, P1, spk.SPK_F32, 3, 1.0, P1, P1, None, None, 0, None),
+         spk.SPK_E_ARG, "positive")
+    _err(L.spk_fc_fire(None, 1, 4, 8, P1, spk.SPK_F32, 3, 1.0, P1, P1, None, None, 0, None),
+         spk.SPK_E_ARG, "NULL")

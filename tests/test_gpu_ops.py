@@ -118,6 +118,8 @@ CONV_CASES = [
     (2, 5, 9, 9, 7, 3, 1, 1, 5, -0.5, 0.3, "f32"),          # negative threshold
     (2, 6, 40, 40, 33, 5, 1, 2, 20, 6.0, 0.04, "f32"),      # unaligned channels, sparse, two column tiles
     (2, 3, 21, 19, 40, 3, 1, 0, 16, 1.5, 0.3, "f16"),       # unaligned channels, half weights, T = 16
+    (2, 112, 6, 6, 40, 3, 1, 1, 12, 60.0, 0.3, "f16"),      # 1008 taps: exactly 32 subtiles of 32
+    (3, 1000, 1, 1, 65, 1, 1, 0, 30, 60.0, 0.2, "f32"),     # 1 x 1 kernel over 1000 channels (an FC layer)
 ]
 
 
