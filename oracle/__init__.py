@@ -58,6 +58,9 @@ def lib():
         L.or_stdp_update.restype = i
         L.or_rstdp_select.argtypes = [P, P, i, i, P, i, P]
         L.or_fc_wta.argtypes = [P, P, i, i, i, i, i, i, P, P]
+        L.or_times_to_spikes.argtypes = [P, i, i64, i, i, P, P]
+        L.or_spikes_to_times.argtypes = [P, P, i, i64, i, i, P]
+        L.or_conv_fire_spikes.argtypes = [P, P, i, i, i, i, i, i, P, i, i, i, i, i, d, P, P]
         _lib = L
     return _lib
 
@@ -268,3 +271,49 @@ def fc_stdp_update(w, in_times, winners, n_winners, cfgs, winner_cfg=None):
     out = stdp_update(w.reshape(O, I, 1, 1), in_times.reshape(B, I, 1, 1), winners, n_winners,
                       cfgs, 1, 0, winner_cfg=winner_cfg)
     return out.reshape(O, I)
+
+
+# --------------------------------------------------------- sparse interface
+
+def times_to_spikes(times, T, cap=None):
+    """Spike list of a time map (§II-B): (spikes uint32 B x cap, offsets int32
+    B x (T + 1)).  Per sample, flat neuron indices grouped by step, ascending
+    within a step; offsets[b, t] counts the spikes before step t."""
+    times = _c(times, np.uint8)
+    B = times.shape[0]
+    n = int(np.prod(times.shape[1:]))
+    cap = n if cap is None else int(cap)
+    spikes = np.zeros((B, max(cap, 1)), np.uint32)[:, :cap].copy()
+    offsets = np.empty((B, T + 1), np.int32)
+    lib().or_times_to_spikes(_p(times), B, n, T, cap, _p(spikes), _p(offsets))
+    return spikes, offsets
+
+
+def spikes_to_times(spikes, offsets, shape, T):
+    """The time map (B x shape) of a spike list; unstored spikes are absent."""
+    spikes = _c(spikes, np.uint32)
+    offsets = _c(offsets, np.int32)
+    B, cap = spikes.shape
+    n = int(np.prod(shape))
+    times = np.empty((B,) + tuple(shape), np.uint8)
+    lib().or_spikes_to_times(_p(spikes), _p(offsets), B, n, T, cap, _p(times))
+    return times
+
+
+def conv_fire_spikes(spikes, offsets, in_shape, w, T, stride, pad, theta):
+    """Conv + fire driven by a spike list: in_shape = (Ci, Hi, Wi) of one
+    sample.  Returns (t_f uint8 B x Co x Ho x Wo, V_key float32)."""
+    spikes = _c(spikes, np.uint32)
+    offsets = _c(offsets, np.int32)
+    w = _c(w, np.float32)
+    B, cap = spikes.shape
+    Ci, Hi, Wi = in_shape
+    Co, Ci2, Kh, Kw = w.shape
+    assert Ci == Ci2 and offsets.shape == (B, T + 1)
+    Ho = (Hi + 2 * pad - Kh) // stride + 1
+    Wo = (Wi + 2 * pad - Kw) // stride + 1
+    tf = np.empty((B, Co, Ho, Wo), np.uint8)
+    vk = np.empty((B, Co, Ho, Wo), np.float32)
+    lib().or_conv_fire_spikes(_p(spikes), _p(offsets), cap, B, T, Ci, Hi, Wi, _p(w), Co, Kh, Kw,
+                              stride, pad, float(theta), _p(tf), _p(vk))
+    return tf, vk

@@ -539,3 +539,108 @@ void or_fc_wta(const uint8_t *times, const float *vkey, int B, int O, int T, int
     }
     free(alive);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Sparse interface: §II-B (spike indices instead of full buffers).         */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * A spike list holds, per sample, the flat indices (c*H + y)*W + x of the
+ * neurons that fire, grouped by time step in ascending order and ascending
+ * index within a step: offsets[b*(T+1) + t] is the number of spikes of sample
+ * b before step t (offsets[.. + T] the total), spikes[b*cap + j] its j-th
+ * spike.  Spikes past cap are counted but not stored.
+ */
+void or_times_to_spikes(const uint8_t *times, int B, int64_t n, int T, int cap, uint32_t *spikes,
+                        int32_t *offsets)
+{
+    for (int b = 0; b < B; b++) {
+        const uint8_t *tb = times + (size_t)b * n;
+        int32_t cnt = 0;
+        for (int t = 0; t < T; t++) {
+            offsets[(size_t)b * (T + 1) + t] = cnt;
+            for (int64_t i = 0; i < n; i++)
+                if (tb[i] == t) {
+                    if (cnt < cap) spikes[(size_t)b * cap + cnt] = (uint32_t)i;
+                    cnt++;
+                }
+        }
+        offsets[(size_t)b * (T + 1) + T] = cnt;
+    }
+}
+
+/* The time map a spike list describes (its stored spikes only). */
+void or_spikes_to_times(const uint32_t *spikes, const int32_t *offsets, int B, int64_t n, int T,
+                        int cap, uint8_t *times)
+{
+    memset(times, OR_NEVER, (size_t)B * n);
+    for (int b = 0; b < B; b++)
+        for (int t = 0; t < T; t++) {
+            const int32_t *ob = offsets + (size_t)b * (T + 1);
+            int32_t end = ob[t + 1] < cap ? ob[t + 1] : cap;
+            for (int32_t j = ob[t]; j < end; j++) {
+                uint32_t i = spikes[(size_t)b * cap + j];
+                if ((int64_t)i < n) times[(size_t)b * n + i] = (uint8_t)t;
+            }
+        }
+}
+
+/*
+ * Conv + fire driven by a spike list: each stored spike of step t adds its
+ * weight to every output neuron whose window holds it (the change of
+ * potential at t, Eq. 2 restricted to the new arrivals); the potential is the
+ * running sum of those changes over the steps, and the firing rule is that
+ * of or_fire_neuron.  Work is proportional to the spikes times their fan-out.
+ */
+void or_conv_fire_spikes(const uint32_t *spikes, const int32_t *offsets, int cap, int B, int T,
+                         int Ci, int Hi, int Wi, const float *w, int Co, int Kh, int Kw, int stride,
+                         int pad, double theta, uint8_t *out_times, float *out_vkey)
+{
+    int Ho = (Hi + 2 * pad - Kh) / stride + 1;
+    int Wo = (Wi + 2 * pad - Kw) / stride + 1;
+    size_t per_t = (size_t)Co * Ho * Wo;
+    double *dV = (double *)malloc(sizeof(double) * T * per_t);
+    double *V = (double *)malloc(sizeof(double) * T);
+    for (int b = 0; b < B; b++) {
+        memset(dV, 0, sizeof(double) * T * per_t);
+        const int32_t *ob = offsets + (size_t)b * (T + 1);
+        for (int t = 0; t < T; t++) {
+            int32_t end = ob[t + 1] < cap ? ob[t + 1] : cap;
+            for (int32_t j = ob[t]; j < end; j++) {
+                uint32_t i = spikes[(size_t)b * cap + j];
+                if ((int64_t)i >= (int64_t)Ci * Hi * Wi) continue;
+                int c = (int)(i / (uint32_t)(Hi * Wi));
+                int iy = (int)(i / (uint32_t)Wi) % Hi, ix = (int)(i % (uint32_t)Wi);
+                for (int ky = 0; ky < Kh; ky++) {
+                    int ny = iy + pad - ky;
+                    if (ny < 0 || ny % stride) continue;
+                    int y = ny / stride;
+                    if (y >= Ho) continue;
+                    for (int kx = 0; kx < Kw; kx++) {
+                        int nx = ix + pad - kx;
+                        if (nx < 0 || nx % stride) continue;
+                        int x = nx / stride;
+                        if (x >= Wo) continue;
+                        for (int o = 0; o < Co; o++)
+                            dV[t * per_t + ((size_t)o * Ho + y) * Wo + x] +=
+                                (double)w[(((size_t)o * Ci + c) * Kh + ky) * Kw + kx];
+                    }
+                }
+            }
+        }
+        for (size_t q = 0; q < per_t; q++) {
+            double acc = 0.0;
+            for (int t = 0; t < T; t++) {
+                acc += dV[t * per_t + q];
+                V[t] = acc;
+            }
+            uint8_t tf;
+            double vk;
+            or_fire_neuron(V, T, theta, &tf, &vk);
+            out_times[(size_t)b * per_t + q] = tf;
+            out_vkey[(size_t)b * per_t + q] = (float)vk;
+        }
+    }
+    free(V);
+    free(dV);
+}
