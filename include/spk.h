@@ -305,6 +305,70 @@ spk_status spk_fc_stdp_update(float *w, uint16_t *w_f16, int O, int I, const uin
                               const spk_stdp_config *cfg, int n_cfg, const int32_t *winner_cfg,
                               void *ws, size_t ws_bytes, spk_stream stream);
 
+/* ---------------------------------------------------------------------- */
+/* Sparse interface (§II-B): the indices of the spikes instead of full     */
+/* buffers.                                                                */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * A spike list of B samples over T steps:
+ *   spikes   uint32 B x cap (device): for sample b, the flat neuron indices
+ *            (c*H + y)*W + x of its spikes, grouped by step in ascending
+ *            order and by ascending index within a step;
+ *   offsets  int32 B x (T + 1) (device): offsets[b*(T+1) + t] = number of
+ *            spikes of sample b before step t; the entry at T is its total.
+ * A sample with more than cap spikes keeps its first cap (in that order);
+ * the offsets still count all of them, so total > cap tells the caller, and
+ * every consumer reads only the stored ones.  Under rank-order coding a
+ * neuron fires once, so cap = C*H*W always suffices.
+ */
+
+/*
+ * spk_times_to_spikes -- spike list of a time map (dense -> sparse).
+ *   times  uint8 B x C x H x W (device); ws of
+ *   spk_times_to_spikes_workspace_size(...) bytes (per-chunk counts).
+ * Deterministic: the list is the stable sort of the spiking neurons by step.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (T range, C*H*W >= 2^31, B > 65535),
+ * SPK_E_WORKSPACE.
+ */
+size_t spk_times_to_spikes_workspace_size(int B, int C, int H, int W, int T);
+spk_status spk_times_to_spikes(const uint8_t *times, int B, int C, int H, int W, int T, int cap,
+                               uint32_t *spikes, int32_t *offsets, void *ws, size_t ws_bytes,
+                               spk_stream stream);
+
+/*
+ * spk_spikes_to_times -- the time map of a spike list (sparse -> dense):
+ * NEVER everywhere, then t at each stored spike of step t.  Indices
+ * >= C*H*W are ignored; an index listed twice in one sample is invalid.
+ */
+spk_status spk_spikes_to_times(const uint32_t *spikes, const int32_t *offsets, int cap, int B,
+                               int C, int H, int W, int T, uint8_t *times, spk_stream stream);
+
+/*
+ * spk_conv_fire_sparse -- spiking convolution + IF fire driven by a spike
+ * list (§II-B, §II-E.1 Eq. 2, firing of §II-D.3 / §II-E): the same outputs
+ * as spk_conv_fire on the list's time map (first-spike times and V_key,
+ * B x Co x Ho x Wo), at a cost that follows the number of spikes times their
+ * fan-out rather than B*T*Ho*Wo*Co*Ci*Kh*Kw.  theta = +inf is the readout
+ * (V_key = V[T-1], nothing fires).  No dense-potential output.
+ *   spikes, offsets, cap  the input spike list over Ci x Hi x Wi neurons.
+ *   w      Co x Ci x Kh x Kw (device): float master or IEEE half bits; float
+ *          weights are added in float, in step order and tap order
+ *          ((ky, kx, c) row-major) within a step.
+ *   ws     workspace of spk_conv_fire_sparse_workspace_size(...) bytes (a
+ *          padded channels-last time buffer and the weight table).
+ * Errors: SPK_E_ARG, SPK_E_SHAPE, SPK_E_UNSUPPORTED (unknown dtype, or a
+ * weight table of Kh*Kw*Ci taps x 32 maps that does not fit a block's LDS),
+ * SPK_E_WORKSPACE.
+ */
+size_t spk_conv_fire_sparse_workspace_size(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh,
+                                           int Kw, int stride, int pad, spk_dtype w_dtype);
+spk_status spk_conv_fire_sparse(const uint32_t *spikes, const int32_t *offsets, int cap, int B,
+                                int T, int Ci, int Hi, int Wi, const void *w, spk_dtype w_dtype,
+                                int Co, int Kh, int Kw, int stride, int pad, float theta,
+                                uint8_t *out_times, float *out_vkey, void *ws, size_t ws_bytes,
+                                spk_stream stream);
+
 /* float -> IEEE half bits, round to nearest even (the SPK_F16 conv operand). */
 spk_status spk_cast_f16(const float *x, uint16_t *y, int64_t n, spk_stream stream);
 

@@ -72,6 +72,12 @@ _SIGNATURES = {
     "spk_fc_winners": ([_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P], _I),
     "spk_fc_stdp_update_workspace_size": ([_I, _I, _I, _I], _Z),
     "spk_fc_stdp_update": ([_P, _P, _I, _I, _P, _I, _P, _P, _I, _P, _I, _P, _P, _Z, _P], _I),
+    "spk_times_to_spikes_workspace_size": ([_I] * 5, _Z),
+    "spk_times_to_spikes": ([_P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _Z, _P], _I),
+    "spk_spikes_to_times": ([_P, _P, _I, _I, _I, _I, _I, _I, _P, _P], _I),
+    "spk_conv_fire_sparse_workspace_size": ([_I] * 10 + [_I], _Z),
+    "spk_conv_fire_sparse": ([_P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _I, _F, _P,
+                              _P, _P, _Z, _P], _I),
 }
 
 _lib = None
@@ -385,3 +391,62 @@ def winners_numpy(winners: torch.Tensor) -> np.ndarray:
     """Device winners (B x k x 5 int32) -> numpy structured array of WINNER_DTYPE."""
     a = winners.detach().cpu().contiguous().numpy()
     return a.view(np.uint8).reshape(a.shape[0], a.shape[1], 20).view(WINNER_DTYPE)[..., 0]
+
+
+# ------------------------------------------------------- sparse interface
+
+def spk_times_to_spikes(times, T: int, cap: int | None = None):
+    """Spike list of a time map (B x C x H x W): (spikes uint32 as int32 B x cap,
+    offsets int32 B x (T + 1)).  cap defaults to C*H*W (never truncates)."""
+    _dev(times, torch.uint8, "times", 4)
+    B, C, H, W = times.shape
+    cap = C * H * W if cap is None else int(cap)
+    dev = times.device
+    spikes = torch.empty((B, cap), dtype=torch.int32, device=dev)
+    offsets = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+    L = load()
+    nbytes = L.spk_times_to_spikes_workspace_size(B, C, H, W, T)
+    ws = _workspace(max(nbytes, 1), dev)
+    _check(L.spk_times_to_spikes(_ptr(times), B, C, H, W, T, cap, _ptr(spikes), _ptr(offsets),
+                                 _ptr(ws), nbytes, _stream(dev)))
+    return spikes, offsets
+
+
+def spk_spikes_to_times(spikes, offsets, shape, T: int):
+    """Time map B x shape (C, H, W) of a spike list."""
+    _dev(spikes, torch.int32, "spikes", 2)
+    _dev(offsets, torch.int32, "offsets", 2)
+    B, cap = spikes.shape
+    C, H, W = shape
+    times = torch.empty((B, C, H, W), dtype=torch.uint8, device=spikes.device)
+    _check(load().spk_spikes_to_times(_ptr(spikes), _ptr(offsets), cap, B, C, H, W, T, _ptr(times),
+                                      _stream(spikes.device)))
+    return times
+
+
+def spk_conv_fire_sparse(spikes, offsets, in_shape, w, T: int, stride: int = 1, pad: int = 0,
+                         theta: float = math.inf):
+    """Conv + fire driven by a spike list over in_shape = (Ci, Hi, Wi):
+    (out_times uint8, out_vkey float32), B x Co x Ho x Wo."""
+    _dev(spikes, torch.int32, "spikes", 2)
+    _dev(offsets, torch.int32, "offsets", 2)
+    if w.dtype not in (torch.float32, torch.float16):
+        raise ValueError("w: expected float32 or float16")
+    _dev(w, w.dtype, "w", 4)
+    B, cap = spikes.shape
+    Ci, Hi, Wi = in_shape
+    Co, Ci2, Kh, Kw = w.shape
+    if Ci != Ci2:
+        raise ValueError(f"w has {Ci2} input channels, input has {Ci}")
+    Ho, Wo = out_extent(Hi, Kh, stride, pad), out_extent(Wi, Kw, stride, pad)
+    dev = spikes.device
+    out_times = torch.empty((B, Co, Ho, Wo), dtype=torch.uint8, device=dev)
+    out_vkey = torch.empty((B, Co, Ho, Wo), dtype=torch.float32, device=dev)
+    dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
+    L = load()
+    nbytes = L.spk_conv_fire_sparse_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, dt)
+    ws = _workspace(max(nbytes, 1), dev)
+    _check(L.spk_conv_fire_sparse(_ptr(spikes), _ptr(offsets), cap, B, T, Ci, Hi, Wi, _ptr(w), dt,
+                                  Co, Kh, Kw, stride, pad, float(theta), _ptr(out_times),
+                                  _ptr(out_vkey), _ptr(ws), nbytes, _stream(dev)))
+    return out_times, out_vkey

@@ -143,3 +143,33 @@ def test_fc_validation():
          spk.SPK_E_ARG, "positive")
     _err(L.spk_fc_fire(None, 1, 4, 8, P1, spk.SPK_F32, 3, 1.0, P1, P1, None, None, 0, None),
          spk.SPK_E_ARG, "NULL")
+
+
+def test_sparse_validation():
+    L = spk.load()
+    F32, F16 = spk.SPK_F32, spk.SPK_F16
+    _err(L.spk_times_to_spikes(None, 1, 2, 3, 4, 5, 10, P1, P1, P1, 1 << 20, None), spk.SPK_E_ARG,
+         "NULL")
+    _err(L.spk_times_to_spikes(P1, 1, 2, 3, 4, 255, 10, P1, P1, P1, 1 << 20, None), spk.SPK_E_SHAPE,
+         "T=")
+    _err(L.spk_times_to_spikes(P1, 1, 2, 3, 4, 5, 10, P1, P1, P1, 0, None), spk.SPK_E_WORKSPACE,
+         "workspace")
+    assert L.spk_times_to_spikes_workspace_size(2, 64, 64, 64, 30) > 0
+    _err(L.spk_spikes_to_times(P1, P1, -1, 1, 2, 3, 4, 5, P1, None), spk.SPK_E_ARG, "cap")
+    _err(L.spk_spikes_to_times(P1, None, 4, 1, 2, 3, 4, 5, P1, None), spk.SPK_E_ARG, "NULL")
+    args = [P1, P1, 100, 2, 15, 6, 28, 28, P1, F32, 30, 5, 5, 1, 2, 10.0, P1, P1, P1, 1 << 30, None]
+    ok = list(args)
+    bad = list(ok); bad[4] = 0
+    _err(L.spk_conv_fire_sparse(*bad), spk.SPK_E_SHAPE, "T=")
+    bad = list(ok); bad[9] = 7
+    _err(L.spk_conv_fire_sparse(*bad), spk.SPK_E_UNSUPPORTED, "dtype")
+    bad = list(ok); bad[11] = 40
+    _err(L.spk_conv_fire_sparse(*bad), spk.SPK_E_SHAPE, "empty")
+    bad = list(ok); bad[15] = float("nan")
+    _err(L.spk_conv_fire_sparse(*bad), spk.SPK_E_ARG, "NaN")
+    bad = list(ok); bad[19] = 16
+    _err(L.spk_conv_fire_sparse(*bad), spk.SPK_E_WORKSPACE, "workspace")
+    bad = list(ok); bad[5] = 4096; bad[9] = F16
+    _err(L.spk_conv_fire_sparse(*bad), spk.SPK_E_UNSUPPORTED, "LDS")
+    assert L.spk_conv_fire_sparse_workspace_size(2, 15, 6, 28, 28, 30, 5, 5, 1, 2, F32) > 0
+    assert L.spk_conv_fire_sparse_workspace_size(2, 15, 4096, 28, 28, 30, 5, 5, 1, 2, F16) == 0

@@ -88,3 +88,127 @@ def test_oracle_spike_conv_single_spike_and_truncation():
     sp1, off1 = oracle.times_to_spikes(t, T, cap=1)
     tf1, _ = oracle.conv_fire_spikes(sp1, off1, (Ci, Hi, Wi), w, T, 1, 1, 0.05)
     assert tf1[0, 0, 0, 0] == NEVER and tf1[0, 0, 1, 2] == 2
+
+
+# ------------------------------------------------------ GPU against oracle
+
+import math  # noqa: E402
+
+import torch  # noqa: E402
+
+from parity import check_fire, check_potentials, excused_from_potentials, gpu, np_  # noqa: E402
+from paper_2301_13659_amd import spk  # noqa: E402
+
+
+def _t(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("B,C,H,W,T,dens,cap", [(3, 4, 7, 9, 11, 0.3, None), (2, 64, 64, 64, 30, 0.05, None),
+                                                (2, 5, 33, 17, 254, 0.02, None), (4, 3, 5, 5, 1, 0.6, None),
+                                                (3, 30, 14, 14, 15, 0.8, 500), (2, 2, 3, 3, 4, 0.0, 4)])
+def test_spike_list_conversions_match_oracle(B, C, H, W, T, dens, cap):
+    dev = gpu()
+    rng = np.random.default_rng(C * H + T)
+    t = random_times(rng, (B, C, H, W), T, dens)
+    gs, go = spk.spk_times_to_spikes(_t(t, dev), T, cap)
+    os_, oo = oracle.times_to_spikes(t, T, cap)
+    np.testing.assert_array_equal(np_(go), oo)
+    for b in range(B):
+        nb = min(int(oo[b, T]), os_.shape[1])
+        np.testing.assert_array_equal(np_(gs)[b, :nb].view(np.uint32), os_[b, :nb])
+    back = spk.spk_spikes_to_times(gs, go, (C, H, W), T)
+    np.testing.assert_array_equal(np_(back), oracle.spikes_to_times(os_, oo, (C, H, W), T))
+
+
+SPARSE_CASES = [
+    # B, Ci, Hi, Wi, Co, K, stride, pad, T, theta, density, dtype, signed
+    (2, 6, 28, 28, 30, 5, 1, 2, 15, 6.0, 0.3, "f32", False),
+    (3, 64, 20, 18, 128, 3, 1, 1, 30, 20.0, 0.05, "f16", False),
+    (2, 64, 12, 12, 128, 3, 1, 1, 30, 20.0, 0.10, "f16", False),
+    (2, 30, 14, 14, 250, 3, 1, 1, 15, 10.0, 0.8, "f32", False),
+    (2, 6, 40, 50, 4, 5, 1, 2, 30, 2.0, 0.04, "f32", False),
+    (2, 4, 26, 41, 20, 17, 1, 0, 30, 12.0, 0.2, "f32", False),
+    (2, 5, 13, 11, 7, 3, 2, 1, 9, 1.0, 0.4, "f32", True),
+    (1, 3, 9, 9, 5, 3, 1, 0, 6, -0.5, 0.2, "f32", True),
+    (2, 8, 10, 9, 40, 3, 1, 1, 12, math.inf, 0.5, "f32", False),
+    (1, 64, 7, 7, 33, 5, 1, 2, 8, 50.0, 1.0, "f16", False),
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", SPARSE_CASES)
+def test_conv_fire_sparse_matches_oracle(case):
+    dev = gpu()
+    B, Ci, Hi, Wi, Co, K, s, p, T, theta, dens, dt, signed = case
+    rng = np.random.default_rng(B * 1000 + Ci * 10 + K + Co)
+    t = random_times(rng, (B, Ci, Hi, Wi), T, dens)
+    w = rng.uniform(-0.5 if signed else 0.0, 1.0, size=(Co, Ci, K, K)).astype(np.float32)
+    if dt == "f16":
+        # halves in [0.5, 1): multiples of 2^-11, so every partial sum below
+        # 2^13 is exact in float and the summation order cannot matter
+        w = (0.5 + 0.5 * w).astype(np.float16).astype(np.float32)
+    w_dev = _t(w, dev).to(torch.float16) if dt == "f16" else _t(w, dev)
+    gs, go = spk.spk_times_to_spikes(_t(t, dev), T)
+    g_tf, g_vk = spk.spk_conv_fire_sparse(gs, go, (Ci, Hi, Wi), w_dev, T, s, p, theta)
+    os_, oo = oracle.times_to_spikes(t, T)
+    o_tf, o_vk = oracle.conv_fire_spikes(os_, oo, (Ci, Hi, Wi), w, T, s, p, theta)
+    if math.isinf(theta):
+        assert np.all(np_(g_tf) == NEVER)
+        check_potentials(np_(g_vk), o_vk, "readout v_key")
+        return
+    _, _, o_V = oracle.conv_fire(t, w, T, s, p, theta, potentials=True)
+    exc = excused_from_potentials(o_V, theta)
+    check_fire(np_(g_tf), np_(g_vk), o_tf, o_vk, exc)
+    if dt == "f16":  # exact sums: bit-equal to the dense interface
+        d_tf, d_vk = spk.spk_conv_fire(_t(t, dev), w_dev, T, s, p, theta)
+        assert torch.equal(d_tf, g_tf) and torch.equal(d_vk, g_vk)
+
+
+@pytest.mark.gpu
+def test_conv_fire_sparse_truncated_list_and_repeat():
+    """A list cut at cap is the input without its later spikes; two runs agree
+    bit for bit."""
+    dev = gpu()
+    rng = np.random.default_rng(5)
+    B, Ci, Hi, Wi, Co, T = 2, 8, 12, 12, 16, 10
+    t = random_times(rng, (B, Ci, Hi, Wi), T, 0.3)
+    w = rng.uniform(0, 1, size=(Co, Ci, 3, 3)).astype(np.float32)
+    cap = 60
+    gs, go = spk.spk_times_to_spikes(_t(t, dev), T, cap)
+    g1 = spk.spk_conv_fire_sparse(gs, go, (Ci, Hi, Wi), _t(w, dev), T, 1, 1, 3.0)
+    g2 = spk.spk_conv_fire_sparse(gs, go, (Ci, Hi, Wi), _t(w, dev), T, 1, 1, 3.0)
+    assert torch.equal(g1[0], g2[0]) and torch.equal(g1[1], g2[1])
+    os_, oo = oracle.times_to_spikes(t, T, cap)
+    o_tf, o_vk = oracle.conv_fire_spikes(os_, oo, (Ci, Hi, Wi), w, T, 1, 1, 3.0)
+    cut = oracle.spikes_to_times(os_, oo, (Ci, Hi, Wi), T)
+    _, _, o_V = oracle.conv_fire(cut, w, T, 1, 1, 3.0, potentials=True)
+    check_fire(np_(g1[0]), np_(g1[1]), o_tf, o_vk, excused_from_potentials(o_V, 3.0))
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("density_index", [0, 2])
+def test_conv_fire_sparse_full_spike_input_workload(density_index):
+    """The spike-input layer at its full size (B = 128, 64 x 64 x 64, T = 30,
+    128 maps, fp16 weights): sampled samples against the oracle, the rest
+    against the dense interface, which is exact for these weights."""
+    from paper_2301_13659_amd import workloads as wls
+    dev = gpu()
+    wl = wls.get(5)
+    t = wls.make_spike_times(wl, density_index)
+    spec = wl.convs[0]
+    w = wls.make_weights(wl, 1)
+    w16 = _t(w, dev).to(torch.float16)
+    td = _t(t, dev)
+    gs, go = spk.spk_times_to_spikes(td, wl.T)
+    g_tf, g_vk = spk.spk_conv_fire_sparse(gs, go, t.shape[1:], w16, wl.T, spec.stride, spec.pad,
+                                          spec.theta)
+    d_tf, d_vk = spk.spk_conv_fire(td, w16, wl.T, spec.stride, spec.pad, spec.theta)
+    assert torch.equal(d_tf, g_tf) and torch.equal(d_vk, g_vk)
+    for b in (0, wl.batch - 1):
+        os_, oo = oracle.times_to_spikes(t[b:b + 1], wl.T)
+        o_tf, o_vk = oracle.conv_fire_spikes(os_, oo, t.shape[1:], w, wl.T, spec.stride, spec.pad,
+                                             spec.theta)
+        np.testing.assert_array_equal(np_(g_tf[b:b + 1]), o_tf)
+        np.testing.assert_array_equal(np_(g_vk[b:b + 1]), o_vk)
