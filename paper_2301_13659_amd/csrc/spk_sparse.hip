@@ -17,6 +17,7 @@
 #include <hip/hip_fp16.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "spk_internal.h"
 
@@ -163,38 +164,38 @@ __device__ __forceinline__ int step_of(const int32_t *ob, int T, int32_t j)
     return lo;
 }
 
-// One thread per (sample, stored spike): writes its step at its neuron of
+// Threads of sample blockIdx.y stride over its stored spikes; each writes its
+// step at its neuron of
 // the B x C x H x W time map (dst_pad < 0) or of the padded channels-last
 // buffer [b][y + pad][x + pad][c] (dst_pad >= 0).
 __global__ void k_list_place(const uint32_t *__restrict__ spikes, const int32_t *__restrict__ offsets,
                              int cap, int B, int T, int C, int H, int W, int dst_pad,
                              uint8_t *__restrict__ dst)
 {
-    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (g >= (int64_t)B * cap) return;
-    const int b = (int)(g / cap);
-    const int32_t j = (int32_t)(g - (int64_t)b * cap);
+    const int b = blockIdx.y;
     const int32_t *ob = offsets + (size_t)b * (T + 1);
-    if (j >= ob[T]) return;
-    const uint32_t idx = spikes[g];
+    const int32_t total = min(ob[T], cap);
     const int64_t n = (int64_t)C * H * W;
-    if ((int64_t)idx >= n) return;
-    const uint8_t t = (uint8_t)step_of(ob, T, j);
-    if (dst_pad < 0) {
-        dst[(size_t)b * n + idx] = t;
-        return;
+    for (int32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < total; j += gridDim.x * blockDim.x) {
+        const uint32_t idx = spikes[(size_t)b * cap + j];
+        if ((int64_t)idx >= n) continue;
+        const uint8_t t = (uint8_t)step_of(ob, T, j);
+        if (dst_pad < 0) {
+            dst[(size_t)b * n + idx] = t;
+            continue;
+        }
+        const int c = (int)(idx / (uint32_t)(H * W));
+        const int r = (int)(idx - (uint32_t)c * H * W);
+        const int y = r / W, x = r - y * W;
+        const int Hp = H + 2 * dst_pad, Wp = W + 2 * dst_pad;
+        dst[(((size_t)b * Hp + y + dst_pad) * Wp + x + dst_pad) * C + c] = t;
     }
-    const int c = (int)(idx / (uint32_t)(H * W));
-    const int r = (int)(idx - (uint32_t)c * H * W);
-    const int y = r / W, x = r - y * W;
-    const int Hp = H + 2 * dst_pad, Wp = W + 2 * dst_pad;
-    dst[(((size_t)b * Hp + y + dst_pad) * Wp + x + dst_pad) * C + c] = t;
 }
 
 // ------------------------------------------------------------ event conv
 
 constexpr int kEvMaxWaves = 16;
-constexpr int kEvMaxChunks = 16;  // list capacity per wave <= 64 * this
+constexpr int kEvMaxChunks = 4;  // list capacity per wave <= 64 * this
 constexpr int kEvSlack = 64;
 
 struct EGeom {
@@ -210,16 +211,17 @@ struct EGeom {
     int nruns;  // ceil(P / 4): runs of four positions
     int cap;    // list entries per wave
     int vec;    // outputs aligned for 4-position vector stores
+    int tbits;  // bits of T - 1 (radix passes of the step sort)
     int wchunk; // bytes of one chunk's weight table (multiple of 16)
 };
 
 // Weight table of chunk ch: [tap][CH] with tap = ky*run + kx*Ci + c, zero
-// for maps past Co.
+// for maps past Co, and one zero row at tap = taps.
 template <typename WT, bool kHalfIn>
 __global__ void k_ev_pack_w(const void *__restrict__ wv, EGeom g, uint8_t *__restrict__ wt)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t per = (int64_t)g.taps * g.CH;
+    const int64_t per = (int64_t)(g.taps + 1) * g.CH;  // + a zero row
     if (i >= per * g.NCH) return;
     const int ch = (int)(i / per);
     const int r = (int)(i - (int64_t)ch * per);
@@ -228,7 +230,7 @@ __global__ void k_ev_pack_w(const void *__restrict__ wv, EGeom g, uint8_t *__res
     const int ky = tap / g.run, j = tap - ky * g.run;
     const int kx = j / g.Ci, c = j - kx * g.Ci;
     WT v = (WT)0.0f;
-    if (o < g.Co) {
+    if (o < g.Co && tap < g.taps) {
         const size_t at = (((size_t)o * g.Ci + c) * g.Kh + ky) * g.Kw + kx;
         if (kHalfIn) v = (WT)reinterpret_cast<const _Float16 *>(wv)[at];
         else v = (WT)reinterpret_cast<const float *>(wv)[at];
@@ -236,22 +238,68 @@ __global__ void k_ev_pack_w(const void *__restrict__ wv, EGeom g, uint8_t *__res
     reinterpret_cast<WT *>(wt + (size_t)ch * g.wchunk)[r] = v;
 }
 
+// The weights of one table row for this lane's maps, as floats.
 template <typename WT, int MPL>
-__device__ __forceinline__ void add_row(float (&V)[MPL], const WT *row)
+__device__ __forceinline__ void load_row(const WT *row, float (&w)[MPL])
 {
     if constexpr (MPL == 2) {
         if constexpr (sizeof(WT) == 2) {
             typedef _Float16 hh2 __attribute__((ext_vector_type(2)));
-            const hh2 w = *reinterpret_cast<const hh2 *>(row);
-            V[0] += (float)w[0];
-            V[1] += (float)w[1];
+            const hh2 v = *reinterpret_cast<const hh2 *>(row);
+            w[0] = (float)v[0];
+            w[1] = (float)v[1];
         } else {
-            const float2 w = *reinterpret_cast<const float2 *>(row);
-            V[0] += w.x;
-            V[1] += w.y;
+            const float2 v = *reinterpret_cast<const float2 *>(row);
+            w[0] = v.x;
+            w[1] = v.y;
         }
     } else {
-        V[0] += (float)row[0];
+        w[0] = (float)row[0];
+    }
+}
+
+template <typename WT, int MPL>
+__device__ __forceinline__ void add_row(float (&V)[MPL], const WT *row)
+{
+    float w[MPL];
+    load_row<WT, MPL>(row, w);
+#pragma unroll
+    for (int q = 0; q < MPL; q++) V[q] += w[q];
+}
+
+// Raw table words of one row (two halves or one float per map) and their
+// accumulation: a half is widened inside a fused multiply-add by 1, which
+// rounds once, exactly as the float addition of the widened half.
+template <typename WT, int MPL>
+struct RowBits {
+    typedef typename std::conditional<sizeof(WT) == 2, uint32_t,
+                                      typename std::conditional<MPL == 2, float2, float>::type>::type type;
+};
+
+template <typename WT, int MPL>
+__device__ __forceinline__ typename RowBits<WT, MPL>::type load_bits(const uint8_t *p)
+{
+    if constexpr (sizeof(WT) == 2) {
+        if constexpr (MPL == 2) return *reinterpret_cast<const uint32_t *>(p);
+        else return (uint32_t)*reinterpret_cast<const uint16_t *>(p);
+    } else {
+        return *reinterpret_cast<const typename RowBits<WT, MPL>::type *>(p);
+    }
+}
+
+template <typename WT, int MPL>
+__device__ __forceinline__ void acc_bits(float (&V)[MPL], typename RowBits<WT, MPL>::type b)
+{
+    if constexpr (sizeof(WT) == 2) {
+        typedef _Float16 hh2 __attribute__((ext_vector_type(2)));
+        const hh2 h = __builtin_bit_cast(hh2, b);
+        V[0] = __builtin_fmaf((float)h[0], 1.0f, V[0]);
+        if constexpr (MPL == 2) V[1] = __builtin_fmaf((float)h[1], 1.0f, V[1]);
+    } else if constexpr (MPL == 2) {
+        V[0] += b.x;
+        V[1] += b.y;
+    } else {
+        V[0] += b;
     }
 }
 
@@ -267,20 +315,67 @@ __device__ __forceinline__ void fire_check(const float (&V)[MPL], float theta, u
     }
 }
 
-// One output position for this wave's maps: compact the spikes of the
-// window into the wave's list (tap << 8 | t, in tap order), then walk the
-// steps; each step adds the weights of its spikes in tap order and, if it
-// brought any (or is step 0), tests theta.  A window with more spikes than
-// the list holds is walked by rescanning it once per step.
-template <typename WT, int MPL>
-__device__ __forceinline__ void ev_position(const uint8_t *__restrict__ xp, const WT *sw,
-                                            uint32_t *list, const EGeom &g, int p, int lane,
-                                            int col, float theta, bool readout,
-                                            uint32_t (&tf)[MPL], float (&vk)[MPL])
+template <int MPL>
+__device__ __forceinline__ bool all_fired(const uint32_t (&tf)[MPL])
 {
-    const int b = p / g.HoWo, rem = p - b * g.HoWo;
-    const int y = rem / g.Wo, x = rem - y * g.Wo;
-    const uint8_t *org = xp + ((size_t)(b * g.Hp + y * g.stride) * g.Wp + x * g.stride) * g.Ci;
+    bool open = false;
+#pragma unroll
+    for (int q = 0; q < MPL; q++) open |= tf[q] == (uint32_t)spk::kNever;
+    return !__ballot(open);
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+constexpr int kEvLoads = 16;  // window loads of a position kept in flight
+
+// Load i of a window covers taps [64 * (i % nch), +64) of kernel row
+// i / nch.  off: this lane's byte offset from the window origin (0 where the
+// lane has no tap, so every load stays inside the window); rowo: the byte
+// offset of the lane's tap row in the weight table, -1 where it has none.
+template <typename WT>
+__device__ __forceinline__ void window_tables(const EGeom &g, int lane, int (&off)[kEvLoads],
+                                              int (&rowo)[kEvLoads])
+{
+#pragma unroll
+    for (int i = 0; i < kEvLoads; i++) {
+        const int ky = i / g.nch, j = i - ky * g.nch;
+        const int k = j * 64 + lane;
+        const bool ok = i < g.Kh * g.nch && k < g.run;
+        off[i] = ok ? ky * g.rowb + k : 0;
+        rowo[i] = ok ? (ky * g.run + k) * g.CH * (int)sizeof(WT) : -1;
+    }
+}
+
+__device__ __forceinline__ void window_load(const uint8_t *org, const int (&off)[kEvLoads], int nload,
+                                            uint32_t (&buf)[kEvLoads])
+{
+#pragma unroll
+    for (int i = 0; i < kEvLoads; i++)
+        if (i < nload) buf[i] = org[off[i]];
+}
+
+// One output position for this wave's maps.  The spikes of the window are
+// compacted into the wave's list as (row << 8 | t), row being the byte
+// offset of the spike's tap in the weight table, in tap order.
+//  - n <= 64: the list, one entry per lane, is sorted by t with a stable
+//    radix sort (ballots and a lane permute per bit); lanes past n hold an
+//    entry of the zero row at step 255.  It is walked in order, four table
+//    reads in flight, and theta is tested after the last spike of each step.
+//  - n <= cap: the steps are walked one by one, each adding its spikes in
+//    tap order from up to four 64-entry chunks.
+//  - otherwise the window is rescanned once per step.
+// Within a step the weights are added in tap order on every path.
+template <typename WT, int MPL>
+__device__ __forceinline__ void ev_position(const uint8_t *__restrict__ org, bool pf,
+                                            const uint32_t (&buf)[kEvLoads],
+                                            const int (&rowo)[kEvLoads], const uint8_t *swb,
+                                            uint32_t *list, const EGeom &g, int lane, int colb,
+                                            float theta, bool test, uint32_t (&tf)[MPL],
+                                            float (&vk)[MPL])
+{
     float V[MPL];
 #pragma unroll
     for (int q = 0; q < MPL; q++) {
@@ -288,23 +383,74 @@ __device__ __forceinline__ void ev_position(const uint8_t *__restrict__ xp, cons
         tf[q] = spk::kNever;
         vk[q] = 0.0f;
     }
+    const int rowbytes = g.CH * (int)sizeof(WT);
     int n = 0;
-    for (int ky = 0; ky < g.Kh; ky++) {
-        const uint8_t *row = org + (size_t)ky * g.rowb;
-        for (int j = 0; j < g.nch; j++) {
-            const int k = j * 64 + lane;
-            const uint32_t t = k < g.run ? (uint32_t)row[k] : 255u;
-            const bool act = t < (uint32_t)g.T;
-            const uint64_t m = __ballot(act);
-            if (m) {
-                const int slot = n + (int)__builtin_amdgcn_mbcnt_hi(
-                                         (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-                if (act && slot < g.cap) list[slot] = ((uint32_t)(ky * g.run + k) << 8) | t;
+    if (pf) {
+        const int nload = g.Kh * g.nch;
+#pragma unroll
+        for (int i = 0; i < kEvLoads; i++) {
+            if (i < nload) {
+                const uint32_t t = buf[i];
+                const bool act = t < (uint32_t)g.T && rowo[i] >= 0;
+                const uint64_t m = __ballot(act);
+                int slot = n + (int)lanes_below(m);
+                slot = act && slot < g.cap ? slot : g.cap;  // the spare slot
+                list[slot] = ((uint32_t)rowo[i] << 8) | t;
+                n += __popcll(m);
+            }
+        }
+    } else {
+        for (int ky = 0; ky < g.Kh; ky++) {
+            const uint8_t *row = org + (size_t)ky * g.rowb;
+            for (int j = 0; j < g.nch; j++) {
+                const int k = j * 64 + lane;
+                const uint32_t t = k < g.run ? (uint32_t)row[k] : 255u;
+                const bool act = t < (uint32_t)g.T;
+                const uint64_t m = __ballot(act);
+                int slot = n + (int)lanes_below(m);
+                slot = act && slot < g.cap ? slot : g.cap;
+                list[slot] = ((uint32_t)((ky * g.run + k) * rowbytes) << 8) | t;
                 n += __popcll(m);
             }
         }
     }
-    if (n <= g.cap) {
+    if (n <= 64) {
+        const uint32_t dummy = ((uint32_t)(g.taps * rowbytes) << 8) | 0xFFu;
+        uint32_t e = lane < n ? list[lane] : dummy;
+        for (int k = 0; k < g.tbits; k++) {
+            const bool one = (e >> k) & 1u;
+            const uint64_t m0 = __ballot(!one);
+            const int dest = one ? __popcll(m0) + (int)lanes_below(~m0) : (int)lanes_below(m0);
+            e = (uint32_t)__builtin_amdgcn_ds_permute(dest << 2, (int)e);
+        }
+        // entries that end a step: the next one has another t
+        uint32_t en1 = (uint32_t)__builtin_amdgcn_ds_bpermute(((lane + 1) & 63) << 2, (int)e);
+        en1 = lane == 63 ? dummy : en1;
+        const uint64_t ends = __ballot((e & 0xFFu) != (en1 & 0xFFu) && (e & 0xFFu) != 0xFFu);
+        if (test && theta < 0.0f) {
+            const uint32_t t0 = (uint32_t)__builtin_amdgcn_readlane((int)e, 0) & 0xFFu;
+            if (t0 != 0) fire_check<MPL>(V, theta, 0u, tf, vk);
+        }
+        for (int i = 0; i < n; i += 4) {
+            uint32_t en[4];
+            typename RowBits<WT, MPL>::type w[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                en[k] = (uint32_t)__builtin_amdgcn_readlane((int)e, i + k);
+                w[k] = load_bits<WT, MPL>(swb + (en[k] >> 8) + colb);
+            }
+            bool tested = false;
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                acc_bits<WT, MPL>(V, w[k]);
+                if (test && ((ends >> (i + k)) & 1u)) {
+                    fire_check<MPL>(V, theta, en[k] & 0xFFu, tf, vk);
+                    tested = true;
+                }
+            }
+            if (tested && all_fired<MPL>(tf)) break;
+        }
+    } else if (n <= g.cap) {
         const int nc = (n + 63) >> 6;
         uint32_t e[kEvMaxChunks];
 #pragma unroll
@@ -321,18 +467,15 @@ __device__ __forceinline__ void ev_position(const uint8_t *__restrict__ xp, cons
                         const int i = __builtin_ctzll(m);
                         m &= m - 1;
                         const uint32_t ent = (uint32_t)__builtin_amdgcn_readlane((int)e[c], i);
-                        add_row<WT, MPL>(V, sw + (size_t)(ent >> 8) * g.CH + col);
+                        add_row<WT, MPL>(V, reinterpret_cast<const WT *>(swb + (ent >> 8) + colb));
                         any = true;
                         left--;
                     }
                 }
             }
-            if (!readout && (any || t == 0)) {
+            if (test && (any || t == 0)) {
                 fire_check<MPL>(V, theta, (uint32_t)t, tf, vk);
-                bool open = false;
-#pragma unroll
-                for (int q = 0; q < MPL; q++) open |= tf[q] == (uint32_t)spk::kNever;
-                if (!__ballot(open)) break;
+                if (all_fired<MPL>(tf)) break;
             }
         }
     } else {
@@ -347,21 +490,49 @@ __device__ __forceinline__ void ev_position(const uint8_t *__restrict__ xp, cons
                     while (m) {
                         const int i = __builtin_ctzll(m);
                         m &= m - 1;
-                        add_row<WT, MPL>(V, sw + (size_t)(ky * g.run + j * 64 + i) * g.CH + col);
+                        const uint32_t ro = (uint32_t)((ky * g.run + j * 64 + i) * rowbytes);
+                        add_row<WT, MPL>(V, reinterpret_cast<const WT *>(swb + ro + colb));
                         any = true;
                     }
                 }
             }
-            if (!readout && (any || t == 0)) fire_check<MPL>(V, theta, (uint32_t)t, tf, vk);
+            if (test && (any || t == 0)) fire_check<MPL>(V, theta, (uint32_t)t, tf, vk);
         }
     }
 #pragma unroll
     for (int q = 0; q < MPL; q++) vk[q] = tf[q] == (uint32_t)spk::kNever ? V[q] : vk[q];
 }
 
+// Output position p as (sample, row, column), advanced one position at a time.
+struct PosIt {
+    int b, y, x;
+    __device__ void set(const EGeom &g, int p)
+    {
+        b = p / g.HoWo;
+        const int rem = p - b * g.HoWo;
+        y = rem / g.Wo;
+        x = rem - y * g.Wo;
+    }
+    __device__ void next(const EGeom &g)
+    {
+        if (++x == g.Wo) {
+            x = 0;
+            if (++y == g.Ho) {
+                y = 0;
+                b++;
+            }
+        }
+    }
+    __device__ const uint8_t *origin(const uint8_t *xp, const EGeom &g) const
+    {
+        return xp + ((size_t)(b * g.Hp + y * g.stride) * g.Wp + x * g.stride) * g.Ci;
+    }
+};
+
 // Block -> (map chunk, range of position runs); the chunks of a range sit
 // on one XCD.  Each wave takes every nwaves-th run of four consecutive
-// positions and writes a map's four results with one store each for the
+// positions, loads each position's window while the previous one is being
+// processed, and writes a map's four results with one store each for the
 // times and the potentials.
 template <typename WT, int MPL>
 __global__ __launch_bounds__(64 * kEvMaxWaves) void k_fire_ev(const uint8_t *__restrict__ xp,
@@ -384,42 +555,79 @@ __global__ __launch_bounds__(64 * kEvMaxWaves) void k_fire_ev(const uint8_t *__r
         for (int i = threadIdx.x; i < g.wchunk / 16; i += blockDim.x) dst[i] = src[i];
     }
     __syncthreads();
-    const WT *sw = reinterpret_cast<const WT *>(lds);
-    uint32_t *list = reinterpret_cast<uint32_t *>(lds + g.wchunk) + (size_t)wave * g.cap;
-    const int col = min(lane * MPL, g.CH - MPL);
-    const bool readout = __builtin_isinf(theta) && theta > 0.0f;
+    uint32_t *list = reinterpret_cast<uint32_t *>(lds + g.wchunk) + (size_t)wave * (g.cap + 1);
+    const int colb = min(lane * MPL, g.CH - MPL) * (int)sizeof(WT);
+    const bool test = !(__builtin_isinf(theta) && theta > 0.0f);
     const int r_begin = (int)((long long)range * g.nruns / nranges);
     const int r_end = (int)((long long)(range + 1) * g.nruns / nranges);
-    for (int r = r_begin + wave; r < r_end; r += nwaves) {
+    int off[kEvLoads], rowo[kEvLoads];
+    window_tables<WT>(g, lane, off, rowo);
+    const int nload = g.Kh * g.nch;
+    const bool pf = nload <= kEvLoads;
+    uint32_t cur[kEvLoads], nxt[kEvLoads];
+    int r = r_begin + wave;
+    PosIt pos, pn;
+    if (r < r_end) {
+        pos.set(g, 4 * r);
+        if (pf) window_load(pos.origin(xp, g), off, nload, cur);
+    }
+    for (; r < r_end; r += nwaves) {
         const int p0 = 4 * r;
-        uint32_t tf[4][MPL];
-        float vk[4][MPL];
+        const int cnt = min(4, g.P - p0);
+        uint32_t tpack[MPL];
+        float v4[MPL][4];
 #pragma unroll
-        for (int k = 0; k < 4; k++) {
-            if (p0 + k < g.P)
-                ev_position<WT, MPL>(xp, sw, list, g, p0 + k, lane, col, theta, readout, tf[k], vk[k]);
+        for (int mq = 0; mq < MPL; mq++) {
+            tpack[mq] = 0u;
+#pragma unroll
+            for (int k = 0; k < 4; k++) v4[mq][k] = 0.0f;
         }
+#pragma unroll 1
+        for (int k = 0; k < cnt; k++) {
+            // the next position of this wave: the following one, or the
+            // first of its next run
+            const bool last = k == cnt - 1;
+            const bool more = !last || r + nwaves < r_end;
+            if (more) {
+                pn = pos;
+                if (!last) pn.next(g);
+                else pn.set(g, 4 * (r + nwaves));
+                if (pf) window_load(pn.origin(xp, g), off, nload, nxt);
+            }
+            uint32_t tf[MPL];
+            float vk[MPL];
+            ev_position<WT, MPL>(pos.origin(xp, g), pf, cur, rowo, lds, list, g, lane, colb, theta,
+                                 test, tf, vk);
+#pragma unroll
+            for (int mq = 0; mq < MPL; mq++) {
+                tpack[mq] |= tf[mq] << (8 * k);
+#pragma unroll
+                for (int kk = 0; kk < 4; kk++) v4[mq][kk] = kk == k ? vk[mq] : v4[mq][kk];
+            }
+            if (more) {
+                pos = pn;
+#pragma unroll
+                for (int i = 0; i < kEvLoads; i++) cur[i] = nxt[i];
+            }
+        }
+        const int b0 = p0 / g.HoWo, rem0 = p0 - b0 * g.HoWo;
 #pragma unroll
         for (int mq = 0; mq < MPL; mq++) {
             const int cc = lane * MPL + mq;
             const int o = ch * g.CH + cc;
             if (cc >= g.CH || o >= g.Co) continue;
-            const int b0 = p0 / g.HoWo, rem0 = p0 - b0 * g.HoWo;
-            if (g.vec && p0 + 3 < g.P) {
+            if (g.vec && cnt == 4) {
                 const size_t at = ((size_t)b0 * g.Co + o) * g.HoWo + rem0;
-                *reinterpret_cast<uint32_t *>(out_t + at) =
-                    tf[0][mq] | (tf[1][mq] << 8) | (tf[2][mq] << 16) | (tf[3][mq] << 24);
+                *reinterpret_cast<uint32_t *>(out_t + at) = tpack[mq];
                 *reinterpret_cast<float4 *>(out_v + at) =
-                    make_float4(vk[0][mq], vk[1][mq], vk[2][mq], vk[3][mq]);
+                    make_float4(v4[mq][0], v4[mq][1], v4[mq][2], v4[mq][3]);
             } else {
-#pragma unroll
-                for (int k = 0; k < 4; k++) {
+                for (int k = 0; k < cnt; k++) {
                     const int p = p0 + k;
-                    if (p >= g.P) break;
                     const int b = p / g.HoWo, rem = p - b * g.HoWo;
                     const size_t at = ((size_t)b * g.Co + o) * g.HoWo + rem;
-                    out_t[at] = (uint8_t)tf[k][mq];
-                    out_v[at] = vk[k][mq];
+                    out_t[at] = (uint8_t)(tpack[mq] >> (8 * k));
+                    out_v[at] = k == 0 ? v4[mq][0] : k == 1 ? v4[mq][1] : k == 2 ? v4[mq][2] : v4[mq][3];
                 }
             }
         }
@@ -465,20 +673,22 @@ bool ev_plan(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int s
     g.HoWo = g.Ho * g.Wo;
     g.P = B * g.HoWo;
     g.nruns = (g.P + 3) / 4;
+    g.tbits = 0;
+    while ((1 << g.tbits) < T) g.tbits++;
     const int wb = half_w ? 2 : 4;
     const int lds_max = ev_lds_block();
     for (int CH : {128, 64, 32}) {
         if (CH > 32 && Co <= CH / 2) continue;  // a smaller chunk holds every map
         g.CH = CH;
         g.NCH = (Co + CH - 1) / CH;
-        g.wchunk = (int)spk::align_up((size_t)g.taps * CH * wb, 16);
+        g.wchunk = (int)spk::align_up((size_t)(g.taps + 1) * CH * wb, 16);
         for (int wv : {kEvMaxWaves, 8}) {
             long long room = (long long)lds_max - g.wchunk;
-            int cap = room > 0 ? (int)std::min<long long>(64 * kEvMaxChunks, room / (wv * 4) / 64 * 64) : 0;
+            int cap = room > 0 ? (int)std::min<long long>(64 * kEvMaxChunks, (room / (wv * 4) - 1) / 64 * 64) : 0;
             if (cap >= 64) {
                 g.cap = cap;
                 waves = wv;
-                lds = (size_t)g.wchunk + (size_t)wv * cap * 4;
+                lds = (size_t)g.wchunk + (size_t)wv * (cap + 1) * 4;
                 return true;
             }
         }
@@ -563,9 +773,8 @@ extern "C" spk_status spk_spikes_to_times(const uint32_t *spikes, const int32_t 
     const size_t total = (size_t)B * n;
     hipLaunchKernelGGL(k_fill_u8, dim3((unsigned)std::min<size_t>(4096, (total / 16 + 255) / 256 + 1)),
                        dim3(256), 0, s, times, total, (uint8_t)spk::kNever);
-    const int64_t nthreads = (int64_t)B * cap;
-    if (nthreads > 0)
-        hipLaunchKernelGGL(k_list_place, dim3((unsigned)((nthreads + 255) / 256)), dim3(256), 0, s,
+    if (cap > 0)
+        hipLaunchKernelGGL(k_list_place, dim3(std::min(64, (cap + 4095) / 4096), B), dim3(256), 0, s,
                            spikes, offsets, cap, B, T, C, H, W, -1, times);
     SPK_LAUNCHED("spk_spikes_to_times");
     return SPK_OK;
@@ -630,11 +839,10 @@ extern "C" spk_status spk_conv_fire_sparse(const uint32_t *spikes, const int32_t
     const size_t xb = ev_xp_bytes(g);
     hipLaunchKernelGGL(k_fill_u8, dim3((unsigned)std::min<size_t>(4096, (xb / 16 + 255) / 256 + 1)),
                        dim3(256), 0, s, xp, xb, (uint8_t)T);
-    const int64_t nthreads = (int64_t)B * cap;
-    if (nthreads > 0)
-        hipLaunchKernelGGL(k_list_place, dim3((unsigned)((nthreads + 255) / 256)), dim3(256), 0, s,
+    if (cap > 0)
+        hipLaunchKernelGGL(k_list_place, dim3(std::min(64, (cap + 4095) / 4096), B), dim3(256), 0, s,
                            spikes, offsets, cap, B, T, Ci, Hi, Wi, pad, xp);
-    const int64_t nw = (int64_t)g.NCH * g.taps * g.CH;
+    const int64_t nw = (int64_t)g.NCH * (g.taps + 1) * g.CH;
     if (half_w)
         hipLaunchKernelGGL((k_ev_pack_w<_Float16, true>), dim3((unsigned)((nw + 255) / 256)), dim3(256),
                            0, s, w, g, wt);
