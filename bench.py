@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=2, help="1..5 (default: three-layer net)")
     ap.add_argument("--density", type=int, default=1, help="spike-density index of workload 5")
+    ap.add_argument("--sparse", action="store_true",
+                    help="spike-input workloads: take the input as a spike list (sparse interface)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU budget of the oracle baseline (0 disables it)")
     ap.add_argument("--no-breakdown", action="store_true")
@@ -92,6 +94,10 @@ def hbm_stages(wl, pipe, kept, stage_ms):
     if kept.dog is not None:
         put("dog", pipe.images.numel() + kept.dog.numel() * 4)
         put("code", kept.dog.numel() * 4 + kept.times0.numel())
+    if pipe.spike_list is not None:
+        # time map written once, the list and its offsets read once
+        nsp = int(pipe.spike_list[1][:, -1].sum().item())
+        put("unpack", pipe.spike_input.numel() + 4 * nsp + pipe.spike_list[1].numel() * 4)
     pi = 0
     li = 0
     t = kept.times0 if kept.times0 is not None else pipe.spike_input
@@ -132,7 +138,7 @@ def fanout_events(t_in, spec, torch):
     return float((fired * cover.to(torch.float64)).sum().item()) * spec.co
 
 
-def cpu_baseline(wl, budget_s):
+def cpu_baseline(wl, budget_s, sparse=False):
     """The oracle (plain C, one thread) on whole samples of the same workload until the
     budget is spent; samples/s."""
     import numpy as np
@@ -160,7 +166,12 @@ def cpu_baseline(wl, budget_s):
             if kind == "pool":
                 t = oracle.pool(t, s.k, s.stride, s.pad)
                 continue
-            tf, vk = oracle.conv_fire(t, ws[li], wl.T, s.stride, s.pad, s.theta)
+            if sparse and li == 0:
+                sp, off = oracle.times_to_spikes(t, wl.T)
+                tf, vk = oracle.conv_fire_spikes(sp, off, t.shape[1:], ws[li], wl.T, s.stride, s.pad,
+                                                 s.theta)
+            else:
+                tf, vk = oracle.conv_fire(t, ws[li], wl.T, s.stride, s.pad, s.theta)
             if s.stdp or s.readout:
                 cand = tf if s.readout else oracle.inhibit(tf, vk)
                 win, n = oracle.kwta(cand, vk, wl.T, s.k_win, s.radius, s.readout)
@@ -191,7 +202,7 @@ def main():
 
     dev = torch.device("cuda:0")
     wl = wls.get(args.workload)
-    pipe = Pipeline(wl, dev, density_index=args.density)
+    pipe = Pipeline(wl, dev, density_index=args.density, sparse=args.sparse)
     work = conv_work(wl)
     flops_dense = conv_flops(wl)
 
@@ -258,11 +269,19 @@ def main():
     hbm = hbm_stages(wl, pipe, kept, stage_ms) if per_layer else {}
 
     achieved = work[dom][0] / (dom_ms * 1e-3) / 1e12
+    sparse_dom = args.sparse and dom == 0
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_F16_MFMA_TFLOPS,
                 "unit": "TFLOP/s", "frac": achieved / PEAK_F16_MFMA_TFLOPS,
-                "traffic": measured_traffic(wl, dom + 1),
-                "kernel": f"spk_conv_fire ({dom_name})", "kernel_ms": dom_ms,
+                "traffic": None if sparse_dom else measured_traffic(wl, dom + 1),
+                "kernel": f"spk_conv_fire{'_sparse' if sparse_dom else ''} ({dom_name})",
+                "kernel_ms": dom_ms,
                 "work": f"{work[dom][1]} = {work[dom][0]:.4g} flop per launch"}
+    if sparse_dom:
+        # the event conv does not compute the dense product: its frac is the
+        # dense-equivalent rate, above 1 where the skipped work outweighs
+        roofline["effective"] = True
+        if per_layer:
+            roofline["events_per_s"] = per_layer[0]["events_per_s"]
     line = {
         "metric": "samples/sec and synaptic events/sec per layer; % fp16 MFMA / HBM peak",
         "value": value, "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
@@ -273,8 +292,10 @@ def main():
         "per_layer": per_layer, "stage_ms": stage_ms, "hbm_stages": hbm, "roofline": roofline,
         "library": spk.version(),
     }
+    if args.sparse:
+        line["config"]["interface"] = "sparse (spike-list input)"
     if args.cpu_seconds > 0:
-        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, sparse=args.sparse)
     print(json.dumps(line))
 
 

@@ -39,15 +39,25 @@ class StepOutputs:
 
 
 class Pipeline:
-    def __init__(self, wl: wls.Workload, device="cuda", density_index: int = 0):
+    def __init__(self, wl: wls.Workload, device="cuda", density_index: int = 0, sparse: bool = False):
+        """sparse: a spike-input workload takes its input as a spike list (the
+        sparse interface of §II-B): the first conv layer runs
+        spk_conv_fire_sparse on it, and the step rebuilds the input time map
+        for STDP with spk_spikes_to_times."""
         self.wl = wl
         self.device = torch.device(device)
+        self.sparse = sparse
+        self.spike_list = None
         if wl.image_hw is not None:
+            if sparse:
+                raise ValueError("the sparse interface takes a spike input; this workload codes images")
             self.images = torch.from_numpy(wls.make_images(wl)).to(self.device)
             self.spike_input = None
         else:
             self.images = None
             self.spike_input = torch.from_numpy(wls.make_spike_times(wl, density_index)).to(self.device)
+            if sparse:
+                self.spike_list = spk.spk_times_to_spikes(self.spike_input, wl.T)
         self.layers = []
         for li, spec in enumerate(wl.convs, start=1):
             w = torch.from_numpy(wls.make_weights(wl, li)).to(self.device)
@@ -90,6 +100,8 @@ class Pipeline:
             t = timed("code", lambda: spk.spk_latency_code(x, wl.T, wl.min_value))
             if keep:
                 out.dog, out.times0 = x, t
+        elif self.spike_list is not None:
+            t = None  # rebuilt from the list where a stage needs the time map
         else:
             t = self.spike_input
         li = 0
@@ -104,8 +116,15 @@ class Pipeline:
             layer = self.layers[li]
             w_op = layer.w16 if layer.w16 is not None else layer.w
             n = li + 1
-            tf, vk = timed(f"conv{n}", lambda: spk.spk_conv_fire(t, w_op, wl.T, s.stride, s.pad,
-                                                                 s.theta))
+            if t is None:
+                sp, off = self.spike_list
+                tf, vk = timed(f"conv{n}", lambda: spk.spk_conv_fire_sparse(
+                    sp, off, wl.input_chw(), w_op, wl.T, s.stride, s.pad, s.theta))
+                if (s.stdp and learn) or keep:
+                    t = timed("unpack", lambda: spk.spk_spikes_to_times(sp, off, wl.input_chw(), wl.T))
+            else:
+                tf, vk = timed(f"conv{n}", lambda: spk.spk_conv_fire(t, w_op, wl.T, s.stride, s.pad,
+                                                                     s.theta))
             if keep:
                 out.layer_in.append(t)
                 out.layer_out.append((tf, vk))

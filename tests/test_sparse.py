@@ -212,3 +212,25 @@ def test_conv_fire_sparse_full_spike_input_workload(density_index):
                                              spec.theta)
         np.testing.assert_array_equal(np_(g_tf[b:b + 1]), o_tf)
         np.testing.assert_array_equal(np_(g_vk[b:b + 1]), o_vk)
+
+
+@pytest.mark.gpu
+def test_sparse_pipeline_step_equals_dense_step():
+    """A training step of the spike-input workload through the sparse
+    interface gives the dense step's spikes, winners and weights."""
+    from paper_2301_13659_amd import workloads as wls
+    from paper_2301_13659_amd.pipeline import Pipeline
+    dev = gpu()
+    wl = wls.get(5)
+    dense = Pipeline(wl, dev, density_index=0)
+    sparse = Pipeline(wl, dev, density_index=0, sparse=True)
+    od = dense.step(keep=True)
+    os_ = sparse.step(keep=True)
+    assert torch.equal(od.layer_in[0], os_.layer_in[0])
+    for (a, b), (c, d) in zip(od.layer_out, os_.layer_out):
+        assert torch.equal(a, c) and torch.equal(b, d)
+    for k in od.winners:
+        assert torch.equal(od.winners[k][0], os_.winners[k][0])
+        assert torch.equal(od.winners[k][1], os_.winners[k][1])
+    for ld, ls in zip(dense.layers, sparse.layers):
+        assert torch.equal(ld.w, ls.w)
