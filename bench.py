@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, help="1..5 (default: three-layer net)")
+    ap.add_argument("--workload", type=int, default=2, help="1..6 (default: three-layer net)")
     ap.add_argument("--density", type=int, default=1, help="spike-density index of workload 5")
     ap.add_argument("--sparse", action="store_true",
                     help="spike-input workloads: take the input as a spike list (sparse interface)")
@@ -93,6 +93,7 @@ def hbm_stages(wl, pipe, kept, stage_ms):
 
     if kept.dog is not None:
         put("dog", pipe.images.numel() + kept.dog.numel() * 4)
+        put("threshold", kept.dog.numel() * 8)
         put("code", kept.dog.numel() * 4 + kept.times0.numel())
     if pipe.spike_list is not None:
         # time map written once, the list and its offsets read once
@@ -102,6 +103,9 @@ def hbm_stages(wl, pipe, kept, stage_ms):
     li = 0
     t = kept.times0 if kept.times0 is not None else pipe.spike_input
     for kind, s in wl.stages:
+        if kind == "gather":
+            put("gather", t.numel() * 5)
+            continue
         if kind == "pool":
             out = kept.pooled[pi]
             pi += 1
@@ -152,17 +156,24 @@ def cpu_baseline(wl, budget_s, sparse=False):
     labels = wls.make_labels(wl)
     cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
     filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
+    if wl.log_stds:
+        filters = oracle.log_filters(wl.log_stds, wl.log_ksize)
     done = 0
     t0 = time.perf_counter()
     while done < wl.batch and time.perf_counter() - t0 < budget_s:
         b = done
         if imgs is not None:
             x = oracle.dog_filter(imgs[b:b + 1], filters)
+            if wl.pre_threshold is not None:
+                x = oracle.threshold(x, wl.pre_threshold, 0.0)
             t = oracle.latency_code(x, wl.T, wl.min_value)
         else:
             t = spikes[b:b + 1]
         li = 0
         for kind, s in wl.stages:
+            if kind == "gather":
+                oracle.gather(t, wl.T)
+                continue
             if kind == "pool":
                 t = oracle.pool(t, s.k, s.stride, s.pad)
                 continue

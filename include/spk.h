@@ -305,6 +305,41 @@ spk_status spk_fc_stdp_update(float *w, uint16_t *w_f16, int O, int I, const uin
                               const spk_stdp_config *cfg, int n_cfg, const int32_t *winner_cfg,
                               void *ws, size_t ws_bytes, spk_stream stream);
 
+/*
+ * spk_log_filter -- Laplacian-of-Gaussian bank (§II-C.3): each deviation s
+ * is approximated by two DoG filters, on-centre (s/sqrt 2, s*sqrt 2) and
+ * off-centre (s*sqrt 2, s/sqrt 2), applied as spk_dog_filter does (output
+ * channel c*2n + 2i for the on-centre filter of stds[i], + 1 for the off one).
+ *   stds   n_std deviations (host), 1 <= n_std <= 4; ksize odd; pad as in
+ *          spk_dog_filter.
+ * Errors: those of spk_dog_filter, SPK_E_ARG (deviation <= 0 or not finite),
+ * SPK_E_SHAPE (n_std > 4).
+ */
+spk_status spk_log_filter(const uint8_t *img, int B, int C, int H, int W, const float *stds,
+                          int n_std, int ksize, int pad, float *out, spk_stream stream);
+
+/*
+ * spk_threshold -- in place, x = x if x > threshold else value (n floats,
+ * device).  Applied to filter outputs before coding, it silences the weak
+ * responses (§IV's example uses 0.01); NaN becomes value.
+ */
+spk_status spk_threshold(float *x, int64_t n, float threshold, float value, spk_stream stream);
+
+/*
+ * spk_quantize -- binarize trained weights (§IV): w = lower if w < mid else
+ * upper, in place on the float master (n values, device), and the half copy
+ * w_f16 (nullable) set to the same values.
+ */
+spk_status spk_quantize(float *w, uint16_t *w_f16, int64_t n, float lower, float mid, float upper,
+                        spk_stream stream);
+
+/*
+ * spk_gather -- feature values of a spike output (§IV): per neuron, the
+ * number of steps at which its cumulative frame is on, T - t for a neuron
+ * that fired at t, else 0.  times uint8 (n, device) -> out float (n, device).
+ */
+spk_status spk_gather(const uint8_t *times, int64_t n, int T, float *out, spk_stream stream);
+
 /* ---------------------------------------------------------------------- */
 /* Sparse interface (§II-B): the indices of the spikes instead of full     */
 /* buffers.                                                                */

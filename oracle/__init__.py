@@ -8,6 +8,7 @@ never does, and the two share no code.  All arrays are numpy, C-contiguous.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 import subprocess
 
@@ -59,6 +60,9 @@ def lib():
         L.or_rstdp_select.argtypes = [P, P, i, i, P, i, P]
         L.or_fc_wta.argtypes = [P, P, i, i, i, i, i, i, P, P]
         L.or_times_to_spikes.argtypes = [P, i, i64, i, i, P, P]
+        L.or_threshold.argtypes = [P, i64, f, f]
+        L.or_quantize.argtypes = [P, i64, f, f, f]
+        L.or_gather.argtypes = [P, i64, i, P]
         L.or_spikes_to_times.argtypes = [P, P, i, i64, i, i, P]
         L.or_conv_fire_spikes.argtypes = [P, P, i, i, i, i, i, i, P, i, i, i, i, i, d, P, P]
         _lib = L
@@ -317,3 +321,55 @@ def conv_fire_spikes(spikes, offsets, in_shape, w, T, stride, pad, theta):
     lib().or_conv_fire_spikes(_p(spikes), _p(offsets), cap, B, T, Ci, Hi, Wi, _p(w), Co, Kh, Kw,
                               stride, pad, float(theta), _p(tf), _p(vk))
     return tf, vk
+
+
+# ------------------------------------------ steps around the hot path (§IV)
+
+def log_filters(stds, ksize):
+    """The DoG pair that stands for each LoG deviation s (§II-C.3): on-centre
+    (s/sqrt 2, s*sqrt 2), then off-centre (s*sqrt 2, s/sqrt 2), deviations
+    held in float32 as a filter description carries them."""
+    out = []
+    for s in stds:
+        s = float(np.float32(s))
+        a = float(np.float32(s / math.sqrt(2.0)))
+        b = float(np.float32(s * math.sqrt(2.0)))
+        out += [(int(ksize), a, b), (int(ksize), b, a)]
+    return out
+
+
+def log_filter(img, stds, ksize, pad=-1):
+    return dog_filter(img, log_filters(stds, ksize), pad)
+
+
+def threshold(x, thr, value=0.0):
+    x = _c(x, np.float32).copy()
+    lib().or_threshold(_p(x), x.size, float(thr), float(value))
+    return x
+
+
+def quantize(w, lower, mid, upper):
+    w = _c(w, np.float32).copy()
+    lib().or_quantize(_p(w), w.size, float(lower), float(mid), float(upper))
+    return w
+
+
+def gather(times, T):
+    times = _c(times, np.uint8)
+    out = np.empty(times.shape, np.float32)
+    lib().or_gather(_p(times), times.size, int(T), _p(out))
+    return out
+
+
+def lr_factor(samples_seen, a_causal, every=2000, factor=1.5, cap=0.15):
+    """Learning-rate schedule of §IV's example: the rates grow by `factor`
+    after every `every` samples, until the causal rate reaches `cap` (where it
+    stays).  Returns the multiplier of both rates before a batch that starts
+    after `samples_seen` samples."""
+    k = samples_seen // every
+    f = 1.0
+    for _ in range(k):
+        if a_causal * f >= cap:
+            break
+        f = min(f * factor, cap / a_causal)
+    return f

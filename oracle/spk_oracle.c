@@ -644,3 +644,31 @@ void or_conv_fire_spikes(const uint32_t *spikes, const int32_t *offsets, int cap
     free(V);
     free(dV);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Steps around the hot path in the example network of §IV.                 */
+/* ------------------------------------------------------------------------ */
+
+/* Weak filter responses are silenced before coding: x <= threshold -> value. */
+void or_threshold(float *x, int64_t n, float threshold, float value)
+{
+    for (int64_t i = 0; i < n; i++)
+        if (!(x[i] > threshold)) x[i] = value;
+}
+
+/* Trained weights binarized: below mid -> lower, otherwise upper. */
+void or_quantize(float *w, int64_t n, float lower, float mid, float upper)
+{
+    for (int64_t i = 0; i < n; i++) w[i] = w[i] < mid ? lower : upper;
+}
+
+/* A neuron's feature: how many of the T cumulative frames have it on. */
+void or_gather(const uint8_t *times, int64_t n, int T, float *out)
+{
+    for (int64_t i = 0; i < n; i++) {
+        int on = 0;
+        for (int t = 0; t < T; t++)
+            if (times[i] <= t) on++;
+        out[i] = (float)on;
+    }
+}

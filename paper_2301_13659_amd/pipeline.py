@@ -36,6 +36,7 @@ class StepOutputs:
     winners: dict = field(default_factory=dict)      # conv index -> (winners, n_winners)
     winner_cfg: dict = field(default_factory=dict)   # conv index -> winner_cfg (R-STDP)
     pooled: list = field(default_factory=list)
+    features: torch.Tensor | None = None             # gather of the last stage's spikes
 
 
 class Pipeline:
@@ -64,8 +65,32 @@ class Pipeline:
             w16 = w.to(torch.float16) if spec.w_dtype == "f16" else None
             self.layers.append(LayerState(spec, w, w16))
         self.labels = torch.from_numpy(wls.make_labels(wl)).to(self.device) if wl.rstdp_group else None
-        self.cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
+        self.base_cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
+        self.cfgs = list(self.base_cfgs)
         self.filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
+        self.samples_seen = 0   # samples learnt from, for the learning-rate schedule
+
+    def rate_factor(self) -> float:
+        """Multiplier of the STDP rates for the next batch under the workload's
+        schedule (§IV's example): x factor after every `every` samples, until
+        the first configuration's causal rate reaches the cap."""
+        if self.wl.lr_schedule is None:
+            return 1.0
+        every, factor, cap = self.wl.lr_schedule
+        a0 = abs(self.base_cfgs[0][0])
+        f = 1.0
+        for _ in range(self.samples_seen // every):
+            if a0 * f >= cap:
+                break
+            f = min(f * factor, cap / a0)
+        return f
+
+    def quantize(self, lower: float = 0.0, mid: float = 0.5, upper: float = 1.0):
+        """Binarize the weights of the learning layers (§IV's example, after a
+        layer's training)."""
+        for layer in self.layers:
+            if layer.spec.stdp:
+                spk.spk_quantize(layer.w, lower, mid, upper, w_f16=layer.w16)
 
     def snapshot_weights(self):
         return [(l.w.clone(), None if l.w16 is None else l.w16.clone()) for l in self.layers]
@@ -95,8 +120,16 @@ class Pipeline:
             timers.setdefault(name, []).append((a, b))
             return r
 
+        if self.wl.lr_schedule is not None and learn:
+            f = self.rate_factor()
+            self.cfgs = [(a * f, b * f, lo, up, st) for a, b, lo, up, st in self.base_cfgs]
         if self.images is not None:
-            x = timed("dog", lambda: spk.spk_dog_filter(self.images, self.filters))
+            if wl.log_stds:
+                x = timed("dog", lambda: spk.spk_log_filter(self.images, wl.log_stds, wl.log_ksize))
+            else:
+                x = timed("dog", lambda: spk.spk_dog_filter(self.images, self.filters))
+            if wl.pre_threshold is not None:
+                timed("threshold", lambda: spk.spk_threshold(x, wl.pre_threshold, 0.0))
             t = timed("code", lambda: spk.spk_latency_code(x, wl.T, wl.min_value))
             if keep:
                 out.dog, out.times0 = x, t
@@ -107,6 +140,11 @@ class Pipeline:
         li = 0
         pi = 0
         for kind, s in wl.stages:
+            if kind == "gather":
+                feats = timed("gather", lambda: spk.spk_gather(t, wl.T))
+                if keep:
+                    out.features = feats
+                continue
             if kind == "pool":
                 pi += 1
                 t = timed(f"pool{pi}", lambda: spk.spk_pool(t, s.k, s.stride, s.pad))
@@ -145,6 +183,8 @@ class Pipeline:
                         w_f16=layer.w16))
             t = tf
             li += 1
+        if learn:
+            self.samples_seen += wl.batch
         return out
 
 
@@ -164,6 +204,8 @@ def conv_work(wl: wls.Workload, dense: bool = False) -> list:
     C, H, W = wl.input_chw()
     res = []
     for kind, s in wl.stages:
+        if kind == "gather":
+            continue
         if kind == "pool":
             H = (H + 2 * s.pad - s.k) // s.stride + 1
             W = (W + 2 * s.pad - s.k) // s.stride + 1

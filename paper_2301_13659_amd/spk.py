@@ -72,6 +72,10 @@ _SIGNATURES = {
     "spk_fc_winners": ([_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P], _I),
     "spk_fc_stdp_update_workspace_size": ([_I, _I, _I, _I], _Z),
     "spk_fc_stdp_update": ([_P, _P, _I, _I, _P, _I, _P, _P, _I, _P, _I, _P, _P, _Z, _P], _I),
+    "spk_log_filter": ([_P, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P], _I),
+    "spk_threshold": ([_P, _I64, _F, _F, _P], _I),
+    "spk_quantize": ([_P, _P, _I64, _F, _F, _F, _P], _I),
+    "spk_gather": ([_P, _I64, _I, _P, _P], _I),
     "spk_times_to_spikes_workspace_size": ([_I] * 5, _Z),
     "spk_times_to_spikes": ([_P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _Z, _P], _I),
     "spk_spikes_to_times": ([_P, _P, _I, _I, _I, _I, _I, _I, _P, _P], _I),
@@ -450,3 +454,46 @@ def spk_conv_fire_sparse(spikes, offsets, in_shape, w, T: int, stride: int = 1, 
                                   Co, Kh, Kw, stride, pad, float(theta), _ptr(out_times),
                                   _ptr(out_vkey), _ptr(ws), nbytes, _stream(dev)))
     return out_times, out_vkey
+
+
+# ------------------------------------------------ steps around the hot path
+
+def spk_log_filter(img, stds, ksize: int, pad: int = -1):
+    """LoG bank: img uint8 B x C x H x W -> float32 B x (C*2n) x Ho x Wo."""
+    _dev(img, torch.uint8, "img", 4)
+    B, C, H, W = img.shape
+    n = len(stds)
+    Ho = H if pad < 0 else H + 2 * pad - ksize + 1
+    Wo = W if pad < 0 else W + 2 * pad - ksize + 1
+    out = torch.empty((B, C * 2 * n, Ho, Wo), dtype=torch.float32, device=img.device)
+    arr = (ctypes.c_float * n)(*[float(s) for s in stds])
+    _check(load().spk_log_filter(_ptr(img), B, C, H, W, arr, n, ksize, pad, _ptr(out),
+                                 _stream(img.device)))
+    return out
+
+
+def spk_threshold(x, threshold: float, value: float = 0.0):
+    """In place: x = x if x > threshold else value (float32)."""
+    _dev(x, torch.float32, "x")
+    _check(load().spk_threshold(_ptr(x), x.numel(), float(threshold), float(value), _stream(x.device)))
+    return x
+
+
+def spk_quantize(w, lower: float, mid: float, upper: float, w_f16=None):
+    """In place on float32 weights (and their half copy)."""
+    _dev(w, torch.float32, "w")
+    if w_f16 is not None:
+        _dev(w_f16, torch.float16, "w_f16")
+        if w_f16.numel() != w.numel():
+            raise ValueError("w_f16 must match w")
+    _check(load().spk_quantize(_ptr(w), _ptr(w_f16), w.numel(), float(lower), float(mid), float(upper),
+                               _stream(w.device)))
+    return w
+
+
+def spk_gather(times, T: int):
+    """Feature values of a time map: float32, T - t where fired, else 0."""
+    _dev(times, torch.uint8, "times")
+    out = torch.empty(times.shape, dtype=torch.float32, device=times.device)
+    _check(load().spk_gather(_ptr(times), times.numel(), T, _ptr(out), _stream(times.device)))
+    return out

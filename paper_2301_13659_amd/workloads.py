@@ -1,4 +1,4 @@
-"""Seeded synthetic inputs and layer parameters for the five spiking-conv workloads.
+"""Seeded synthetic inputs and layer parameters for the six spiking-conv workloads.
 
 This module only lays out workload parameters and draws random numbers: images,
 spike-time maps, initial weights and labels.  It holds none of the method's
@@ -56,6 +56,8 @@ class ConvSpec:
     radius: int           # inhibition radius (Chebyshev)
     stdp: bool            # this layer learns in the workload's step
     w_dtype: str = "f32"  # "f32" master on the conv, or "f16" operand
+    w_mean: float = 0.8   # initial weights: normal(w_mean, w_std) clipped to [0, 1]
+    w_std: float = 0.05
 
     @property
     def readout(self) -> bool:
@@ -71,7 +73,7 @@ class PoolSpec:
 
 @dataclass(frozen=True)
 class Workload:
-    index: int                       # 1..5
+    index: int                       # 1..6
     name: str
     batch: int
     T: int
@@ -85,6 +87,10 @@ class Workload:
     stdp: tuple = (StdpConfig(0.004, -0.003),)
     rstdp_group: int = 0             # >0: R-STDP with class(o) = o // group
     n_classes: int = 0
+    log_stds: tuple = ()             # LoG bank (two DoGs per deviation) instead of `dog`
+    log_ksize: int = 0
+    pre_threshold: float | None = None  # filter outputs <= this are zeroed before coding
+    lr_schedule: tuple | None = None    # (every samples, factor, cap of the causal rate)
     description: str = ""
 
     def with_batch(self, batch: int) -> "Workload":
@@ -97,7 +103,8 @@ class Workload:
     def input_chw(self) -> tuple:
         if self.spikes_chw is not None:
             return self.spikes_chw
-        return (len(self.dog), self.image_hw[0], self.image_hw[1])
+        nf = 2 * len(self.log_stds) if self.log_stds else len(self.dog)
+        return (nf, self.image_hw[0], self.image_hw[1])
 
 
 def _dog_pair(k: int, s1: float) -> tuple:
@@ -152,6 +159,21 @@ WORKLOADS = {
         stages=(("conv", ConvSpec(128, 64, 3, 1, 1, 20.0, 16, 2, True, "f16")),),
         description="fp16 spiking conv 128x64x3x3 pad 1 on 64ch 64x64 spike frames, batch 128, "
                     "T=30, theta 20, k=16 r=2, STDP"),
+    6: Workload(
+        index=6, name="cfg6-demo-b64", batch=64, T=15, image_hw=(28, 28), image_kind="strokes",
+        log_stds=(0.471, 1.099, 2.042), log_ksize=7, pre_threshold=0.01, min_value=0.0,
+        stages=(
+            ("conv", ConvSpec(100, 6, 5, 1, 2, 16.0, 5, 3, True, w_mean=0.5, w_std=0.02)),
+            ("pool", PoolSpec(2, 2, 0)),
+            ("conv", ConvSpec(200, 100, 3, 1, 1, 5.0, 8, 1, True, w_mean=0.5, w_std=0.02)),
+            ("pool", PoolSpec(3, 3, 0)),
+            ("gather", None),
+        ),
+        stdp=(StdpConfig(0.0004, -0.0003),),
+        lr_schedule=(2000, 1.5, 0.15),
+        description="the paper's example network: LoG bank (3 deviations, 7x7) -> threshold 0.01 -> "
+                    "T=15 -> conv1 100x5x5 theta 16 k5 r3 -> pool 2 -> conv2 200x3x3 theta 5 k8 r1 -> "
+                    "pool 3 -> gather; STDP with the learning-rate schedule, batch 64"),
 }
 
 
@@ -230,7 +252,8 @@ def make_spike_times(wl: Workload, density_index: int) -> np.ndarray:
 def make_weights(wl: Workload, layer: int) -> np.ndarray:
     """float32 Co x Ci x K x K initial weights of conv layer `layer` (1-based).
 
-    f32 layers: normal(0.8, 0.05) clipped to [0, 1].  f16 layers: uniform(0.7, 0.9)
+    f32 layers: normal(w_mean, w_std) clipped to [0, 1] (0.8, 0.05 unless the layer
+    says otherwise).  f16 layers: uniform(0.7, 0.9)
     rounded to half precision and held as float32 (the exact half values).
     """
     spec = wl.convs[layer - 1]
@@ -238,7 +261,7 @@ def make_weights(wl: Workload, layer: int) -> np.ndarray:
     shape = (spec.co, spec.ci, spec.k, spec.k)
     if spec.w_dtype == "f16":
         return rng.uniform(0.7, 0.9, size=shape).astype(np.float16).astype(np.float32)
-    return np.clip(rng.normal(0.8, 0.05, size=shape), 0.0, 1.0).astype(np.float32)
+    return np.clip(rng.normal(spec.w_mean, spec.w_std, size=shape), 0.0, 1.0).astype(np.float32)
 
 
 def make_labels(wl: Workload) -> np.ndarray:

@@ -173,3 +173,18 @@ def test_sparse_validation():
     _err(L.spk_conv_fire_sparse(*bad), spk.SPK_E_UNSUPPORTED, "LDS")
     assert L.spk_conv_fire_sparse_workspace_size(2, 15, 6, 28, 28, 30, 5, 5, 1, 2, F32) > 0
     assert L.spk_conv_fire_sparse_workspace_size(2, 15, 4096, 28, 28, 30, 5, 5, 1, 2, F16) == 0
+
+
+def test_demo_ops_validation():
+    import ctypes
+    L = spk.load()
+    stds = (ctypes.c_float * 5)(0.5, 1.0, 1.5, 2.0, 2.5)
+    _err(L.spk_log_filter(P1, 1, 1, 8, 8, stds, 5, 7, -1, P1, None), spk.SPK_E_SHAPE, "8 filters")
+    bad = (ctypes.c_float * 1)(-1.0)
+    _err(L.spk_log_filter(P1, 1, 1, 8, 8, bad, 1, 7, -1, P1, None), spk.SPK_E_ARG, "positive")
+    _err(L.spk_log_filter(P1, 1, 1, 8, 8, stds, 1, 6, -1, P1, None), spk.SPK_E_ARG, "odd")
+    _err(L.spk_threshold(P1, 10, float("nan"), 0.0, None), spk.SPK_E_ARG, "NaN")
+    _err(L.spk_threshold(None, 10, 0.1, 0.0, None), spk.SPK_E_ARG, "NULL")
+    _err(L.spk_quantize(P1, None, -1, 0.0, 0.5, 1.0, None), spk.SPK_E_ARG, "n=")
+    _err(L.spk_gather(P1, 10, 0, P1, None), spk.SPK_E_SHAPE, "T=")
+    assert L.spk_threshold(None, 0, 0.1, 0.0, None) == spk.SPK_OK

@@ -41,25 +41,34 @@ def _check_conv_sampled(t_in, w, spec, T, g_tf, g_vk, rng, n=300):
             check_potentials(np.array([g_vk[b, o, y, x]]), np.array([vk]), "v_key")
 
 
-def _run_and_check(wl, full_conv: bool, density_index: int = 1):
+def _run_and_check(wl, full_conv: bool, density_index: int = 1, samples_seen: int = 0):
     dev = gpu()
     pipe = Pipeline(wl, dev, density_index=density_index)
+    pipe.samples_seen = samples_seen
     w_before = [np_(l.w16.float() if l.w16 is not None else l.w).copy() for l in pipe.layers]
     master_before = [np_(l.w).copy() for l in pipe.layers]
     out = pipe.step(keep=True)
     torch.cuda.synchronize()
     rng = np.random.default_rng(wl.index)
     filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
+    if wl.log_stds:
+        filters = oracle.log_filters(wl.log_stds, wl.log_ksize)
     if pipe.images is not None:
         img = np_(pipe.images)
         g_dog = np_(out.dog)
-        np.testing.assert_array_equal(g_dog.view(np.uint32),
-                                      oracle.dog_filter(img, filters).view(np.uint32))
+        o_dog = oracle.dog_filter(img, filters)
+        if wl.pre_threshold is not None:
+            o_dog = oracle.threshold(o_dog, wl.pre_threshold, 0.0)
+        np.testing.assert_array_equal(g_dog.view(np.uint32), o_dog.view(np.uint32))
         np.testing.assert_array_equal(np_(out.times0), oracle.latency_code(g_dog, wl.T, wl.min_value))
     excused_total = 0
     pool_i = 0
     li = 0
     for kind, s in wl.stages:
+        if kind == "gather":
+            last = np_(out.pooled[pool_i - 1]) if wl.stages[-2][0] == "pool" else np_(out.layer_out[li - 1][0])
+            np.testing.assert_array_equal(np_(out.features), oracle.gather(last, wl.T))
+            continue
         if kind == "pool":
             src = np_(out.layer_out[li - 1][0])
             np.testing.assert_array_equal(np_(out.pooled[pool_i]), oracle.pool(src, s.k, s.stride, s.pad))
@@ -86,7 +95,8 @@ def _run_and_check(wl, full_conv: bool, density_index: int = 1):
                     wc = np_(out.winner_cfg[li])
                     np.testing.assert_array_equal(
                         wc, oracle.rstdp_select(g_win, g_n, np_(pipe.labels), wl.rstdp_group))
-                cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
+                f = oracle.lr_factor(samples_seen, wl.stdp[0].a_causal, *wl.lr_schedule) if wl.lr_schedule else 1.0
+                cfgs = [(c.a_causal * f, c.a_anticausal * f, c.lower, c.upper, c.stabilize) for c in wl.stdp]
                 ref = oracle.stdp_update(master_before[li], t_in, g_win, g_n, cfgs, s.stride, s.pad,
                                          winner_cfg=wc)
                 got = np_(pipe.layers[li].w)
@@ -104,13 +114,31 @@ def test_workload_step_reduced_batch(cfg, batch):
     assert excused <= 5
 
 
+@pytest.mark.parametrize("samples_seen", [0, 4000, 10 ** 6])
+def test_demo_step_reduced_batch(samples_seen):
+    """The paper's example network: LoG bank, threshold, two learning layers
+    with the learning-rate schedule at three points of training, gather."""
+    wl = workloads.get(6).with_batch(2)
+    _run_and_check(wl, full_conv=True, samples_seen=samples_seen)
+
+
+def test_demo_quantize_after_training():
+    dev = gpu()
+    pipe = Pipeline(workloads.get(6).with_batch(4), dev)
+    pipe.step()
+    before = [np_(l.w).copy() for l in pipe.layers]
+    pipe.quantize()
+    for b, l in zip(before, pipe.layers):
+        np.testing.assert_array_equal(np_(l.w), oracle.quantize(b, 0.0, 0.5, 1.0))
+
+
 @pytest.mark.parametrize("density_index", [0, 1, 2])
 def test_cfg5_step_reduced_batch(density_index):
     wl = workloads.get(5).with_batch(1)
     _run_and_check(wl, full_conv=False, density_index=density_index)
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_workload_step_full_size(cfg):
     wl = workloads.get(cfg)
     _run_and_check(wl, full_conv=(cfg == 1), density_index=1)
