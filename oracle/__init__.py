@@ -61,6 +61,9 @@ def lib():
         L.or_fc_wta.argtypes = [P, P, i, i, i, i, i, i, P, P]
         L.or_times_to_spikes.argtypes = [P, i, i64, i, i, P, P]
         L.or_threshold.argtypes = [P, i64, f, f]
+        L.or_rate_code.argtypes = [P, P, i, i64, i, f, P]
+        L.or_conv_if_rate.argtypes = [P, i, i, i, i, i, P, i, i, i, i, i, d, P, P]
+        L.or_rate_pool.argtypes = [P, P, i, i, i, i, i, i, i, i, i, P, P]
         L.or_quantize.argtypes = [P, i64, f, f, f]
         L.or_gather.argtypes = [P, i64, i, P]
         L.or_spikes_to_times.argtypes = [P, P, i, i64, i, i, P]
@@ -373,3 +376,46 @@ def lr_factor(samples_seen, a_causal, every=2000, factor=1.5, cap=0.15):
             break
         f = min(f * factor, cap / a_causal)
     return f
+
+
+# ------------------------------------------------- rate coding (§II-D.1)
+
+def rate_code(x, u, T, min_value=0.01):
+    """x float B x ... ; u float B x T x ... uniform draws -> frames uint8 B x T x ..."""
+    x = _c(x, np.float32)
+    B = x.shape[0]
+    n = int(np.prod(x.shape[1:]))
+    u = _c(u, np.float32)
+    assert u.shape == (B, T) + x.shape[1:]
+    frames = np.empty(u.shape, np.uint8)
+    lib().or_rate_code(_p(x), _p(u), B, n, T, float(min_value), _p(frames))
+    return frames
+
+
+def conv_if_rate(frames, w, stride, pad, theta):
+    """IF with reset over rate frames B x T x Ci x Hi x Wi -> (frames B x T x Co x Ho x Wo, counts)."""
+    frames = _c(frames, np.uint8)
+    w = _c(w, np.float32)
+    B, T, Ci, Hi, Wi = frames.shape
+    Co, Ci2, Kh, Kw = w.shape
+    assert Ci == Ci2
+    Ho = (Hi + 2 * pad - Kh) // stride + 1
+    Wo = (Wi + 2 * pad - Kw) // stride + 1
+    out = np.empty((B, T, Co, Ho, Wo), np.uint8)
+    cnt = np.empty((B, Co, Ho, Wo), np.int32)
+    lib().or_conv_if_rate(_p(frames), B, T, Ci, Hi, Wi, _p(w), Co, Kh, Kw, stride, pad, float(theta),
+                          _p(out), _p(cnt))
+    return out, cnt
+
+
+def rate_pool(frames, counts, k, stride, pad=0):
+    frames = _c(frames, np.uint8)
+    counts = _c(counts, np.int32)
+    B, T, C, Hi, Wi = frames.shape
+    kh, kw = (k, k) if np.isscalar(k) else k
+    Ho = (Hi + 2 * pad - kh) // stride + 1
+    Wo = (Wi + 2 * pad - kw) // stride + 1
+    out = np.empty((B, T, C, Ho, Wo), np.uint8)
+    oc = np.empty((B, C, Ho, Wo), np.int32)
+    lib().or_rate_pool(_p(frames), _p(counts), B, T, C, Hi, Wi, kh, kw, stride, pad, _p(out), _p(oc))
+    return out, oc

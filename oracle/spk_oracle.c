@@ -672,3 +672,114 @@ void or_gather(const uint8_t *times, int64_t n, int T, float *out)
         out[i] = (float)on;
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Rate coding (§II-D.1) and the rate-coded network (§II-E.3, §III-D).      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Per sample, the firing probability of a value is its ratio to the
+ * sample's largest value (values <= min_value never fire); at each step the
+ * neuron fires when that step's uniform draw u (an input, B x T x n) is below
+ * it.  Frames are B x T x n, one per step, not cumulative.
+ */
+void or_rate_code(const float *x, const float *u, int B, int64_t n, int T, float min_value,
+                  uint8_t *frames)
+{
+    for (int b = 0; b < B; b++) {
+        const float *xb = x + (size_t)b * n;
+        float xmax = 0.0f;
+        int any = 0;
+        for (int64_t i = 0; i < n; i++)
+            if (xb[i] > min_value && (!any || xb[i] > xmax)) {
+                xmax = xb[i];
+                any = 1;
+            }
+        for (int t = 0; t < T; t++)
+            for (int64_t i = 0; i < n; i++) {
+                float p = (any && xb[i] > min_value) ? xb[i] / xmax : 0.0f;
+                size_t at = ((size_t)b * T + t) * n + i;
+                frames[at] = u[at] < p ? 1 : 0;
+            }
+    }
+}
+
+/*
+ * Integrate-and-fire over rate-coded frames: the potential adds each step's
+ * input current (Eq. 2 on that step's frame); when it exceeds theta the
+ * neuron fires at that step and its potential returns to zero.  out_frames
+ * B x T x Co x Ho x Wo, counts B x Co x Ho x Wo (spikes per neuron).
+ */
+void or_conv_if_rate(const uint8_t *frames, int B, int T, int Ci, int Hi, int Wi, const float *w,
+                     int Co, int Kh, int Kw, int stride, int pad, double theta,
+                     uint8_t *out_frames, int32_t *counts)
+{
+    int Ho = (Hi + 2 * pad - Kh) / stride + 1;
+    int Wo = (Wi + 2 * pad - Kw) / stride + 1;
+    for (int b = 0; b < B; b++)
+        for (int o = 0; o < Co; o++)
+            for (int y = 0; y < Ho; y++)
+                for (int x = 0; x < Wo; x++) {
+                    double V = 0.0;
+                    int32_t cnt = 0;
+                    for (int t = 0; t < T; t++) {
+                        const uint8_t *f = frames + ((size_t)b * T + t) * Ci * Hi * Wi;
+                        double I = 0.0;
+                        for (int c = 0; c < Ci; c++)
+                            for (int ky = 0; ky < Kh; ky++)
+                                for (int kx = 0; kx < Kw; kx++) {
+                                    int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
+                                    if (iy < 0 || iy >= Hi || ix < 0 || ix >= Wi) continue;
+                                    if (f[((size_t)c * Hi + iy) * Wi + ix])
+                                        I += (double)w[(((size_t)o * Ci + c) * Kh + ky) * Kw + kx];
+                                }
+                        V += I;
+                        uint8_t s = 0;
+                        if (V > theta) {
+                            s = 1;
+                            V = 0.0;
+                            cnt++;
+                        }
+                        out_frames[(((size_t)b * T + t) * Co + o) * Ho * Wo + (size_t)y * Wo + x] = s;
+                    }
+                    counts[((size_t)(b * Co + o) * Ho + y) * Wo + x] = cnt;
+                }
+}
+
+/*
+ * Rate-based max pooling: each window passes on the spike train of its
+ * neuron with the most spikes (the first in row-major order among equals);
+ * padding holds no neuron, and a window with none gives an empty train.
+ */
+void or_rate_pool(const uint8_t *in_frames, const int32_t *in_counts, int B, int T, int C, int Hi,
+                  int Wi, int Kh, int Kw, int stride, int pad, uint8_t *out_frames,
+                  int32_t *out_counts)
+{
+    int Ho = (Hi + 2 * pad - Kh) / stride + 1;
+    int Wo = (Wi + 2 * pad - Kw) / stride + 1;
+    for (int b = 0; b < B; b++)
+        for (int c = 0; c < C; c++)
+            for (int y = 0; y < Ho; y++)
+                for (int x = 0; x < Wo; x++) {
+                    int by = -1, bx = -1;
+                    int32_t best = -1;
+                    for (int ky = 0; ky < Kh; ky++)
+                        for (int kx = 0; kx < Kw; kx++) {
+                            int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
+                            if (iy < 0 || iy >= Hi || ix < 0 || ix >= Wi) continue;
+                            int32_t v = in_counts[((size_t)(b * C + c) * Hi + iy) * Wi + ix];
+                            if (v > best) {
+                                best = v;
+                                by = iy;
+                                bx = ix;
+                            }
+                        }
+                    out_counts[((size_t)(b * C + c) * Ho + y) * Wo + x] = best < 0 ? 0 : best;
+                    for (int t = 0; t < T; t++) {
+                        uint8_t s = 0;
+                        if (by >= 0)
+                            s = in_frames[(((size_t)b * T + t) * C + c) * Hi * Wi + (size_t)by * Wi + bx];
+                        out_frames[(((size_t)b * T + t) * C + c) * Ho * Wo + (size_t)y * Wo + x] = s;
+                    }
+                }
+}

@@ -277,3 +277,9 @@ def random_times(rng: np.random.Generator, shape, T: int, density: float) -> np.
     t = rng.integers(0, T, size=shape)
     return np.where(fires, t, NEVER).astype(np.uint8)
 
+
+
+def uniform_draws(seed: int, shape) -> np.ndarray:
+    """float32 draws, uniform on [0, 1), for stochastic coding (rate coding
+    takes them as an input)."""
+    return _rng(seed).random(shape, dtype=np.float32)

@@ -1,0 +1,110 @@
+"""Rate coding (§II-D.1), integrate-and-fire over rate-coded frames and
+rate-based pooling (§II-E.3): the oracle pinned on the CPU, then libspk
+against it on the GPU."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from parity import gpu, np_
+from paper_2301_13659_amd.workloads import uniform_draws
+
+
+# ----------------------------------------------------------- oracle pins
+
+def test_oracle_rate_code_rules():
+    rng = np.random.default_rng(0)
+    B, T, n = 3, 400, 50
+    x = rng.uniform(0, 1, size=(B, n)).astype(np.float32)
+    x[:, :5] = 0.0                      # never fire
+    x[:, 5] = 2.0                       # the sample's largest: fires every step
+    u = uniform_draws(1, (B, T, n))
+    f = oracle.rate_code(x, u, T, 0.01)
+    assert f[:, :, :5].sum() == 0
+    assert np.all(f[:, :, 5] == 1)
+    # the empirical rate of every neuron is within 5 sigma of its ratio to the maximum
+    p = x / 2.0
+    p[:, :5] = 0
+    rate = f.mean(axis=1)
+    sd = np.sqrt(np.maximum(p * (1 - p), 1e-12) / T)
+    assert np.all(np.abs(rate - p) <= 5 * sd + 1e-9)
+    # scaling a sample leaves its frames unchanged; a larger value fires
+    # whenever a smaller one does (same draws)
+    np.testing.assert_array_equal(oracle.rate_code(x * 3.0, u, T, 0.03), f)
+    big = x.copy()
+    big[:, 6:] = np.minimum(big[:, 6:] * 1.5, 2.0)
+    fb = oracle.rate_code(big, u, T, 0.01)
+    assert np.all(fb[:, :, 6:] >= f[:, :, 6:])
+
+
+def _if_direct(frames, w, stride, pad, theta):
+    """Currents from scipy's correlation of each frame (float64), then the
+    integrate-and-fire scan with reset in plain Python."""
+    from scipy.signal import correlate
+    B, T, Ci, Hi, Wi = frames.shape
+    Co, _, K, _ = w.shape
+    outs, cnts = [], []
+    for b in range(B):
+        cur = []
+        for t in range(T):
+            fp = np.pad(frames[b, t].astype(np.float64), ((0, 0), (pad, pad), (pad, pad)))
+            I = np.stack([correlate(fp, w[o].astype(np.float64), mode="valid")[0] for o in range(Co)])
+            cur.append(I[:, ::stride, ::stride])
+        cur = np.stack(cur)                      # T x Co x Ho x Wo
+        V = np.zeros(cur.shape[1:])
+        spikes = np.zeros(cur.shape, np.uint8)
+        for t in range(T):
+            V = V + cur[t]
+            fire = V > theta
+            spikes[t] = fire
+            V[fire] = 0.0
+        outs.append(spikes)
+        cnts.append(spikes.sum(axis=0).astype(np.int32))
+    return np.stack(outs), np.stack(cnts)
+
+
+@pytest.mark.parametrize("B,T,Ci,H,W,Co,K,s,p,theta,dens", [(2, 9, 3, 7, 6, 4, 3, 1, 1, 1.5, 0.4),
+                                                             (1, 12, 2, 9, 9, 3, 5, 2, 2, 2.0, 0.3),
+                                                             (2, 5, 4, 5, 5, 2, 1, 1, 0, 0.7, 0.5)])
+def test_oracle_rate_if_matches_correlation_and_scan(B, T, Ci, H, W, Co, K, s, p, theta, dens):
+    rng = np.random.default_rng(Ci * 7 + K)
+    frames = (rng.random((B, T, Ci, H, W)) < dens).astype(np.uint8)
+    w = rng.uniform(0, 1, size=(Co, Ci, K, K)).astype(np.float32)
+    of, oc = oracle.conv_if_rate(frames, w, s, p, theta)
+    df, dc = _if_direct(frames, w, s, p, theta)
+    np.testing.assert_array_equal(of, df)
+    np.testing.assert_array_equal(oc, dc)
+
+
+def test_oracle_rate_if_constant_current():
+    """Every input on at every step: a constant current I, so a neuron fires
+    every floor(theta / I) + 1 steps."""
+    T, Ci, K = 40, 2, 3
+    frames = np.ones((1, T, Ci, 5, 5), np.uint8)
+    w = np.full((1, Ci, K, K), 0.25, np.float32)      # I = 18 * 0.25 = 4.5 inside
+    of, oc = oracle.conv_if_rate(frames, w, 1, 0, 10.0)
+    period = math.floor(10.0 / 4.5) + 1                # 3
+    assert np.all(oc == T // period)
+    assert np.all(of[0, period - 1::period] == 1) and of.sum() == oc.sum()
+
+
+def test_oracle_rate_pool_selects_the_most_active_train():
+    rng = np.random.default_rng(4)
+    B, T, C, H, W = 2, 20, 3, 7, 8
+    frames = (rng.random((B, T, C, H, W)) < rng.random((1, 1, C, H, W))).astype(np.uint8)
+    counts = frames.sum(axis=1).astype(np.int32)
+    for k, s, pad in [(2, 2, 0), (3, 3, 1), (3, 2, 0)]:
+        of, oc = oracle.rate_pool(frames, counts, k, s, pad)
+        Ho, Wo = of.shape[3:]
+        cp = np.pad(counts, ((0, 0), (0, 0), (pad, pad), (pad, pad)), constant_values=-1)
+        for b in range(B):
+            for c in range(C):
+                for y in range(Ho):
+                    for x in range(Wo):
+                        win = cp[b, c, y * s:y * s + k, x * s:x * s + k]
+                        j = int(np.argmax(win))          # first maximum, row-major
+                        iy, ix = y * s + j // k - pad, x * s + j % k - pad
+                        assert oc[b, c, y, x] == win.max()
+                        np.testing.assert_array_equal(of[b, :, c, y, x], frames[b, :, c, iy, ix])
