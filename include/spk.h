@@ -341,6 +341,56 @@ spk_status spk_quantize(float *w, uint16_t *w_f16, int64_t n, float lower, float
 spk_status spk_gather(const uint8_t *times, int64_t n, int T, float *out, spk_stream stream);
 
 /* ---------------------------------------------------------------------- */
+/* Rate coding (§II-D.1) and the rate-coded network (§II-E, §II-E.3).      */
+/* Layers exchange frames B x T x C x H x W (uint8 0/1, one per step, not  */
+/* cumulative) and spike counts B x C x H x W (int32).                     */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * spk_rate_code -- per sample, a value's firing probability is its ratio to
+ * the sample's largest value (values <= min_value never fire, min_value >=
+ * 0); at step t the neuron fires when u[b][t][i] < that probability.
+ *   x      float B x n (device); u float B x T x n uniform draws on [0, 1)
+ *          (device; the caller's random numbers); frames uint8 B x T x n.
+ *   ws     B * 4 bytes (per-sample maxima).
+ */
+spk_status spk_rate_code(const float *x, const float *u, int B, int64_t n, int T, float min_value,
+                         uint8_t *frames, void *ws, size_t ws_bytes, spk_stream stream);
+
+/*
+ * spk_conv_if_rate -- integrate-and-fire over rate-coded frames: each step
+ * adds its current (Eq. 2 on that step's frame) to the potential; above
+ * theta the neuron fires at that step and its potential returns to zero.
+ *   frames      uint8 B x T x Ci x Hi x Wi (device).
+ *   w           Co x Ci x Kh x Kw: float master (two half products) or half.
+ *   out_frames  uint8 B x T x Co x Ho x Wo; counts int32 B x Co x Ho x Wo.
+ *   ws          spk_conv_if_rate_workspace_size(...) bytes (a padded
+ *               channels-last copy of the frames and the weight fragments).
+ * Float weights are accumulated in float: exact where the sums are (integer
+ * or binarized weights, halves summing below 2^13).
+ * Errors: SPK_E_ARG, SPK_E_SHAPE, SPK_E_UNSUPPORTED (dtype; weight slices
+ * beyond LDS), SPK_E_WORKSPACE.
+ */
+size_t spk_conv_if_rate_workspace_size(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw,
+                                       int stride, int pad, spk_dtype w_dtype);
+spk_status spk_conv_if_rate(const uint8_t *frames, int B, int T, int Ci, int Hi, int Wi,
+                            const void *w, spk_dtype w_dtype, int Co, int Kh, int Kw, int stride,
+                            int pad, float theta, uint8_t *out_frames, int32_t *counts, void *ws,
+                            size_t ws_bytes, spk_stream stream);
+
+/*
+ * spk_rate_pool -- rate-based max pooling (§II-E.3, Eq. 3 shapes): each
+ * window passes on the frames of its neuron with the highest count (the
+ * first in row-major window order among equals); padding holds no neuron.
+ */
+spk_status spk_rate_pool(const uint8_t *in_frames, const int32_t *in_counts, int B, int T, int C,
+                         int Hi, int Wi, int Kh, int Kw, int stride, int pad, uint8_t *out_frames,
+                         int32_t *out_counts, spk_stream stream);
+
+/* spk_rate_features -- firing rates as features: out = counts / T (float). */
+spk_status spk_rate_features(const int32_t *counts, int64_t n, int T, float *out, spk_stream stream);
+
+/* ---------------------------------------------------------------------- */
 /* Sparse interface (§II-B): the indices of the spikes instead of full     */
 /* buffers.                                                                */
 /* ---------------------------------------------------------------------- */

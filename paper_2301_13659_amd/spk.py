@@ -72,6 +72,11 @@ _SIGNATURES = {
     "spk_fc_winners": ([_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P], _I),
     "spk_fc_stdp_update_workspace_size": ([_I, _I, _I, _I], _Z),
     "spk_fc_stdp_update": ([_P, _P, _I, _I, _P, _I, _P, _P, _I, _P, _I, _P, _P, _Z, _P], _I),
+    "spk_rate_code": ([_P, _P, _I, _I64, _I, _F, _P, _P, _Z, _P], _I),
+    "spk_conv_if_rate_workspace_size": ([_I] * 11, _Z),
+    "spk_conv_if_rate": ([_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _Z, _P], _I),
+    "spk_rate_pool": ([_P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P], _I),
+    "spk_rate_features": ([_P, _I64, _I, _P, _P], _I),
     "spk_log_filter": ([_P, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P], _I),
     "spk_threshold": ([_P, _I64, _F, _F, _P], _I),
     "spk_quantize": ([_P, _P, _I64, _F, _F, _F, _P], _I),
@@ -496,4 +501,65 @@ def spk_gather(times, T: int):
     _dev(times, torch.uint8, "times")
     out = torch.empty(times.shape, dtype=torch.float32, device=times.device)
     _check(load().spk_gather(_ptr(times), times.numel(), T, _ptr(out), _stream(times.device)))
+    return out
+
+
+# ------------------------------------------------------------ rate coding
+
+def spk_rate_code(x, u, T: int, min_value: float = 0.01):
+    """x float32 B x ... ; u float32 B x T x ... uniform draws -> frames uint8 B x T x ..."""
+    _dev(x, torch.float32, "x")
+    _dev(u, torch.float32, "u")
+    B = x.shape[0]
+    n = x[0].numel()
+    if tuple(u.shape) != (B, T) + tuple(x.shape[1:]):
+        raise ValueError("u must be B x T x (the shape of one sample of x)")
+    frames = torch.empty(u.shape, dtype=torch.uint8, device=x.device)
+    ws = _workspace(4 * B, x.device)
+    _check(load().spk_rate_code(_ptr(x), _ptr(u), B, n, T, float(min_value), _ptr(frames), _ptr(ws),
+                                4 * B, _stream(x.device)))
+    return frames
+
+
+def spk_conv_if_rate(frames, w, stride: int = 1, pad: int = 0, theta: float = 1.0):
+    """IF with reset over frames uint8 B x T x Ci x Hi x Wi -> (frames, counts int32)."""
+    _dev(frames, torch.uint8, "frames", 5)
+    if w.dtype not in (torch.float32, torch.float16):
+        raise ValueError("w: expected float32 or float16")
+    _dev(w, w.dtype, "w", 4)
+    B, T, Ci, Hi, Wi = frames.shape
+    Co, Ci2, Kh, Kw = w.shape
+    if Ci != Ci2:
+        raise ValueError(f"w has {Ci2} input channels, frames have {Ci}")
+    Ho, Wo = out_extent(Hi, Kh, stride, pad), out_extent(Wi, Kw, stride, pad)
+    dev = frames.device
+    out = torch.empty((B, T, Co, Ho, Wo), dtype=torch.uint8, device=dev)
+    counts = torch.empty((B, Co, Ho, Wo), dtype=torch.int32, device=dev)
+    dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
+    L = load()
+    nbytes = L.spk_conv_if_rate_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, dt)
+    ws = _workspace(max(nbytes, 1), dev)
+    _check(L.spk_conv_if_rate(_ptr(frames), B, T, Ci, Hi, Wi, _ptr(w), dt, Co, Kh, Kw, stride, pad,
+                              float(theta), _ptr(out), _ptr(counts), _ptr(ws), nbytes, _stream(dev)))
+    return out, counts
+
+
+def spk_rate_pool(frames, counts, k, stride=None, pad: int = 0):
+    _dev(frames, torch.uint8, "frames", 5)
+    _dev(counts, torch.int32, "counts", 4)
+    B, T, C, Hi, Wi = frames.shape
+    kh, kw = (k, k) if isinstance(k, int) else k
+    stride = kh if stride is None else stride
+    Ho, Wo = out_extent(Hi, kh, stride, pad), out_extent(Wi, kw, stride, pad)
+    out = torch.empty((B, T, C, Ho, Wo), dtype=torch.uint8, device=frames.device)
+    oc = torch.empty((B, C, Ho, Wo), dtype=torch.int32, device=frames.device)
+    _check(load().spk_rate_pool(_ptr(frames), _ptr(counts), B, T, C, Hi, Wi, kh, kw, stride, pad,
+                                _ptr(out), _ptr(oc), _stream(frames.device)))
+    return out, oc
+
+
+def spk_rate_features(counts, T: int):
+    _dev(counts, torch.int32, "counts")
+    out = torch.empty(counts.shape, dtype=torch.float32, device=counts.device)
+    _check(load().spk_rate_features(_ptr(counts), counts.numel(), T, _ptr(out), _stream(counts.device)))
     return out
