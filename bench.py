@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, help="1..6 (default: three-layer net)")
+    ap.add_argument("--workload", type=int, default=2, help="1..7 (default: three-layer net)")
     ap.add_argument("--density", type=int, default=1, help="spike-density index of workload 5")
     ap.add_argument("--sparse", action="store_true",
                     help="spike-input workloads: take the input as a spike list (sparse interface)")
@@ -91,10 +91,21 @@ def hbm_stages(wl, pipe, kept, stage_ms):
             res[name] = {"bytes": int(nbytes), "GB/s": round(gbs, 1),
                          "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
+    rate = wl.coding == "rate"
     if kept.dog is not None:
         put("dog", pipe.images.numel() + kept.dog.numel() * 4)
         put("threshold", kept.dog.numel() * 8)
-        put("code", kept.dog.numel() * 4 + kept.times0.numel())
+        if rate:  # values, then one draw read and one frame byte written per step
+            put("code", kept.dog.numel() * 4 + kept.times0.numel() * 5)
+        else:
+            put("code", kept.dog.numel() * 4 + kept.times0.numel())
+    if rate:
+        for i, (f, c) in enumerate(kept.pooled, start=1):
+            src = kept.layer_out[i - 1]
+            put(f"pool{i}", src[0].numel() + src[1].numel() * 4 + f.numel() + c.numel() * 4)
+        if kept.features is not None:
+            put("gather", kept.features.numel() * 8)
+        return res
     if pipe.spike_list is not None:
         # time map written once, the list and its offsets read once
         nsp = int(pipe.spike_list[1][:, -1].sum().item())
@@ -129,8 +140,14 @@ def hbm_stages(wl, pipe, kept, stage_ms):
 
 def fanout_events(t_in, spec, torch):
     """Synaptic events of a conv layer: every input spike counted once times its fan-out
-    (number of output neurons whose window holds it)."""
+    (number of output neurons whose window holds it).  t_in is a time map
+    B x C x H x W, or rate-coded frames B x T x C x H x W (every spike of every step)."""
     import torch.nn.functional as F
+    if t_in.dim() == 5:
+        fired = t_in.to(torch.float64).sum(dim=(0, 1, 2))
+        t_in = t_in[:, 0]
+    else:
+        fired = (t_in != 255).to(torch.float64).sum(dim=(0, 1))
     B, C, H, W = t_in.shape
     Ho = (H + 2 * spec.pad - spec.k) // spec.stride + 1
     Wo = (W + 2 * spec.pad - spec.k) // spec.stride + 1
@@ -138,8 +155,41 @@ def fanout_events(t_in, spec, torch):
                                torch.ones((1, 1, spec.k, spec.k), device=t_in.device),
                                stride=spec.stride, padding=spec.pad)
     cover = F.pad(cover, (0, W - cover.shape[-1], 0, H - cover.shape[-2]))[0, 0]
-    fired = (t_in != 255).to(torch.float64).sum(dim=(0, 1))
     return float((fired * cover.to(torch.float64)).sum().item()) * spec.co
+
+
+def cpu_baseline_rate(wl, budget_s):
+    """Rate-coded inference through the oracle, sample by sample; samples/s."""
+    import oracle
+    from paper_2301_13659_amd import workloads as wls
+
+    imgs = wls.make_images(wl)
+    draws = wls.make_rate_draws(wl)
+    ws = [wls.make_weights(wl, i + 1) for i in range(len(wl.convs))]
+    filters = oracle.log_filters(wl.log_stds, wl.log_ksize)
+    done = 0
+    t0 = time.perf_counter()
+    while done < wl.batch and time.perf_counter() - t0 < budget_s:
+        b = done
+        x = oracle.dog_filter(imgs[b:b + 1], filters)
+        if wl.pre_threshold is not None:
+            x = oracle.threshold(x, wl.pre_threshold, 0.0)
+        f = oracle.rate_code(x, draws[b:b + 1], wl.T, wl.min_value)
+        c = None
+        li = 0
+        for kind, s in wl.stages:
+            if kind == "gather":
+                continue
+            if kind == "pool":
+                f, c = oracle.rate_pool(f, c, s.k, s.stride, s.pad)
+                continue
+            f, c = oracle.conv_if_rate(f, ws[li], s.stride, s.pad, s.theta)
+            li += 1
+        done += 1
+    el = time.perf_counter() - t0
+    return {"value": done / el, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of the {wl.batch} samples of one batch, whole inference, "
+                      f"{el:.1f} s single-threaded C"}
 
 
 def cpu_baseline(wl, budget_s, sparse=False):
@@ -149,6 +199,9 @@ def cpu_baseline(wl, budget_s, sparse=False):
 
     import oracle
     from paper_2301_13659_amd import workloads as wls
+
+    if wl.coding == "rate":
+        return cpu_baseline_rate(wl, budget_s)
 
     imgs = wls.make_images(wl) if wl.image_hw is not None else None
     spikes = wls.make_spike_times(wl, 1) if wl.image_hw is None else None
@@ -209,11 +262,14 @@ def main():
 
     from paper_2301_13659_amd import spk
     from paper_2301_13659_amd import workloads as wls
-    from paper_2301_13659_amd.pipeline import Pipeline, conv_flops, conv_work
+    from paper_2301_13659_amd.pipeline import Pipeline, RatePipeline, conv_flops, conv_work
 
     dev = torch.device("cuda:0")
     wl = wls.get(args.workload)
-    pipe = Pipeline(wl, dev, density_index=args.density, sparse=args.sparse)
+    if wl.coding == "rate":
+        pipe = RatePipeline(wl, dev)
+    else:
+        pipe = Pipeline(wl, dev, density_index=args.density, sparse=args.sparse)
     work = conv_work(wl)
     flops_dense = conv_flops(wl)
 

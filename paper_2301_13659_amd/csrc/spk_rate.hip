@@ -6,7 +6,8 @@
 // B x T x C x H x W (one byte per neuron and step, the dense interface of
 // §II-A) plus spike counts.  The convolution is an implicit GEMM per step on
 // the matrix cores: a tile is 32 output positions x 32 maps, its 16-tap
-// slices read one step's frame from a padded channels-last copy, and the
+// slices read one step's frame from a padded channels-last copy held as
+// halves, and the
 // accumulator is the potential itself: each step's products add the step's
 // current to it, and after the step the neurons above theta spike and are
 // set back to zero.  The wave walks all T steps of its tile, so the
@@ -25,7 +26,8 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kSlack = 16;  // readable bytes past the end of the packed frames
+constexpr int kSlack = 16;  // readable halves past the end of the packed frames
+constexpr int kBatch = 16;  // slices loaded together
 
 // ------------------------------------------------------------ rate code
 
@@ -105,12 +107,13 @@ RGeom make_rgeom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, i
 
 size_t rate_xp_bytes(const RGeom &g)
 {
-    return spk::align_up((size_t)g.B * g.T * g.Hp * g.rowb + kSlack, 256);
+    return spk::align_up(((size_t)g.B * g.T * g.Hp * g.rowb + kSlack) * sizeof(uint16_t), 256);
 }
 
-// One thread per padded pixel (b, t, yp, xp): its Cp channel bytes, zero in
-// the padding and past Ci.
-__global__ void k_rate_pack(const uint8_t *__restrict__ frames, RGeom g, uint8_t *__restrict__ fp)
+// One thread per padded pixel (b, t, yp, xp): its Cp channels as halves (1.0
+// where the neuron spikes at that step, 0 in the padding and past Ci), so an
+// A fragment is one 16-byte load.
+__global__ void k_rate_pack(const uint8_t *__restrict__ frames, RGeom g, uint16_t *__restrict__ fp)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t npix = (int64_t)g.B * g.T * g.Hp * g.Wp;
@@ -125,16 +128,21 @@ __global__ void k_rate_pack(const uint8_t *__restrict__ frames, RGeom g, uint8_t
     const int iy = yp - g.pad, ix = xp - g.pad;
     const bool in = (unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi;
     const uint8_t *src = frames + (size_t)bt * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi + ix;
-    uint8_t *dst = fp + (size_t)i * g.Cp;
+    uint16_t *dst = fp + (size_t)i * g.Cp;
     for (int c0 = 0; c0 < g.Cp; c0 += 8) {
-        uint64_t v = 0;
+        u4 v;
 #pragma unroll
-        for (int e = 0; e < 8; e++) {
-            const int c = c0 + e;
-            const uint64_t s = (in && c < g.Ci) ? (uint64_t)(src[(size_t)c * g.Hi * g.Wi] != 0) : 0u;
-            v |= s << (8 * e);
+        for (int q = 0; q < 4; q++) {
+            uint32_t w = 0;
+#pragma unroll
+            for (int e = 0; e < 2; e++) {
+                const int c = c0 + 2 * q + e;
+                const bool on = in && c < g.Ci && src[(size_t)c * g.Hi * g.Wi] != 0;
+                w |= (on ? 0x3C00u : 0u) << (16 * e);
+            }
+            v[q] = w;
         }
-        *reinterpret_cast<uint64_t *>(dst + c0) = v;
+        *reinterpret_cast<u4 *>(dst + c0) = v;
     }
 }
 
@@ -170,26 +178,12 @@ __global__ void k_rate_pack_w(const void *__restrict__ wv, RGeom g, h8 *__restri
     bp[i] = f;
 }
 
-// 8 spike bytes (0 or 1) -> 8 halves (0 or 1.0).
-__device__ __forceinline__ h8 spikes_to_halves(uint64_t v)
-{
-    const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-    u4 w;
-    w[0] = __builtin_amdgcn_perm(0u, lo, 0x0c010c00u);
-    w[1] = __builtin_amdgcn_perm(0u, lo, 0x0c030c02u);
-    w[2] = __builtin_amdgcn_perm(0u, hi, 0x0c010c00u);
-    w[3] = __builtin_amdgcn_perm(0u, hi, 0x0c030c02u);
-#pragma unroll
-    for (int q = 0; q < 4; q++) w[q] = (w[q] << 14) - (w[q] << 10);  // x 0x3C00 (half 1.0)
-    return __builtin_bit_cast(h8, w);
-}
-
 // Block: 4 waves = (4 / ntb) position tiles x ntb column tiles, whose B
 // fragments sit in LDS.  A wave walks the T steps of its 32 x 32 tile; two
 // accumulator chains (even and odd slices) keep the matrix cores busy, and
 // are summed into the potential after each step.
 template <int NP>
-__global__ __launch_bounds__(kThreads) void k_rate_conv(const uint8_t *__restrict__ fp,
+__global__ __launch_bounds__(kThreads) void k_rate_conv(const uint16_t *__restrict__ fp,
                                                         const h8 *__restrict__ bp, RGeom g,
                                                         float theta, uint8_t *__restrict__ out,
                                                         int32_t *__restrict__ counts)
@@ -218,8 +212,8 @@ __global__ __launch_bounds__(kThreads) void k_rate_conv(const uint8_t *__restric
     const int b = pc / g.HoWo, rem = pc - b * g.HoWo;
     const int y = rem / g.Wo, x = rem - y * g.Wo;
     const size_t stepb = (size_t)g.Hp * g.rowb;
-    const uint8_t *src0 = fp + (size_t)b * g.T * stepb + (size_t)(y * g.stride) * g.rowb +
-                          (size_t)(x * g.stride) * g.Cp + 8 * h;
+    const uint16_t *src0 = fp + (size_t)b * g.T * stepb + (size_t)(y * g.stride) * g.rowb +
+                           (size_t)(x * g.stride) * g.Cp + 8 * h;
     const h8 *bw = sb + (size_t)ntl * per + lane;
     const int o = 32 * nt + (lane & 31);
     const bool real_o = o < g.Co;
@@ -229,27 +223,28 @@ __global__ __launch_bounds__(kThreads) void k_rate_conv(const uint8_t *__restric
 #pragma unroll
     for (int e = 0; e < 16; e++) cnt[e] = 0;
 
+    // a step's slices are loaded together, so the wave waits once per batch
     for (int t = 0; t < g.T; t++) {
-        const uint8_t *src = src0 + (size_t)t * stepb;
-        int ky = 0, jq = 0;
-        for (int s = 0; s < g.SK; s += 2) {
-            const uint64_t a0 = *reinterpret_cast<const uint64_t *>(src + ky * g.rowb + jq * 16);
-            int ky1 = ky, jq1 = jq + 1;
-            if (jq1 == g.Q16) { jq1 = 0; ky1++; }
-            const bool two = s + 1 < g.SK;
-            const uint64_t a1 = two ? *reinterpret_cast<const uint64_t *>(src + ky1 * g.rowb + jq1 * 16) : 0u;
-            const h8 A0 = spikes_to_halves(a0), A1 = spikes_to_halves(a1);
+        const uint16_t *src = src0 + (size_t)t * stepb;
+        for (int q0 = 0; q0 < g.SK; q0 += kBatch) {
+            h8 A[kBatch];
 #pragma unroll
-            for (int k = 0; k < NP; k++)
-                V = __builtin_amdgcn_mfma_f32_32x32x16_f16(A0, bw[(s * NP + k) * 64], V, 0, 0, 0);
-            if (two) {
-#pragma unroll
-                for (int k = 0; k < NP; k++)
-                    V2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(A1, bw[((s + 1) * NP + k) * 64], V2, 0, 0, 0);
+            for (int q = 0; q < kBatch; q++) {
+                const int qq = q0 + q;
+                const int ky = qq / g.Q16, jq = qq - ky * g.Q16;
+                A[q] = qq < g.SK ? *reinterpret_cast<const h8 *>(src + ky * g.rowb + jq * 16) : h8{};
             }
-            jq = jq1 + 1;
-            ky = ky1;
-            if (jq >= g.Q16) { jq -= g.Q16; ky++; }
+#pragma unroll
+            for (int q = 0; q < kBatch; q++) {
+                const int qq = q0 + q;
+                if (qq < g.SK) {
+#pragma unroll
+                    for (int k = 0; k < NP; k++) {
+                        if (q & 1) V2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(A[q], bw[(qq * NP + k) * 64], V2, 0, 0, 0);
+                        else V = __builtin_amdgcn_mfma_f32_32x32x16_f16(A[q], bw[(qq * NP + k) * 64], V, 0, 0, 0);
+                    }
+                }
+            }
         }
         uint32_t sp[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -422,8 +417,8 @@ extern "C" spk_status spk_conv_if_rate(const uint8_t *frames, int B, int T, int 
     SPK_REQUIRE(ws_bytes >= need, SPK_E_WORKSPACE, "spk_conv_if_rate: workspace %zu < %zu bytes",
                 ws_bytes, need);
     g.vec = (g.HoWo % 4 == 0) && ((uintptr_t)out_frames % 4 == 0);
-    uint8_t *fp = static_cast<uint8_t *>(ws);
-    h8 *bp = reinterpret_cast<h8 *>(fp + xb);
+    uint16_t *fp = static_cast<uint16_t *>(ws);
+    h8 *bp = reinterpret_cast<h8 *>(static_cast<uint8_t *>(ws) + xb);
     hipStream_t s = spk::stream_of(stream);
     const int64_t npix = (int64_t)B * T * g.Hp * g.Wp + kSlack;
     hipLaunchKernelGGL(k_rate_pack, dim3((unsigned)((npix + 255) / 256)), dim3(256), 0, s, frames, g, fp);

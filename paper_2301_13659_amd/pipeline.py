@@ -219,3 +219,74 @@ def conv_work(wl: wls.Workload, dense: bool = False) -> list:
             res.append((one * wl.T, "2*B*T*Ho*Wo*Co*Ci*Kh*Kw"))
         C, H, W = s.co, Ho, Wo
     return res
+
+
+class RatePipeline:
+    """Rate-coded inference of a workload (§II-D.1, §III-D): filter bank and
+    threshold, rate coding with the workload's uniform draws, then per conv
+    layer integrate-and-fire over the frames (reset after a spike), rate
+    pooling between layers, and the firing rates of the last stage as
+    features.  No learning: the weights are a trained network's (binarized)."""
+
+    def __init__(self, wl: wls.Workload, device="cuda"):
+        if wl.coding != "rate":
+            raise ValueError("RatePipeline runs rate-coded workloads")
+        self.wl = wl
+        self.device = torch.device(device)
+        self.images = torch.from_numpy(wls.make_images(wl)).to(self.device)
+        self.draws = torch.from_numpy(wls.make_rate_draws(wl)).to(self.device)
+        self.layers = []
+        for li, spec in enumerate(wl.convs, start=1):
+            w = torch.from_numpy(wls.make_weights(wl, li)).to(self.device)
+            w16 = w.to(torch.float16) if spec.w_dtype == "f16" else None
+            self.layers.append(LayerState(spec, w, w16))
+        self.filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
+
+    def step(self, keep: bool = False, timers: dict | None = None, only: set | None = None):
+        wl = self.wl
+        out = StepOutputs() if keep else None
+
+        def timed(name, fn):
+            if timers is None or (only is not None and name not in only):
+                return fn()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            r = fn()
+            b.record()
+            timers.setdefault(name, []).append((a, b))
+            return r
+
+        if wl.log_stds:
+            x = timed("dog", lambda: spk.spk_log_filter(self.images, wl.log_stds, wl.log_ksize))
+        else:
+            x = timed("dog", lambda: spk.spk_dog_filter(self.images, self.filters))
+        if wl.pre_threshold is not None:
+            timed("threshold", lambda: spk.spk_threshold(x, wl.pre_threshold, 0.0))
+        f = timed("code", lambda: spk.spk_rate_code(x, self.draws, wl.T, wl.min_value))
+        if keep:
+            out.dog, out.times0 = x, f
+        counts = None
+        li = pi = 0
+        for kind, s in wl.stages:
+            if kind == "gather":
+                feats = timed("gather", lambda: spk.spk_rate_features(counts, wl.T))
+                if keep:
+                    out.features = feats
+                continue
+            if kind == "pool":
+                pi += 1
+                f, counts = timed(f"pool{pi}", lambda: spk.spk_rate_pool(f, counts, s.k, s.stride, s.pad))
+                if keep:
+                    out.pooled.append((f, counts))
+                continue
+            layer = self.layers[li]
+            w_op = layer.w16 if layer.w16 is not None else layer.w
+            if keep:
+                out.layer_in.append(f)
+            f, counts = timed(f"conv{li + 1}", lambda: spk.spk_conv_if_rate(f, w_op, s.stride, s.pad,
+                                                                            s.theta))
+            if keep:
+                out.layer_out.append((f, counts))
+            li += 1
+        return out

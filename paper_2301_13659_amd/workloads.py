@@ -1,4 +1,4 @@
-"""Seeded synthetic inputs and layer parameters for the six spiking-conv workloads.
+"""Seeded synthetic inputs and layer parameters for the seven spiking-conv workloads.
 
 This module only lays out workload parameters and draws random numbers: images,
 spike-time maps, initial weights and labels.  It holds none of the method's
@@ -12,7 +12,7 @@ only mimic the shapes, value ranges and sparsity of such inputs.
 
 Seeds: image = 13659 + 100*cfg, weights of layer l (1-based) = 13659 + 100*cfg
 + 10*l, labels = 13659 + 100*cfg + 50, spike-time maps = 13659 + 100*cfg + 60 +
-density index.  Every draw uses numpy's PCG64 generator.
+density index, rate-coding draws = 13659 + 100*cfg + 70.  Every draw uses numpy's PCG64 generator.
 """
 from __future__ import annotations
 
@@ -73,7 +73,7 @@ class PoolSpec:
 
 @dataclass(frozen=True)
 class Workload:
-    index: int                       # 1..6
+    index: int                       # 1..7
     name: str
     batch: int
     T: int
@@ -91,6 +91,8 @@ class Workload:
     log_ksize: int = 0
     pre_threshold: float | None = None  # filter outputs <= this are zeroed before coding
     lr_schedule: tuple | None = None    # (every samples, factor, cap of the causal rate)
+    coding: str = "rank"             # "rank": rank-order (time maps); "rate": rate coding (frames)
+    binarize: float | None = None    # weights w < this -> 0 else 1 (a trained, quantized net)
     description: str = ""
 
     def with_batch(self, batch: int) -> "Workload":
@@ -174,6 +176,20 @@ WORKLOADS = {
         description="the paper's example network: LoG bank (3 deviations, 7x7) -> threshold 0.01 -> "
                     "T=15 -> conv1 100x5x5 theta 16 k5 r3 -> pool 2 -> conv2 200x3x3 theta 5 k8 r1 -> "
                     "pool 3 -> gather; STDP with the learning-rate schedule, batch 64"),
+    7: Workload(
+        index=7, name="cfg7-rate-b64", batch=64, T=300, image_hw=(28, 28), image_kind="strokes",
+        log_stds=(0.471, 1.099, 2.042), log_ksize=7, pre_threshold=0.01, min_value=0.0,
+        coding="rate", binarize=0.5,
+        stages=(
+            ("conv", ConvSpec(25, 6, 5, 1, 2, 16.0, 0, 0, False, "f16", w_mean=0.5, w_std=0.02)),
+            ("pool", PoolSpec(2, 2, 0)),
+            ("conv", ConvSpec(50, 25, 3, 1, 1, 5.0, 0, 0, False, "f16", w_mean=0.5, w_std=0.02)),
+            ("pool", PoolSpec(3, 3, 0)),
+            ("gather", None),
+        ),
+        description="rate-coded inference of the example network with 25 and 50 maps: LoG bank -> "
+                    "threshold 0.01 -> rate code T=300 -> conv1 25x5x5 theta 16 -> rate pool 2 -> "
+                    "conv2 50x3x3 theta 5 -> rate pool 3 -> firing rates; binarized weights, batch 64"),
 }
 
 
@@ -253,12 +269,16 @@ def make_weights(wl: Workload, layer: int) -> np.ndarray:
     """float32 Co x Ci x K x K initial weights of conv layer `layer` (1-based).
 
     f32 layers: normal(w_mean, w_std) clipped to [0, 1] (0.8, 0.05 unless the layer
-    says otherwise).  f16 layers: uniform(0.7, 0.9)
+    says otherwise).  A workload with `binarize` draws those and keeps 0 / 1 (the
+    weights of a trained network after quantization).  f16 layers: uniform(0.7, 0.9)
     rounded to half precision and held as float32 (the exact half values).
     """
     spec = wl.convs[layer - 1]
     rng = _rng(SEED_BASE + 100 * wl.index + 10 * layer)
     shape = (spec.co, spec.ci, spec.k, spec.k)
+    if wl.binarize is not None:
+        w = np.clip(rng.normal(spec.w_mean, spec.w_std, size=shape), 0.0, 1.0)
+        return (w >= wl.binarize).astype(np.float32)
     if spec.w_dtype == "f16":
         return rng.uniform(0.7, 0.9, size=shape).astype(np.float16).astype(np.float32)
     return np.clip(rng.normal(spec.w_mean, spec.w_std, size=shape), 0.0, 1.0).astype(np.float32)
@@ -283,3 +303,8 @@ def uniform_draws(seed: int, shape) -> np.ndarray:
     """float32 draws, uniform on [0, 1), for stochastic coding (rate coding
     takes them as an input)."""
     return _rng(seed).random(shape, dtype=np.float32)
+
+
+def make_rate_draws(wl: Workload) -> np.ndarray:
+    """float32 B x T x C x H x W uniform draws of a rate-coded workload's input."""
+    return uniform_draws(SEED_BASE + 100 * wl.index + 70, (wl.batch, wl.T) + tuple(wl.input_chw()))

@@ -158,3 +158,57 @@ def test_step_is_deterministic():
     np.testing.assert_array_equal(a[0], b[0])
     for x, y in zip(a[1] + a[2] + a[3], b[1] + b[2] + b[3]):
         np.testing.assert_array_equal(x, y)
+
+
+def _rate_chain_check(wl, out, pipe, samples):
+    """Every stage of the rate-coded inference against the oracle, on the
+    given samples (each sample's chain is independent of the others)."""
+    from paper_2301_13659_amd.pipeline import RatePipeline  # noqa: F401
+    filters = oracle.log_filters(wl.log_stds, wl.log_ksize)
+    imgs = np_(pipe.images)
+    draws = np_(pipe.draws)
+    ws = [np_(l.w) for l in pipe.layers]
+    for b in samples:
+        x = oracle.threshold(oracle.dog_filter(imgs[b:b + 1], filters), wl.pre_threshold, 0.0)
+        np.testing.assert_array_equal(np_(out.dog[b:b + 1]).view(np.uint32), x.view(np.uint32))
+        f = oracle.rate_code(x, draws[b:b + 1], wl.T, wl.min_value)
+        np.testing.assert_array_equal(np_(out.times0[b:b + 1]), f)
+        c = None
+        li = pi = 0
+        for kind, s in wl.stages:
+            if kind == "gather":
+                np.testing.assert_array_equal(np_(out.features[b:b + 1]), (c / np.float32(wl.T)).astype(np.float32))
+                continue
+            if kind == "pool":
+                f, c = oracle.rate_pool(f, c, s.k, s.stride, s.pad)
+                gf, gc = out.pooled[pi]
+                np.testing.assert_array_equal(np_(gc[b:b + 1]), c)
+                np.testing.assert_array_equal(np_(gf[b:b + 1]), f)
+                pi += 1
+                continue
+            f, c = oracle.conv_if_rate(f, ws[li], s.stride, s.pad, s.theta)
+            gf, gc = out.layer_out[li]
+            np.testing.assert_array_equal(np_(gc[b:b + 1]), c)
+            np.testing.assert_array_equal(np_(gf[b:b + 1]), f)
+            li += 1
+
+
+def test_rate_inference_reduced_batch():
+    from paper_2301_13659_amd.pipeline import RatePipeline
+    dev = gpu()
+    wl = workloads.get(7).with_batch(2)
+    pipe = RatePipeline(wl, dev)
+    out = pipe.step(keep=True)
+    torch.cuda.synchronize()
+    assert 0 < int(np_(out.layer_out[0][1]).sum())  # the layer is in its firing regime
+    _rate_chain_check(wl, out, pipe, [0, 1])
+
+
+def test_rate_inference_full_size_sampled():
+    from paper_2301_13659_amd.pipeline import RatePipeline
+    dev = gpu()
+    wl = workloads.get(7)
+    pipe = RatePipeline(wl, dev)
+    out = pipe.step(keep=True)
+    torch.cuda.synchronize()
+    _rate_chain_check(wl, out, pipe, [wl.batch - 1])
