@@ -61,12 +61,15 @@ constexpr int kSlackPT = 64;                   // readable bytes past the end of
 constexpr uint32_t kSelLo = 0x04010400u;       // bytes 0,1 -> halves 1024 + b
 constexpr uint32_t kSelHi = 0x04030402u;       // bytes 2,3 -> halves 1024 + b
 
-// LDS: [input as halves (2 * kRange) | fire flag per 16 bytes | staged V x 2 |
-// staged t x 2 | position table x 3]
-constexpr size_t kFlagOff = 2 * (size_t)kRange;
-constexpr size_t kStvOff = kFlagOff + kRange / 16;
+// LDS: [staged V x 2 | staged t x 2 | position table x 3 | fire flag per 16
+// input bytes | input as halves (2 bytes per input byte, sized per launch to
+// the largest group's range, so small images leave room for more blocks)]
+constexpr size_t kStvOff = 0;
 constexpr size_t kSttOff = kStvOff + 2 * 32 * kStageStride * sizeof(float);
 constexpr size_t kTabOff = (kSttOff + 2 * 32 * kStageStride + 15) / 16 * 16;
+constexpr size_t kTabBytes = 3 * kG * 2 * sizeof(int);
+constexpr size_t kFlagOff = kTabOff + kTabBytes;
+constexpr size_t kHalOff = (kFlagOff + kRange / 16 + 15) / 16 * 16;
 
 struct PGeom {
     int B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo;
@@ -79,6 +82,7 @@ struct PGeom {
     int SKp;   // slices of the kernel instance (>= SK; the extra ones are zero)
     int P;     // B * Ho * Wo
     int NT;    // ceil(Co / 32)
+    int hw;    // input words (16 bytes) the LDS halves of a launch hold
     int TP;    // steps per position in a tile: 8, 16 or 32
     int lgTP;
 };
@@ -278,9 +282,11 @@ __device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words,
 #pragma unroll
     for (int i = 0; i < kPf; i++) {
         const int k = (int)threadIdx.x + kThreads * i;
-        size_t w = w0 + (size_t)min(k, nw - 1);
-        w = w < xp_words ? w : xp_words - 1;
-        st.w[i] = k < nw ? reinterpret_cast<const uint4 *>(xp)[w] : make_uint4(0u, 0u, 0u, 0u);
+        if (kThreads * i < nw) {  // words past the range are neither loaded nor stored
+            size_t w = w0 + (size_t)min(k, nw - 1);
+            w = w < xp_words ? w : xp_words - 1;
+            st.w[i] = reinterpret_cast<const uint4 *>(xp)[w];
+        }
     }
     return st;
 }
@@ -289,21 +295,25 @@ __device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words,
 // its 16 times fire within the window (clamped times: any byte below T)?
 // Returns, uniform over the wave, whether under 80% of the wave's words of
 // the range [0, nw) are flagged: a sparse range, worth testing slices in.
-__device__ __forceinline__ bool store_range(const Staged &st, uint8_t *lds, uint32_t never4, int nw)
+__device__ __forceinline__ bool store_range(const Staged &st, uint8_t *hal, uint8_t *flags,
+                                            uint32_t never4, int nw, int hw)
 {
     int flagged = 0, words = 0;
 #pragma unroll
     for (int i = 0; i < kPf; i++) {
         const int k = (int)threadIdx.x + kThreads * i;
+        if (kThreads * i >= nw) break;
         const uint4 v = st.w[i];
         const u4 lo = {__builtin_amdgcn_perm(0x64646464u, v.x, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.x, kSelHi),
                        __builtin_amdgcn_perm(0x64646464u, v.y, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.y, kSelHi)};
         const u4 hi = {__builtin_amdgcn_perm(0x64646464u, v.z, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.z, kSelHi),
                        __builtin_amdgcn_perm(0x64646464u, v.w, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.w, kSelHi)};
-        reinterpret_cast<u4 *>(lds)[2 * k] = lo;
-        reinterpret_cast<u4 *>(lds)[2 * k + 1] = hi;
+        if (k < hw) {
+            reinterpret_cast<u4 *>(hal)[2 * k] = lo;
+            reinterpret_cast<u4 *>(hal)[2 * k + 1] = hi;
+        }
         const bool f = ((v.x ^ never4) | (v.y ^ never4) | (v.z ^ never4) | (v.w ^ never4)) != 0u;
-        lds[kFlagOff + k] = f ? 1 : 0;
+        flags[k] = f ? 1 : 0;
         flagged += __builtin_popcountll(__builtin_amdgcn_ballot_w64(f && k < nw));
         words += __builtin_popcountll(__builtin_amdgcn_ballot_w64(k < nw));
     }
@@ -382,8 +392,9 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
                uint8_t *__restrict__ out_t, float *__restrict__ out_v)
 {
     extern __shared__ __align__(16) uint8_t lds[];
-    uint8_t *hal = lds;
-    const uint8_t *flag = lds + kFlagOff;
+    uint8_t *hal = lds + kHalOff;
+    uint8_t *flags = lds + kFlagOff;
+    const uint8_t *flag = flags;
     auto stv = [&](int i) { return reinterpret_cast<float *>(lds + kStvOff) + i * 32 * kStageStride; };
     auto stt = [&](int i) { return lds + kSttOff + i * 32 * kStageStride; };
     Tab *tabs = reinterpret_cast<Tab *>(lds + kTabOff);
@@ -429,7 +440,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, never4, range_words(a0, a1));
+        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -533,7 +544,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            sparse = store_range(nxt, hal, never4, nxt_words);
+            sparse = store_range(nxt, hal, flags, never4, nxt_words, g.hw);
         }
     }
     __syncthreads();  // the last group is staged
@@ -554,7 +565,8 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
                  float theta, int nranges, uint8_t *__restrict__ out_t, float *__restrict__ out_v)
 {
     extern __shared__ __align__(16) uint8_t lds[];
-    uint8_t *hal = lds;
+    uint8_t *hal = lds + kHalOff;
+    uint8_t *flags = lds + kFlagOff;
     auto stv = [&](int i) { return reinterpret_cast<float *>(lds + kStvOff) + i * 32 * kStageStride; };
     auto stt = [&](int i) { return lds + kSttOff + i * 32 * kStageStride; };
     Tab *tabs = reinterpret_cast<Tab *>(lds + kTabOff);
@@ -582,7 +594,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        (void)store_range(load_range(xp, xp_words, a0, a1), hal, never4, range_words(a0, a1));
+        (void)store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -680,7 +692,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            (void)store_range(nxt, hal, never4, nxt_words);
+            (void)store_range(nxt, hal, flags, never4, nxt_words, g.hw);
         }
     }
     __syncthreads();  // the last group is staged
@@ -787,7 +799,7 @@ int n_ranges(const PGeom &g)
     return nr;
 }
 
-size_t fire_lds() { return kTabOff + 3 * kG * sizeof(Tab); }
+size_t fire_lds(const PGeom &g) { return kHalOff + 32 * (size_t)g.hw; }
 
 }  // namespace
 
@@ -836,6 +848,8 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
     SPK_LAUNCHED("spk_conv_fire");
 
     const int nranges = n_ranges(g);
+    // LDS halves for the largest group's range (the words a group stages)
+    g.hw = (int)((max_rows(g, nranges) * (long long)g.rowb + 64 + 47) / 16);
     const int per_xcd = (nranges + 7) / 8;
     const dim3 grid(8 * g.NT * per_xcd);
     const size_t xw = ((size_t)g.B * g.Hp * g.rowb + kSlackPT) / 16;
@@ -847,7 +861,7 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
     } else {
         launch = kDeep[half_w ? 0 : 1][read_mode(g.Cp)];
     }
-    launch(grid, fire_lds(), s, xp, xw, bp, g, theta, nranges, out_t, out_v);
+    launch(grid, fire_lds(g), s, xp, xw, bp, g, theta, nranges, out_t, out_v);
     return check_launch("spk_conv_fire");
 }
 
