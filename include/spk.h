@@ -425,6 +425,7 @@ spk_status spk_times_to_spikes(const uint8_t *times, int B, int C, int H, int W,
  * spk_spikes_to_times -- the time map of a spike list (sparse -> dense):
  * NEVER everywhere, then t at each stored spike of step t.  Indices
  * >= C*H*W are ignored; an index listed twice in one sample is invalid.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (T range, C*H*W >= 2^31, B > 65535).
  */
 spk_status spk_spikes_to_times(const uint32_t *spikes, const int32_t *offsets, int cap, int B,
                                int C, int H, int W, int T, uint8_t *times, spk_stream stream);
@@ -442,8 +443,9 @@ spk_status spk_spikes_to_times(const uint32_t *spikes, const int32_t *offsets, i
  *          ((ky, kx, c) row-major) within a step.
  *   ws     workspace of spk_conv_fire_sparse_workspace_size(...) bytes (a
  *          padded channels-last time buffer and the weight table).
- * Errors: SPK_E_ARG, SPK_E_SHAPE, SPK_E_UNSUPPORTED (unknown dtype, or a
- * weight table of Kh*Kw*Ci taps x 32 maps that does not fit a block's LDS),
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (T range, empty output, tensors of 2^31
+ * elements, B > 65535), SPK_E_UNSUPPORTED (unknown dtype, or a weight table
+ * of Kh*Kw*Ci taps x 32 maps that does not fit a block's LDS),
  * SPK_E_WORKSPACE.
  */
 size_t spk_conv_fire_sparse_workspace_size(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh,

@@ -769,6 +769,7 @@ extern "C" spk_status spk_spikes_to_times(const uint32_t *spikes, const int32_t 
                 T, SPK_MAX_T);
     const int64_t n = (int64_t)C * H * W;
     SPK_REQUIRE(n < (1ll << 31), SPK_E_SHAPE, "spk_spikes_to_times: C*H*W >= 2^31");
+    SPK_REQUIRE(B <= 65535, SPK_E_SHAPE, "spk_spikes_to_times: B=%d > 65535", B);
     hipStream_t s = spk::stream_of(stream);
     const size_t total = (size_t)B * n;
     hipLaunchKernelGGL(k_fill_u8, dim3((unsigned)std::min<size_t>(4096, (total / 16 + 255) / 256 + 1)),
@@ -820,6 +821,7 @@ extern "C" spk_status spk_conv_fire_sparse(const uint32_t *spikes, const int32_t
                 SPK_E_SHAPE, "spk_conv_fire_sparse: tensor of 2^31 elements or more");
     SPK_REQUIRE((long long)B * (Hi + 2 * pad) * (Wi + 2 * pad) * Ci < (1ll << 40), SPK_E_SHAPE,
                 "spk_conv_fire_sparse: padded input too large");
+    SPK_REQUIRE(B <= 65535, SPK_E_SHAPE, "spk_conv_fire_sparse: B=%d > 65535", B);
     EGeom g;
     int waves;
     size_t lds;

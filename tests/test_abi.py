@@ -188,3 +188,19 @@ def test_demo_ops_validation():
     _err(L.spk_quantize(P1, None, -1, 0.0, 0.5, 1.0, None), spk.SPK_E_ARG, "n=")
     _err(L.spk_gather(P1, 10, 0, P1, None), spk.SPK_E_SHAPE, "T=")
     assert L.spk_threshold(None, 0, 0.1, 0.0, None) == spk.SPK_OK
+
+
+def test_rate_and_batch_limits_validation():
+    L = spk.load()
+    F16 = spk.SPK_F16
+    _err(L.spk_spikes_to_times(P1, P1, 4, 70000, 2, 3, 4, 5, P1, None), spk.SPK_E_SHAPE, "B=")
+    _err(L.spk_rate_code(P1, P1, 2, 10, 5, -0.1, P1, P1, 8, None), spk.SPK_E_ARG, "min_value")
+    _err(L.spk_rate_code(P1, P1, 2, 10, 5, 0.0, P1, P1, 4, None), spk.SPK_E_WORKSPACE, "workspace")
+    _err(L.spk_conv_if_rate(P1, 1, 10, 6, 8, 8, P1, F16, 4, 3, 3, 1, 1, float("inf"), P1, P1, P1,
+                            1 << 30, None), spk.SPK_E_ARG, "finite")
+    _err(L.spk_conv_if_rate(P1, 1, 10, 6, 8, 8, P1, F16, 4, 13, 3, 1, 1, 1.0, P1, P1, P1, 1 << 30, None),
+         spk.SPK_E_SHAPE, "empty")
+    _err(L.spk_conv_if_rate(P1, 1, 10, 6, 8, 8, P1, F16, 4, 3, 3, 1, 1, 1.0, P1, P1, P1, 8, None),
+         spk.SPK_E_WORKSPACE, "workspace")
+    _err(L.spk_rate_pool(P1, P1, 1, 10, 3, 4, 4, 5, 5, 1, 0, P1, P1, None), spk.SPK_E_SHAPE, "empty")
+    assert L.spk_conv_if_rate_workspace_size(2, 300, 6, 28, 28, 25, 5, 5, 1, 2, F16) > 0
