@@ -110,6 +110,109 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
     }
 }
 
+// The same sweep with four consecutive locations per lane (H*W a multiple
+// of 4): each load of a wave brings 256 time bytes and 1 KB of potentials.
+// kG4 waves split the maps (c = g, g + kG4, ...), each in ascending order,
+// and meet in LDS; the result is that of k_pointwise.
+constexpr int kG4 = 8;
+
+__global__ __launch_bounds__(64 * kG4) void k_pointwise4(const uint8_t *times,
+                                                         const float *__restrict__ vkey, int C,
+                                                         int HW, long long total,
+                                                         Rec *__restrict__ recs, uint8_t *inhibited)
+{
+    __shared__ int s_t[kG4][256], s_c[kG4][256];
+    __shared__ float s_v[kG4][256];
+    const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
+    const long long i0 = (long long)blockIdx.x * 256 + 4 * lane;  // b*HW + p, p % 4 == 0
+    const bool ok = i0 < total;
+    const long long b = ok ? i0 / HW : 0, p = i0 - b * HW;
+    const size_t base = (size_t)b * C * HW + p;
+    int bt[4], bc[4];
+    float bv[4];
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        bt[q] = spk::kNever;
+        bc[q] = -1;
+        bv[q] = 0.0f;
+    }
+    if (ok) {
+        auto take = [&](int c, uint32_t t4, float4 v4) {
+            const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                const int t = (t4 >> (8 * q)) & 0xFF;
+                if (t != spk::kNever && (t < bt[q] || (t == bt[q] && vv[q] > bv[q]))) {
+                    bt[q] = t;
+                    bv[q] = vv[q];
+                    bc[q] = c;
+                }
+            }
+        };
+        int c = grp;
+        for (; c + 3 * kG4 < C; c += 4 * kG4) {
+            uint32_t t[4];
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const size_t at = base + (size_t)(c + u * kG4) * HW;
+                t[u] = *reinterpret_cast<const uint32_t *>(times + at);
+                v[u] = *reinterpret_cast<const float4 *>(vkey + at);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u++) take(c + u * kG4, t[u], v[u]);
+        }
+        for (; c < C; c += kG4) {
+            const size_t at = base + (size_t)c * HW;
+            take(c, *reinterpret_cast<const uint32_t *>(times + at), *reinterpret_cast<const float4 *>(vkey + at));
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        s_t[grp][4 * lane + q] = bt[q];
+        s_v[grp][4 * lane + q] = bv[q];
+        s_c[grp][4 * lane + q] = bc[q];
+    }
+    __syncthreads();
+    // 256 locations, one thread each, merge the kG4 partial winners in wave order
+    const int j = threadIdx.x;
+    if (j < 256) {
+        int t0 = s_t[0][j], c0 = s_c[0][j];
+        float v0 = s_v[0][j];
+        for (int g = 1; g < kG4; g++) {
+            const int t = s_t[g][j], c = s_c[g][j];
+            const float v = s_v[g][j];
+            if (c >= 0 && (c0 < 0 || earlier(t, v, c, t0, v0, c0))) {
+                t0 = t;
+                v0 = v;
+                c0 = c;
+            }
+        }
+        s_t[0][j] = t0;
+        s_c[0][j] = c0;
+        const long long i = (long long)blockIdx.x * 256 + j;
+        if (i < total) recs[i] = Rec{((uint32_t)t0 << 24) | (uint32_t)(c0 < 0 ? 0 : c0), v0};
+    }
+    if (inhibited) {
+        __syncthreads();
+        if (ok) {
+            int wt[4], wc[4];
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                wt[q] = s_t[0][4 * lane + q];
+                wc[q] = s_c[0][4 * lane + q];
+            }
+            for (int c = grp; c < C; c += kG4) {
+                uint32_t o = 0;
+#pragma unroll
+                for (int q = 0; q < 4; q++)
+                    o |= (uint32_t)(c == wc[q] ? wt[q] : spk::kNever) << (8 * q);
+                *reinterpret_cast<uint32_t *>(inhibited + base + (size_t)c * HW) = o;
+            }
+        }
+    }
+}
+
 // Wave-wide minima with row shifts and row broadcasts (DPP) instead of LDS
 // permutes.  Lanes without a source keep the identity (all ones); every lane
 // gets the result.
@@ -438,8 +541,14 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     Rec *recs = (Rec *)ws;
     if (pointwise) {
         const long long total = (long long)B * HW;
-        hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 64)), dim3(64 * kGroups), 0, s,
-                           times, vkey, C, HW, total, recs, inhibited);
+        const bool vec = HW % 4 == 0 && (uintptr_t)times % 4 == 0 && (uintptr_t)vkey % 16 == 0 &&
+                         (uintptr_t)inhibited % 4 == 0;
+        if (vec)
+            hipLaunchKernelGGL(k_pointwise4, dim3(spk::ceil_div(total, 256)), dim3(64 * kG4), 0, s,
+                               times, vkey, C, HW, total, recs, inhibited);
+        else
+            hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 64)), dim3(64 * kGroups), 0, s,
+                               times, vkey, C, HW, total, recs, inhibited);
         SPK_LAUNCHED("spk_inhibit_winners");
     } else if (inhibited && inhibited != times) {
         SPK_REQUIRE(hipMemcpyAsync(inhibited, times, (size_t)B * C * HW, hipMemcpyDeviceToDevice,
