@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=2, help="1..7 (default: three-layer net)")
     ap.add_argument("--density", type=int, default=1, help="spike-density index of workload 5")
+    ap.add_argument("--hbm-passes", action="store_true",
+                    help="also time the standalone HBM passes of the first conv layer "
+                         "(inhibition, fire over its dense potentials); on for workload 5")
     ap.add_argument("--sparse", action="store_true",
                     help="spike-input workloads: take the input as a spike list (sparse interface)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -135,6 +138,48 @@ def hbm_stages(wl, pipe, kept, stage_ms):
             put(f"stdp{n}", w.numel() * 8 + wl.batch * s.k_win * (patch + 20))
         t = tf
         li += 1
+    return res
+
+
+def hbm_passes(pipe, kept, torch, spk):
+    """The streaming passes the HBM bar is judged on, on the first conv layer's
+    outputs: pointwise inhibition alone (times + potentials read, inhibited map
+    written) and the fire step over the layer's dense potentials (every step
+    read, times + V_key written).  HIP events around each call, several
+    repetitions, outside the timed steps."""
+    wl = pipe.wl
+    spec = wl.convs[0]
+    t_in = kept.layer_in[0]
+    tf, vk = kept.layer_out[0]
+    layer = pipe.layers[0]
+    w_op = layer.w16 if layer.w16 is not None else layer.w
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(e) / reps
+
+    res = {}
+    out = torch.empty_like(tf)
+    ms = timed(lambda: spk.spk_inhibit(tf, vk, out=out), 10)
+    nbytes = tf.numel() * 6
+    res["inhibit"] = {"bytes": nbytes, "ms": ms, "GB/s": nbytes / (ms * 1e-3) / 1e9,
+                      "frac": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    _, _, V = spk.spk_conv_fire(t_in, w_op, wl.T, spec.stride, spec.pad, spec.theta, potentials=True)
+    ms = timed(lambda: spk.spk_fire(V, spec.theta), 5)
+    nbytes = V.numel() * 4 + tf.numel() * 5
+    res["fire_sweep"] = {"bytes": nbytes, "ms": ms, "GB/s": nbytes / (ms * 1e-3) / 1e9,
+                         "frac": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                         "mode": "standalone fire over the dense-interface potentials"}
+    del V
+    torch.cuda.empty_cache()
     return res
 
 
@@ -334,6 +379,9 @@ def main():
                 "dense_interface_tflops": flops_dense[li] / (c_ms * 1e-3) / 1e12})
 
     hbm = hbm_stages(wl, pipe, kept, stage_ms) if per_layer else {}
+    passes = None
+    if per_layer and wl.coding == "rank" and (args.hbm_passes or wl.index == 5):
+        passes = hbm_passes(pipe, kept, torch, spk)
 
     achieved = work[dom][0] / (dom_ms * 1e-3) / 1e12
     sparse_dom = args.sparse and dom == 0
@@ -359,6 +407,8 @@ def main():
         "per_layer": per_layer, "stage_ms": stage_ms, "hbm_stages": hbm, "roofline": roofline,
         "library": spk.version(),
     }
+    if passes is not None:
+        line["hbm_passes"] = passes
     if args.sparse:
         line["config"]["interface"] = "sparse (spike-list input)"
     if args.cpu_seconds > 0:

@@ -319,6 +319,28 @@ spk_status spk_log_filter(const uint8_t *img, int B, int C, int H, int W, const 
                           int n_std, int ksize, int pad, float *out, spk_stream stream);
 
 /*
+ * spk_inhibit -- pointwise lateral inhibition on its own (§II-F.3, the
+ * paper's inhibit): at each location (b, y, x) only the neuron that fires
+ * earliest (then the higher vkey, then the lower map) keeps its time; all
+ * others become NEVER.  times, vkey B x C x H x W (device); inhibited B x C x
+ * H x W, which may be times itself (in place).  One pass: 6 bytes per neuron.
+ * Errors: SPK_E_ARG, SPK_E_SHAPE (C*H*W >= 2^31).
+ */
+spk_status spk_inhibit(const uint8_t *times, const float *vkey, int B, int C, int H, int W,
+                       uint8_t *inhibited, spk_stream stream);
+
+/*
+ * spk_fire -- the fire step on its own (§II-E, firing rule of §II-D.3): over
+ * dense potentials B x T x n (the dense interface's BTCHW layout, n = C*H*W),
+ * per neuron the first step with V > theta and V there (else NEVER and
+ * V[T-1]).  The same outputs as spk_conv_fire gives with its potentials; a
+ * streaming pass that reads every step.
+ * Errors: SPK_E_ARG (NULL, sizes <= 0, theta NaN), SPK_E_SHAPE (T range).
+ */
+spk_status spk_fire(const float *potentials, int B, int T, int64_t n, float theta,
+                    uint8_t *out_times, float *out_vkey, spk_stream stream);
+
+/*
  * spk_threshold -- in place, x = x if x > threshold else value (n floats,
  * device).  Applied to filter outputs before coding, it silences the weak
  * responses (§IV's example uses 0.01); NaN becomes value.

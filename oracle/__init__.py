@@ -61,6 +61,7 @@ def lib():
         L.or_fc_wta.argtypes = [P, P, i, i, i, i, i, i, P, P]
         L.or_times_to_spikes.argtypes = [P, i, i64, i, i, P, P]
         L.or_threshold.argtypes = [P, i64, f, f]
+        L.or_fire.argtypes = [P, i, i, i64, d, P, P]
         L.or_rate_code.argtypes = [P, P, i, i64, i, f, P]
         L.or_conv_if_rate.argtypes = [P, i, i, i, i, i, P, i, i, i, i, i, d, P, P]
         L.or_rate_pool.argtypes = [P, P, i, i, i, i, i, i, i, i, i, P, P]
@@ -419,3 +420,14 @@ def rate_pool(frames, counts, k, stride, pad=0):
     oc = np.empty((B, C, Ho, Wo), np.int32)
     lib().or_rate_pool(_p(frames), _p(counts), B, T, C, Hi, Wi, kh, kw, stride, pad, _p(out), _p(oc))
     return out, oc
+
+
+def fire(V, theta):
+    """Fire over dense potentials B x T x ... -> (times uint8 B x ..., vkey float32 B x ...)."""
+    V = _c(V, np.float32)
+    B, T = V.shape[:2]
+    n = int(np.prod(V.shape[2:]))
+    tf = np.empty((B,) + V.shape[2:], np.uint8)
+    vk = np.empty((B,) + V.shape[2:], np.float32)
+    lib().or_fire(_p(V), B, T, n, float(np.float32(theta)), _p(tf), _p(vk))
+    return tf, vk

@@ -783,3 +783,20 @@ void or_rate_pool(const uint8_t *in_frames, const int32_t *in_counts, int B, int
                     }
                 }
 }
+
+/* The fire step alone over dense potentials B x T x n (§II-E, §II-D.3): the
+ * rule of or_fire_neuron applied to each neuron's potentials. */
+void or_fire(const float *V, int B, int T, int64_t n, double theta, uint8_t *out_times, float *out_vkey)
+{
+    double *v = (double *)malloc(sizeof(double) * T);
+    for (int b = 0; b < B; b++)
+        for (int64_t i = 0; i < n; i++) {
+            for (int t = 0; t < T; t++) v[t] = (double)V[((size_t)b * T + t) * n + i];
+            uint8_t tf;
+            double vk;
+            or_fire_neuron(v, T, theta, &tf, &vk);
+            out_times[(size_t)b * n + i] = tf;
+            out_vkey[(size_t)b * n + i] = (float)vk;
+        }
+    free(v);
+}

@@ -99,7 +99,7 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
         }
         s_t[0][lane] = bt;
         s_c[0][lane] = bc;
-        if (ok) recs[i] = Rec{((uint32_t)bt << 24) | (uint32_t)(bc < 0 ? 0 : bc), bv};
+        if (ok && recs) recs[i] = Rec{((uint32_t)bt << 24) | (uint32_t)(bc < 0 ? 0 : bc), bv};
     }
     if (inhibited) {
         __syncthreads();
@@ -110,73 +110,92 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
     }
 }
 
-// The same sweep with four consecutive locations per lane (H*W a multiple
-// of 4): each load of a wave brings 256 time bytes and 1 KB of potentials.
-// kG4 waves split the maps (c = g, g + kG4, ...), each in ascending order,
-// and meet in LDS; the result is that of k_pointwise.
+// The same sweep with L consecutive locations per lane (H*W a multiple of
+// L = 4 or 8): each load of a wave brings 64*L time bytes and 256*L bytes of
+// potentials.  kG4 waves split the maps (c = g, g + kG4, ...), each in
+// ascending order, and meet in LDS; the result is that of k_pointwise.
 constexpr int kG4 = 8;
 
-__global__ __launch_bounds__(64 * kG4) void k_pointwise4(const uint8_t *times,
-                                                         const float *__restrict__ vkey, int C,
-                                                         int HW, long long total,
-                                                         Rec *__restrict__ recs, uint8_t *inhibited)
+template <int L> struct TimesVec;
+template <> struct TimesVec<4> { typedef uint32_t type; };
+template <> struct TimesVec<8> { typedef uint2 type; };
+
+template <int L>
+__device__ __forceinline__ uint32_t time_at(const typename TimesVec<L>::type &t, int q)
 {
-    __shared__ int s_t[kG4][256], s_c[kG4][256];
-    __shared__ float s_v[kG4][256];
+    if constexpr (L == 4) return (t >> (8 * q)) & 0xFF;
+    else return ((q < 4 ? t.x : t.y) >> (8 * (q & 3))) & 0xFF;
+}
+
+template <int L>
+__global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
+                                                          const float *__restrict__ vkey, int C,
+                                                          int HW, long long total,
+                                                          Rec *__restrict__ recs, uint8_t *inhibited)
+{
+    typedef typename TimesVec<L>::type TV;
+    constexpr int NL = 64 * L;  // locations of a block
+    __shared__ int s_t[kG4][NL], s_c[kG4][NL];
+    __shared__ float s_v[kG4][NL];
     const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
-    const long long i0 = (long long)blockIdx.x * 256 + 4 * lane;  // b*HW + p, p % 4 == 0
+    const long long i0 = (long long)blockIdx.x * NL + L * lane;  // b*HW + p, p % L == 0
     const bool ok = i0 < total;
     const long long b = ok ? i0 / HW : 0, p = i0 - b * HW;
     const size_t base = (size_t)b * C * HW + p;
-    int bt[4], bc[4];
-    float bv[4];
+    int bt[L], bc[L];
+    float bv[L];
 #pragma unroll
-    for (int q = 0; q < 4; q++) {
+    for (int q = 0; q < L; q++) {
         bt[q] = spk::kNever;
         bc[q] = -1;
         bv[q] = 0.0f;
     }
     if (ok) {
-        auto take = [&](int c, uint32_t t4, float4 v4) {
-            const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+        auto take = [&](int c, const TV &t4, const float4 *v4) {
 #pragma unroll
-            for (int q = 0; q < 4; q++) {
-                const int t = (t4 >> (8 * q)) & 0xFF;
-                if (t != spk::kNever && (t < bt[q] || (t == bt[q] && vv[q] > bv[q]))) {
+            for (int q = 0; q < L; q++) {
+                const int t = (int)time_at<L>(t4, q);
+                const float4 &vq = v4[q >> 2];
+                const float v = (q & 3) == 0 ? vq.x : (q & 3) == 1 ? vq.y : (q & 3) == 2 ? vq.z : vq.w;
+                if (t != spk::kNever && (t < bt[q] || (t == bt[q] && v > bv[q]))) {
                     bt[q] = t;
-                    bv[q] = vv[q];
+                    bv[q] = v;
                     bc[q] = c;
                 }
             }
         };
         int c = grp;
-        for (; c + 3 * kG4 < C; c += 4 * kG4) {
-            uint32_t t[4];
-            float4 v[4];
+        constexpr int kU = 4;  // maps whose loads are in flight together
+        for (; c + (kU - 1) * kG4 < C; c += kU * kG4) {
+            TV t[kU];
+            float4 v[kU][L / 4];
 #pragma unroll
-            for (int u = 0; u < 4; u++) {
+            for (int u = 0; u < kU; u++) {
                 const size_t at = base + (size_t)(c + u * kG4) * HW;
-                t[u] = *reinterpret_cast<const uint32_t *>(times + at);
-                v[u] = *reinterpret_cast<const float4 *>(vkey + at);
+                t[u] = *reinterpret_cast<const TV *>(times + at);
+#pragma unroll
+                for (int r = 0; r < L / 4; r++) v[u][r] = *reinterpret_cast<const float4 *>(vkey + at + 4 * r);
             }
 #pragma unroll
-            for (int u = 0; u < 4; u++) take(c + u * kG4, t[u], v[u]);
+            for (int u = 0; u < kU; u++) take(c + u * kG4, t[u], v[u]);
         }
         for (; c < C; c += kG4) {
             const size_t at = base + (size_t)c * HW;
-            take(c, *reinterpret_cast<const uint32_t *>(times + at), *reinterpret_cast<const float4 *>(vkey + at));
+            float4 v[L / 4];
+#pragma unroll
+            for (int r = 0; r < L / 4; r++) v[r] = *reinterpret_cast<const float4 *>(vkey + at + 4 * r);
+            take(c, *reinterpret_cast<const TV *>(times + at), v);
         }
     }
 #pragma unroll
-    for (int q = 0; q < 4; q++) {
-        s_t[grp][4 * lane + q] = bt[q];
-        s_v[grp][4 * lane + q] = bv[q];
-        s_c[grp][4 * lane + q] = bc[q];
+    for (int q = 0; q < L; q++) {
+        s_t[grp][L * lane + q] = bt[q];
+        s_v[grp][L * lane + q] = bv[q];
+        s_c[grp][L * lane + q] = bc[q];
     }
     __syncthreads();
-    // 256 locations, one thread each, merge the kG4 partial winners in wave order
-    const int j = threadIdx.x;
-    if (j < 256) {
+    // the block's locations, one thread each, merge the kG4 partial winners in wave order
+    for (int j = threadIdx.x; j < NL; j += blockDim.x) {
         int t0 = s_t[0][j], c0 = s_c[0][j];
         float v0 = s_v[0][j];
         for (int g = 1; g < kG4; g++) {
@@ -190,27 +209,46 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise4(const uint8_t *times,
         }
         s_t[0][j] = t0;
         s_c[0][j] = c0;
-        const long long i = (long long)blockIdx.x * 256 + j;
-        if (i < total) recs[i] = Rec{((uint32_t)t0 << 24) | (uint32_t)(c0 < 0 ? 0 : c0), v0};
+        const long long i = (long long)blockIdx.x * NL + j;
+        if (recs && i < total) recs[i] = Rec{((uint32_t)t0 << 24) | (uint32_t)(c0 < 0 ? 0 : c0), v0};
     }
     if (inhibited) {
         __syncthreads();
         if (ok) {
-            int wt[4], wc[4];
+            int wt[L], wc[L];
 #pragma unroll
-            for (int q = 0; q < 4; q++) {
-                wt[q] = s_t[0][4 * lane + q];
-                wc[q] = s_c[0][4 * lane + q];
+            for (int q = 0; q < L; q++) {
+                wt[q] = s_t[0][L * lane + q];
+                wc[q] = s_c[0][L * lane + q];
             }
             for (int c = grp; c < C; c += kG4) {
-                uint32_t o = 0;
+                uint32_t o[2] = {0u, 0u};
 #pragma unroll
-                for (int q = 0; q < 4; q++)
-                    o |= (uint32_t)(c == wc[q] ? wt[q] : spk::kNever) << (8 * q);
-                *reinterpret_cast<uint32_t *>(inhibited + base + (size_t)c * HW) = o;
+                for (int q = 0; q < L; q++)
+                    o[q >> 2] |= (uint32_t)(c == wc[q] ? wt[q] : spk::kNever) << (8 * (q & 3));
+                if constexpr (L == 4)
+                    *reinterpret_cast<uint32_t *>(inhibited + base + (size_t)c * HW) = o[0];
+                else
+                    *reinterpret_cast<uint2 *>(inhibited + base + (size_t)c * HW) = make_uint2(o[0], o[1]);
             }
         }
     }
+}
+
+// Launch of the location sweep: vectorized when H*W and the arrays allow.
+void launch_pointwise(const uint8_t *times, const float *vkey, int C, int HW, long long total, Rec *recs,
+                      uint8_t *inhibited, hipStream_t s)
+{
+    const bool al = (uintptr_t)times % 8 == 0 && (uintptr_t)vkey % 16 == 0 && (uintptr_t)inhibited % 8 == 0;
+    if (al && HW % 8 == 0)
+        hipLaunchKernelGGL(k_pointwise_v<8>, dim3(spk::ceil_div(total, 512)), dim3(64 * kG4), 0, s, times,
+                           vkey, C, HW, total, recs, inhibited);
+    else if (al && HW % 4 == 0)
+        hipLaunchKernelGGL(k_pointwise_v<4>, dim3(spk::ceil_div(total, 256)), dim3(64 * kG4), 0, s, times,
+                           vkey, C, HW, total, recs, inhibited);
+    else
+        hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 64)), dim3(64 * kGroups), 0, s, times,
+                           vkey, C, HW, total, recs, inhibited);
 }
 
 // Wave-wide minima with row shifts and row broadcasts (DPP) instead of LDS
@@ -541,14 +579,7 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     Rec *recs = (Rec *)ws;
     if (pointwise) {
         const long long total = (long long)B * HW;
-        const bool vec = HW % 4 == 0 && (uintptr_t)times % 4 == 0 && (uintptr_t)vkey % 16 == 0 &&
-                         (uintptr_t)inhibited % 4 == 0;
-        if (vec)
-            hipLaunchKernelGGL(k_pointwise4, dim3(spk::ceil_div(total, 256)), dim3(64 * kG4), 0, s,
-                               times, vkey, C, HW, total, recs, inhibited);
-        else
-            hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 64)), dim3(64 * kGroups), 0, s,
-                               times, vkey, C, HW, total, recs, inhibited);
+        launch_pointwise(times, vkey, C, HW, total, recs, inhibited, s);
         SPK_LAUNCHED("spk_inhibit_winners");
     } else if (inhibited && inhibited != times) {
         SPK_REQUIRE(hipMemcpyAsync(inhibited, times, (size_t)B * C * HW, hipMemcpyDeviceToDevice,
@@ -584,5 +615,21 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     hipLaunchKernelGGL(k_select, dim3(B), dim3(k > 0 ? kThreads : 64), lds, s, times, vkey, recs, a,
                        stage, winners, n_winners);
     SPK_LAUNCHED("spk_inhibit_winners");
+    return SPK_OK;
+}
+
+extern "C" spk_status spk_inhibit(const uint8_t *times, const float *vkey, int B, int C, int H, int W,
+                                  uint8_t *inhibited, spk_stream stream)
+{
+    spk::clear_error();
+    SPK_REQUIRE(times && vkey && inhibited, SPK_E_ARG, "spk_inhibit: NULL pointer");
+    SPK_REQUIRE(B > 0 && C > 0 && H > 0 && W > 0, SPK_E_ARG, "spk_inhibit: sizes must be positive");
+    SPK_REQUIRE((long long)C * H * W < (1LL << 31) && (long long)B * H * W < (1LL << 40), SPK_E_SHAPE,
+                "spk_inhibit: C*H*W >= 2^31");
+    const int HW = H * W;
+    const long long total = (long long)B * HW;
+    hipStream_t s = spk::stream_of(stream);
+    launch_pointwise(times, vkey, C, HW, total, nullptr, inhibited, s);
+    SPK_LAUNCHED("spk_inhibit");
     return SPK_OK;
 }

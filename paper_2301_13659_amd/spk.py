@@ -79,6 +79,8 @@ _SIGNATURES = {
     "spk_rate_features": ([_P, _I64, _I, _P, _P], _I),
     "spk_log_filter": ([_P, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P], _I),
     "spk_threshold": ([_P, _I64, _F, _F, _P], _I),
+    "spk_fire": ([_P, _I, _I, _I64, _F, _P, _P, _P], _I),
+    "spk_inhibit": ([_P, _P, _I, _I, _I, _I, _P, _P], _I),
     "spk_quantize": ([_P, _P, _I64, _F, _F, _F, _P], _I),
     "spk_gather": ([_P, _I64, _I, _P, _P], _I),
     "spk_times_to_spikes_workspace_size": ([_I] * 5, _Z),
@@ -562,4 +564,29 @@ def spk_rate_features(counts, T: int):
     _dev(counts, torch.int32, "counts")
     out = torch.empty(counts.shape, dtype=torch.float32, device=counts.device)
     _check(load().spk_rate_features(_ptr(counts), counts.numel(), T, _ptr(out), _stream(counts.device)))
+    return out
+
+
+def spk_fire(potentials, theta: float):
+    """Fire over dense potentials B x T x ... -> (times uint8 B x ..., vkey float32 B x ...)."""
+    _dev(potentials, torch.float32, "potentials")
+    B, T = potentials.shape[:2]
+    n = potentials[0, 0].numel()
+    shape = (B,) + tuple(potentials.shape[2:])
+    out_t = torch.empty(shape, dtype=torch.uint8, device=potentials.device)
+    out_v = torch.empty(shape, dtype=torch.float32, device=potentials.device)
+    _check(load().spk_fire(_ptr(potentials), B, T, n, float(theta), _ptr(out_t), _ptr(out_v),
+                           _stream(potentials.device)))
+    return out_t, out_v
+
+
+def spk_inhibit(times, vkey, out=None):
+    """Pointwise inhibition: a new (or the given, possibly `times` itself) uint8 map."""
+    _dev(times, torch.uint8, "times", 4)
+    _dev(vkey, torch.float32, "vkey", 4)
+    B, C, H, W = times.shape
+    if out is None:
+        out = torch.empty_like(times)
+    _dev(out, torch.uint8, "out", 4)
+    _check(load().spk_inhibit(_ptr(times), _ptr(vkey), B, C, H, W, _ptr(out), _stream(times.device)))
     return out

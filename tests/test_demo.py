@@ -112,3 +112,36 @@ def test_threshold_quantize_gather_bit_exact():
     for T in (1, 15, 254):
         t = random_times(rng, (4, 200, 4, 4), T, 0.5)
         np.testing.assert_array_equal(np_(spk.spk_gather(_t(t, dev), T)), oracle.gather(t, T))
+
+
+# ------------------------------------------------- the fire step on its own
+
+@pytest.mark.parametrize("theta", [2.0, -0.5, math.inf])
+def test_oracle_fire_matches_the_conv_firing(theta):
+    """Fire over the conv's dense potentials gives the conv's own spikes."""
+    rng = np.random.default_rng(9)
+    t = random_times(rng, (2, 4, 9, 8), 10, 0.3)
+    w = rng.uniform(-0.3, 1, size=(5, 4, 3, 3)).astype(np.float32)
+    tf, vk, V = oracle.conv_fire(t, w, 10, 1, 1, theta, potentials=True)
+    f_t, f_v = oracle.fire(V, theta)
+    np.testing.assert_array_equal(f_t, tf)
+    np.testing.assert_allclose(f_v, vk, rtol=1e-6, atol=1e-6)
+
+
+def test_oracle_fire_closed_form():
+    V = np.array([[[0.5], [1.5], [3.0]], [[0.1], [0.2], [0.3]]], np.float32)  # B = 2, T = 3, n = 1
+    tf, vk = oracle.fire(V, 1.0)
+    assert tf.ravel().tolist() == [1, NEVER] and vk.ravel().tolist() == [1.5, np.float32(0.3)]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("B,T,shape,theta", [(3, 15, (30, 28, 28), 6.0), (2, 7, (5, 3, 3), -0.1),
+                                             (2, 30, (16, 8, 8), 20.0), (1, 4, (3,), 1.0)])
+def test_fire_bit_exact(B, T, shape, theta):
+    dev = gpu()
+    rng = np.random.default_rng(T)
+    V = np.cumsum(rng.uniform(-0.5, 2.0, size=(B, T) + shape), axis=1).astype(np.float32)
+    g_t, g_v = spk.spk_fire(_t(V, dev), theta)
+    o_t, o_v = oracle.fire(V, theta)
+    np.testing.assert_array_equal(np_(g_t), o_t)
+    np.testing.assert_array_equal(np_(g_v), o_v)

@@ -247,6 +247,21 @@ def test_inhibit_in_place():
     np.testing.assert_array_equal(np_(tt), oracle.inhibit(times, vkey))
 
 
+@pytest.mark.parametrize("shape", [(2, 9, 6, 7), (3, 128, 8, 8), (2, 30, 28, 28), (1, 5, 3, 5), (2, 7, 2, 6)])
+def test_inhibit_alone_matches_oracle(shape):
+    """spk_inhibit: the vectorized pass (H*W % 4 == 0) and the per-location
+    one, to a new map and in place, with ties in time and potential."""
+    dev = gpu()
+    rng = np.random.default_rng(sum(shape))
+    times = random_times(rng, shape, 6, 0.5)
+    vkey = np.round(rng.uniform(0, 3, size=shape), 1).astype(np.float32)
+    ref = oracle.inhibit(times, vkey)
+    np.testing.assert_array_equal(np_(spk.spk_inhibit(_t(times, dev), _t(vkey, dev))), ref)
+    tt = _t(times, dev)
+    spk.spk_inhibit(tt, _t(vkey, dev), out=tt)
+    np.testing.assert_array_equal(np_(tt), ref)
+
+
 # --------------------------------------------------------------------- STDP
 
 def _winners_dev(win_np, dev):
