@@ -185,21 +185,17 @@ __device__ __forceinline__ uint32_t time_bits(uint2 x)
     return m;
 }
 
-// Copy n 16-byte words from global memory to LDS with the whole block, four
-// loads per thread in flight before their stores.
-__device__ __forceinline__ void copy_to_lds(uint4 *__restrict__ dst, const uint4 *__restrict__ src,
-                                            int n)
+// Copy n 16-byte words from global memory to LDS with the whole block, as
+// direct loads into LDS (no registers): every word of the copy is in flight
+// at once.  The caller's barrier waits for them.
+__device__ __forceinline__ void copy_to_lds(uint8_t *dst, const uint8_t *src, int n)
 {
-    const int step = (int)blockDim.x;
-    int i = threadIdx.x;
-    for (; i + 3 * step < n; i += 4 * step) {
-        const uint4 a = src[i], b = src[i + step], c = src[i + 2 * step], d = src[i + 3 * step];
-        dst[i] = a;
-        dst[i + step] = b;
-        dst[i + 2 * step] = c;
-        dst[i + 3 * step] = d;
-    }
-    for (; i < n; i += step) dst[i] = src[i];
+    typedef __attribute__((address_space(3))) void lds_void;
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = (int)threadIdx.x & 63;
+    for (int w0 = wave * 64; w0 < n; w0 += (int)blockDim.x)
+        if (w0 + lane < n)
+            __builtin_amdgcn_global_load_lds(src + (size_t)(w0 + lane) * 16,
+                                             (lds_void *)(dst + (size_t)w0 * 16), 16, 0, 0);
 }
 
 // ------------------------------------------------------------------ packing
@@ -266,15 +262,15 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
         };
         const bool real = o < g.Co;  // padding maps: zeros
         const int step = (int)blockDim.x;
-        int e = threadIdx.x;
-        for (; e + 3 * step < taps; e += 4 * step) {
-            const float a = wget(e), b = wget(e + step), c = wget(e + 2 * step), d = wget(e + 3 * step);
-            wl[e] = real ? a : 0.0f;
-            wl[e + step] = real ? b : 0.0f;
-            wl[e + 2 * step] = real ? c : 0.0f;
-            wl[e + 3 * step] = real ? d : 0.0f;
+        // 16 loads per thread in flight: a deep map's taps arrive in one or two round trips
+        for (int e0 = threadIdx.x; e0 < taps; e0 += 16 * step) {
+            float v[16];
+#pragma unroll
+            for (int u = 0; u < 16; u++) v[u] = wget(min(e0 + u * step, taps - 1));  // clamped: no branches
+#pragma unroll
+            for (int u = 0; u < 16; u++)
+                if (e0 + u * step < taps) wl[e0 + u * step] = real ? v[u] : 0.0f;
         }
-        for (; e < taps; e += step) wl[e] = real ? wget(e) : 0.0f;
     }
     __syncthreads();
     // this map's lanes: kBig 2 per 16-tap subtile, else 4 per 32-tap subtile
@@ -800,12 +796,14 @@ void k_fire32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g
 // tile (32 maps) and a run of 4*kRoKC subtiles; wave w keeps the B fragments
 // of subtiles w*kRoKC.. in registers.  The block walks row groups of 32
 // positions: it stages the Xp rows that group and its K run touch, each wave
-// accumulates its subtiles, and the four partial tiles are added in LDS in
-// wave order and written to part[split][map][position].  k_readout_sum adds
-// the splits in order.
+// reads all of its A octets and then runs its products back to back, and
+// the four partial tiles are added in LDS in wave order and written to
+// part[split][map][position] with each map's 32 positions in one coalesced
+// store.  k_readout_sum adds the splits in order.
 constexpr int kRoKC = 16;
 constexpr int kRoSteps = kWaves * kRoKC;
-constexpr int kRoRed = kWaves * 1024 * (int)sizeof(float);  // LDS of the partial tiles
+constexpr int kRoStride = 33;                                     // partial tiles: [wave][row][map], padded
+constexpr int kRoRed = kWaves * 32 * kRoStride * (int)sizeof(float);  // LDS of the partial tiles
 
 __host__ __device__ inline void ro_range(const FGeom &g, int p0, int p1, int sp, long long &h0,
                                          long long &h1)
@@ -819,23 +817,43 @@ __host__ __device__ inline void ro_range(const FGeom &g, int p0, int p1, int sp,
     h1 = ((long long)b1 * g.Hp + (long long)y1 * g.stride + ky_hi + 1) * g.rowb;
 }
 
+// Staged range of row group rg: first 16-aligned byte a0 and 16-byte words.
+__device__ __forceinline__ void ro_words(const FGeom &g, int rg, int sp, long long &a0, int &nvec)
+{
+    const int p0 = rg * 32, p1 = min(g.P, p0 + 32) - 1;
+    long long h0, h1;
+    ro_range(g, p0, p1, sp, h0, h1);
+    a0 = h0 & ~15ll;
+    nvec = (int)((h1 - a0 + 15) >> 4) + 1;
+}
+
 template <int NP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g, int iters,
-                 int n_groups, int halo_cap, float *__restrict__ part)
+                 int n_groups, int nx, float *__restrict__ part)
 {
-    // LDS: [partial tiles: wave][element][lane] | halo]
+    // LDS: [partial tiles: wave][position row][map] | halo]
     extern __shared__ __align__(16) uint8_t lds[];
     float *red = reinterpret_cast<float *>(lds);
     uint8_t *halo = lds + kRoRed;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nt = blockIdx.y, sp = blockIdx.z;
+    // Work items j = (split, column tile) major, run of row groups minor.
+    // Blocks go to the 8 XCDs in turn (block L to XCD L % 8); XCD k takes a
+    // contiguous share of the items, so it reads the B fragments of only
+    // about 1/8 of the (split, tile) pairs and they stay in its L2.
+    const int n_items = (int)gridDim.x, xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int per = n_items >> 3, extra = n_items & 7;
+    const int j = xcd * per + min(xcd, extra) + slot;
+    const int bx = j % nx, pair = j / nx;
+    const int nt = pair % g.NT32, sp = pair / g.NT32;
     const int sw0 = sp * kRoSteps + wave * kRoKC;            // this wave's first subtile
     const int nsw = max(0, min(kRoKC, g.S16 - sw0));          // and how many it has
     const int HoWo = g.Ho * g.Wo;
     const int Q8 = g.R8 / 8;
     const int kb0 = sp * kRoSteps * 16;
     const int ky_lo = min(kb0 / g.R8, g.Kh - 1);
+    const int rg0 = bx * iters;
+    const int rg_end = min(n_groups, rg0 + iters);
 
     h8 bw[kRoKC][NP];
 #pragma unroll
@@ -844,24 +862,40 @@ void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeo
 #pragma unroll
         for (int q = 0; q < NP; q++) bw[s][q] = bp[((size_t)(nt * g.S16 + sc) * NP + q) * 64 + lane];
     }
-    const uint32_t cb = 0x6401u + (uint32_t)(g.T - 1);  // half 1025 + (T - 1)
-    const h2 cc = as_h2(cb | (cb << 16));
+    // Per subtile: the comparison constant (half 1025 + (T - 1), or 0 for the
+    // subtiles past the wave's share, whose A fragments are then all zero and
+    // whose products add nothing: every wave runs the same straight-line code)
+    // and the octet's offset from a position's window origin, the same for
+    // every row group.  Octets past K read a row of the halo (their weights
+    // are zero).
+    const uint32_t cb = 0x6401u + (uint32_t)(g.T - 1);
+    const h2 cc = as_h2(cb | (cb << 16)), c0 = as_h2(0u);
+    int offs[kRoKC];
+    {
+        const int q0 = 2 * sw0 + (lane >> 5);
+        int ky = q0 / Q8, jq = q0 - ky * Q8;
+#pragma unroll
+        for (int s = 0; s < kRoKC; s++) {
+            offs[s] = ky < g.Kh ? ky * g.rowb + jq * 8 : ky_lo * g.rowb;
+            jq += 2;
+            while (jq >= Q8) {
+                jq -= Q8;
+                ky++;
+            }
+        }
+    }
 
-    for (int it = 0; it < iters; it++) {
-        const int rg = blockIdx.x * iters + it;
-        if (rg >= n_groups) break;
-        const int p0 = rg * 32, p1 = min(g.P, p0 + 32) - 1;
-        long long h0, h1;
-        ro_range(g, p0, p1, sp, h0, h1);
-        const long long a0 = h0 & ~15ll;
-        const int nvec = (int)((h1 - a0 + 15) >> 4) + 1;
+    for (int rg = rg0; rg < rg_end; rg++) {
+        const int p0 = rg * 32;
+        long long a0;
+        int nvec;
+        ro_words(g, rg, sp, a0, nvec);
         __syncthreads();  // the previous group's halo and partial tiles are no longer read
-        copy_to_lds(reinterpret_cast<uint4 *>(halo), reinterpret_cast<const uint4 *>(xp + a0), nvec);
+        copy_to_lds(halo, xp + a0, nvec);
         __syncthreads();
 
-        f16v acc;
-#pragma unroll
-        for (int e = 0; e < 16; e++) acc[e] = 0.0f;
+        // all of the wave's octets are read before the products start
+        uint2 ab[kRoKC];
         {
             const int p = p0 + (lane & 31);
             const int pc = min(p, g.P - 1);
@@ -869,33 +903,31 @@ void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeo
             const int y = rem / g.Wo, x = rem - y * g.Wo;
             const int base = (int)(((long long)b * g.Hp + (long long)y * g.stride) * g.rowb +
                                    (long long)x * g.stride * g.Ci - a0);
-            const int q0 = 2 * sw0 + (lane >> 5);
-            int ky = q0 / Q8, jq = q0 - ky * Q8;
 #pragma unroll
-            for (int s = 0; s < kRoKC; s++) {
-                if (s < nsw) {
-                    // octets past K read a row of the halo (their weights are zero)
-                    const int off = ky < g.Kh ? ky * g.rowb + jq * 8 : ky_lo * g.rowb;
-                    const h8 a = frag_upto(lds_read8(halo, base + off), cc);
-#pragma unroll
-                    for (int q = 0; q < NP; q++)
-                        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bw[s][q], acc, 0, 0, 0);
-                }
-                jq += 2;
-                while (jq >= Q8) {
-                    jq -= Q8;
-                    ky++;
-                }
-            }
+            for (int s = 0; s < kRoKC; s++) ab[s] = lds_read8(halo, base + offs[s]);
         }
+        f16v acc;
 #pragma unroll
-        for (int e = 0; e < 16; e++) red[(wave * 16 + e) * 64 + lane] = acc[e];
-        __syncthreads();
+        for (int e = 0; e < 16; e++) acc[e] = 0.0f;
+#pragma unroll
+        for (int s = 0; s < kRoKC; s++) {
+            const h8 a = frag_upto(ab[s], s < nsw ? cc : c0);
+#pragma unroll
+            for (int q = 0; q < NP; q++)
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bw[s][q], acc, 0, 0, 0);
+        }
         // element (e, l): position row 8*(e/4) + 4*(l/32) + e%4, map l % 32
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int r = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            red[(wave * 32 + r) * kRoStride + (lane & 31)] = acc[e];
+        }
+        __syncthreads();
         for (int i = threadIdx.x; i < 1024; i += kThreads) {
-            const int e = i >> 6, l = i & 63;
-            const float v = ((red[i] + red[1024 + i]) + red[2048 + i]) + red[3072 + i];
-            const int p = p0 + 8 * (e >> 2) + 4 * (l >> 5) + (e & 3), o = nt * 32 + (l & 31);
+            const int o_l = i >> 5, r = i & 31;
+            const int at = r * kRoStride + o_l, wst = 32 * kRoStride;
+            const float v = ((red[at] + red[wst + at]) + red[2 * wst + at]) + red[3 * wst + at];
+            const int p = p0 + r, o = nt * 32 + o_l;
             if (p < g.P && o < g.Co) part[((size_t)sp * g.Co + o) * g.P + p] = v;
         }
     }
@@ -1135,19 +1167,20 @@ spk_status readout_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
     int iters = (int)std::max<long long>(1, spk::ceil_div((long long)n_groups * g.NT32 * splits, 512));
     iters = std::min(iters, n_groups);
     const size_t lds = ro_halo(g) + kRoRed;
-    dim3 grid(spk::ceil_div(n_groups, iters), g.NT32, splits);
+    const int nx = spk::ceil_div(n_groups, iters);
+    const dim3 grid(nx * g.NT32 * splits);
     if (half_w) {
         if (lds > 64 * 1024)
             (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_readout32<1>),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k_readout32<1>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups,
-                           (int)ro_halo(g), part);
+        hipLaunchKernelGGL(k_readout32<1>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups, nx,
+                           part);
     } else {
         if (lds > 64 * 1024)
             (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_readout32<2>),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k_readout32<2>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups,
-                           (int)ro_halo(g), part);
+        hipLaunchKernelGGL(k_readout32<2>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups, nx,
+                           part);
     }
     SPK_LAUNCHED("spk_conv_fire");
     const long long n = (long long)g.Co * g.P;

@@ -112,9 +112,13 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
 
 // The same sweep with L consecutive locations per lane (H*W a multiple of
 // L = 4 or 8): each load of a wave brings 64*L time bytes and 256*L bytes of
-// potentials.  kG4 waves split the maps (c = g, g + kG4, ...), each in
-// ascending order, and meet in LDS; the result is that of k_pointwise.
+// potentials.  Block (x, y) takes the maps [y*c_per, (y+1)*c_per); its kG4
+// waves split them (c = g, g + kG4, ...), with kU maps' loads in flight at a
+// time, and meet in LDS.  One split (gridDim.y == 1, part == nullptr) gives
+// the result of k_pointwise; with several, each block writes its winner per
+// location to part[y][location] and k_pw_merge finishes.
 constexpr int kG4 = 8;
+constexpr int kU = 4;  // maps whose loads are in flight together
 
 template <int L> struct TimesVec;
 template <> struct TimesVec<4> { typedef uint32_t type; };
@@ -130,7 +134,8 @@ __device__ __forceinline__ uint32_t time_at(const typename TimesVec<L>::type &t,
 template <int L>
 __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
                                                           const float *__restrict__ vkey, int C,
-                                                          int HW, long long total,
+                                                          int HW, long long total, int c_per,
+                                                          Rec *__restrict__ part,
                                                           Rec *__restrict__ recs, uint8_t *inhibited)
 {
     typedef typename TimesVec<L>::type TV;
@@ -164,27 +169,22 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
                 }
             }
         };
-        int c = grp;
-        constexpr int kU = 4;  // maps whose loads are in flight together
-        for (; c + (kU - 1) * kG4 < C; c += kU * kG4) {
+        const int c_lo = (int)blockIdx.y * c_per, c_hi = min(C, c_lo + c_per);
+        // a batch past c_hi loads map c_hi - 1 again (no branch around a load)
+        // and skips it
+        for (int c = c_lo + grp; c < c_hi; c += kU * kG4) {
             TV t[kU];
             float4 v[kU][L / 4];
 #pragma unroll
             for (int u = 0; u < kU; u++) {
-                const size_t at = base + (size_t)(c + u * kG4) * HW;
+                const size_t at = base + (size_t)min(c + u * kG4, c_hi - 1) * HW;
                 t[u] = *reinterpret_cast<const TV *>(times + at);
 #pragma unroll
                 for (int r = 0; r < L / 4; r++) v[u][r] = *reinterpret_cast<const float4 *>(vkey + at + 4 * r);
             }
 #pragma unroll
-            for (int u = 0; u < kU; u++) take(c + u * kG4, t[u], v[u]);
-        }
-        for (; c < C; c += kG4) {
-            const size_t at = base + (size_t)c * HW;
-            float4 v[L / 4];
-#pragma unroll
-            for (int r = 0; r < L / 4; r++) v[r] = *reinterpret_cast<const float4 *>(vkey + at + 4 * r);
-            take(c, *reinterpret_cast<const TV *>(times + at), v);
+            for (int u = 0; u < kU; u++)
+                if (c + u * kG4 < c_hi) take(c + u * kG4, t[u], v[u]);
         }
     }
 #pragma unroll
@@ -210,9 +210,14 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
         s_t[0][j] = t0;
         s_c[0][j] = c0;
         const long long i = (long long)blockIdx.x * NL + j;
-        if (recs && i < total) recs[i] = Rec{((uint32_t)t0 << 24) | (uint32_t)(c0 < 0 ? 0 : c0), v0};
+        const Rec r{((uint32_t)(c0 < 0 ? (int)spk::kNever : t0) << 24) | (uint32_t)(c0 < 0 ? 0 : c0), v0};
+        if (part) {
+            if (i < total) part[(size_t)blockIdx.y * total + i] = r;
+        } else if (recs && i < total) {
+            recs[i] = r;
+        }
     }
-    if (inhibited) {
+    if (inhibited && !part) {
         __syncthreads();
         if (ok) {
             int wt[L], wc[L];
@@ -235,20 +240,136 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
     }
 }
 
-// Launch of the location sweep: vectorized when H*W and the arrays allow.
+// Winners of the map splits, merged per location as a minimum of keys that
+// order records as `earlier` does (a total order on distinct maps, so the
+// order of the splits does not matter), four locations per thread (H*W a
+// multiple of 4).  Block (x, y) writes the inhibited time bytes of maps
+// [y*c_chunk, (y+1)*c_chunk); blocks with y == 0 also write the records.
+__global__ __launch_bounds__(kThreads) void k_pw_merge(const Rec *__restrict__ part, int S,
+                                                       long long total, int C, int HW, int c_chunk,
+                                                       Rec *__restrict__ recs, uint8_t *inhibited)
+{
+    const long long i0 = ((long long)blockIdx.x * kThreads + threadIdx.x) * 4;
+    if (i0 >= total) return;
+    // A record as one 64-bit key, smaller = earlier: time, then the potential
+    // in descending order, then the map; a split without a survivor gives
+    // the largest key.  The merge is a minimum, with no branches.
+    uint64_t best[4];
+    float bv[4];
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        best[q] = ~0ull;
+        bv[q] = 0.0f;
+    }
+    // eight splits' loads in flight at a time; a batch past S repeats split
+    // S - 1, which leaves a minimum unchanged
+    for (int y0 = 0; y0 < S; y0 += 8) {
+        uint4 w[8][2];
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+            const uint4 *pp = reinterpret_cast<const uint4 *>(part + (size_t)min(y0 + u, S - 1) * total + i0);
+            w[u][0] = pp[0];
+            w[u][1] = pp[1];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+            const uint4 a = w[u][0], b = w[u][1];
+            const uint32_t tc[4] = {a.x, a.z, b.x, b.z}, vb[4] = {a.y, a.w, b.y, b.w};
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                const uint32_t t = tc[q] >> 24;
+                const uint64_t key = t == (uint32_t)spk::kNever
+                                         ? ~0ull
+                                         : ((uint64_t)t << 56) |
+                                               ((uint64_t)order_desc(__uint_as_float(vb[q])) << 24) |
+                                               (uint64_t)(tc[q] & 0xFFFFFFu);
+                const bool better = key < best[q];
+                best[q] = better ? key : best[q];
+                bv[q] = better ? __uint_as_float(vb[q]) : bv[q];
+            }
+        }
+    }
+    int t0[4], c0[4];
+    float v0[4];
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        const bool any = best[q] != ~0ull;
+        t0[q] = any ? (int)(best[q] >> 56) : (int)spk::kNever;
+        c0[q] = any ? (int)(best[q] & 0xFFFFFFu) : -1;
+        v0[q] = any ? bv[q] : 0.0f;
+    }
+    if (blockIdx.y == 0 && recs) {
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            recs[i0 + q] = Rec{((uint32_t)t0[q] << 24) | (uint32_t)(c0[q] < 0 ? 0 : c0[q]), v0[q]};
+    }
+    if (inhibited) {
+        const long long b = i0 / HW, p = i0 - b * HW;
+        const int c_lo = (int)blockIdx.y * c_chunk, c_hi = min(C, c_lo + c_chunk);
+        for (int c = c_lo; c < c_hi; c++) {
+            uint32_t o = 0u;
+#pragma unroll
+            for (int q = 0; q < 4; q++) o |= (uint32_t)(c == c0[q] ? t0[q] : (int)spk::kNever) << (8 * q);
+            *reinterpret_cast<uint32_t *>(inhibited + ((size_t)b * C + c) * HW + p) = o;
+        }
+    }
+}
+
+// How a location sweep is laid out: L locations per lane (0: the scalar
+// kernel), X location blocks and S map splits of c_per maps each.  A wave
+// issues the loads of kU maps together, so a block whose waves have several
+// such batches waits several memory latencies: when there are fewer than
+// 1024 location blocks, the maps are split so that each wave has one batch.
+struct PwPlan {
+    int L;
+    long long X;
+    int S, c_per;
+};
+
+PwPlan pw_plan(long long total, int C, int HW, bool aligned, bool may_split)
+{
+    PwPlan pl{0, spk::ceil_div(total, 64), 1, C};
+    if (!aligned || HW % 4 != 0) return pl;
+    pl.L = HW % 8 == 0 ? 8 : 4;
+    pl.X = spk::ceil_div(total, 64 * pl.L);
+    if (may_split && pl.X < 1024 && C > kG4 * kU) {
+        pl.c_per = kG4 * kU;
+        pl.S = spk::ceil_div(C, pl.c_per);
+    }
+    return pl;
+}
+
+size_t pw_part_bytes(long long total, int C, int HW)
+{
+    const PwPlan pl = pw_plan(total, C, HW, true, true);
+    return pl.S > 1 ? spk::align_up((size_t)pl.S * total * sizeof(Rec), 256) : 0;
+}
+
+// Launch of the location sweep: vectorized when H*W and the arrays allow,
+// split over the maps when a workspace for the partial winners is given.
 void launch_pointwise(const uint8_t *times, const float *vkey, int C, int HW, long long total, Rec *recs,
-                      uint8_t *inhibited, hipStream_t s)
+                      uint8_t *inhibited, Rec *part, hipStream_t s)
 {
     const bool al = (uintptr_t)times % 8 == 0 && (uintptr_t)vkey % 16 == 0 && (uintptr_t)inhibited % 8 == 0;
-    if (al && HW % 8 == 0)
-        hipLaunchKernelGGL(k_pointwise_v<8>, dim3(spk::ceil_div(total, 512)), dim3(64 * kG4), 0, s, times,
-                           vkey, C, HW, total, recs, inhibited);
-    else if (al && HW % 4 == 0)
-        hipLaunchKernelGGL(k_pointwise_v<4>, dim3(spk::ceil_div(total, 256)), dim3(64 * kG4), 0, s, times,
-                           vkey, C, HW, total, recs, inhibited);
+    const PwPlan pl = pw_plan(total, C, HW, al, part != nullptr);
+    Rec *pp = pl.S > 1 ? part : nullptr;
+    const dim3 grid((unsigned)pl.X, pl.S);
+    if (pl.L == 8)
+        hipLaunchKernelGGL(k_pointwise_v<8>, grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total, pl.c_per,
+                           pp, recs, inhibited);
+    else if (pl.L == 4)
+        hipLaunchKernelGGL(k_pointwise_v<4>, grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total, pl.c_per,
+                           pp, recs, inhibited);
     else
-        hipLaunchKernelGGL(k_pointwise, dim3(spk::ceil_div(total, 64)), dim3(64 * kGroups), 0, s, times,
-                           vkey, C, HW, total, recs, inhibited);
+        hipLaunchKernelGGL(k_pointwise, dim3((unsigned)pl.X), dim3(64 * kGroups), 0, s, times, vkey, C, HW,
+                           total, recs, inhibited);
+    if (pp) {
+        const long long xm = spk::ceil_div(total, 4 * kThreads);
+        const int chunks = (int)std::min<long long>(C, spk::ceil_div(1024, xm));
+        const int c_chunk = (int)spk::ceil_div(C, chunks);
+        hipLaunchKernelGGL(k_pw_merge, dim3((unsigned)xm, (unsigned)spk::ceil_div(C, c_chunk)), dim3(kThreads),
+                           0, s, pp, pl.S, total, C, HW, c_chunk, recs, inhibited);
+    }
 }
 
 // Wave-wide minima with row shifts and row broadcasts (DPP) instead of LDS
@@ -546,9 +667,9 @@ void launch_select_reg(int B, hipStream_t s, const uint8_t *times, const float *
 
 extern "C" size_t spk_inhibit_winners_workspace_size(int B, int C, int H, int W)
 {
-    (void)C;
-    if (B <= 0 || H <= 0 || W <= 0) return 0;
-    return spk::align_up((size_t)B * H * W * sizeof(Rec), 256);
+    if (B <= 0 || C <= 0 || H <= 0 || W <= 0) return 0;
+    const long long total = (long long)B * H * W;
+    return spk::align_up((size_t)total * sizeof(Rec), 256) + pw_part_bytes(total, C, H * W);
 }
 
 extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vkey, int B, int C,
@@ -579,7 +700,9 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     Rec *recs = (Rec *)ws;
     if (pointwise) {
         const long long total = (long long)B * HW;
-        launch_pointwise(times, vkey, C, HW, total, recs, inhibited, s);
+        Rec *part = reinterpret_cast<Rec *>(reinterpret_cast<char *>(ws) +
+                                            spk::align_up((size_t)total * sizeof(Rec), 256));
+        launch_pointwise(times, vkey, C, HW, total, recs, inhibited, part, s);
         SPK_LAUNCHED("spk_inhibit_winners");
     } else if (inhibited && inhibited != times) {
         SPK_REQUIRE(hipMemcpyAsync(inhibited, times, (size_t)B * C * HW, hipMemcpyDeviceToDevice,
@@ -629,7 +752,7 @@ extern "C" spk_status spk_inhibit(const uint8_t *times, const float *vkey, int B
     const int HW = H * W;
     const long long total = (long long)B * HW;
     hipStream_t s = spk::stream_of(stream);
-    launch_pointwise(times, vkey, C, HW, total, nullptr, inhibited, s);
+    launch_pointwise(times, vkey, C, HW, total, nullptr, inhibited, nullptr, s);
     SPK_LAUNCHED("spk_inhibit");
     return SPK_OK;
 }
