@@ -112,13 +112,15 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
 
 // The same sweep with L consecutive locations per lane (H*W a multiple of
 // L = 4 or 8): each load of a wave brings 64*L time bytes and 256*L bytes of
-// potentials.  Block (x, y) takes the maps [y*c_per, (y+1)*c_per); its kG4
-// waves split them (c = g, g + kG4, ...), with kU maps' loads in flight at a
+// potentials.  Block (x, y) takes the maps [y*c_per, (y+1)*c_per); its G
+// waves split them (c = g, g + G, ...), with U maps' loads in flight at a
 // time, and meet in LDS.  One split (gridDim.y == 1, part == nullptr) gives
 // the result of k_pointwise; with several, each block writes its winner per
 // location to part[y][location] and k_pw_merge finishes.
-constexpr int kG4 = 8;
-constexpr int kU = 4;  // maps whose loads are in flight together
+constexpr int kG4 = 8;   // waves of a block, and
+constexpr int kU = 4;    // maps in flight per wave, of the usual form;
+constexpr int kGW = 16;  // those of the wide form (L = 4) for layers with
+constexpr int kUW = 8;   // few location blocks
 
 template <int L> struct TimesVec;
 template <> struct TimesVec<4> { typedef uint32_t type; };
@@ -131,8 +133,8 @@ __device__ __forceinline__ uint32_t time_at(const typename TimesVec<L>::type &t,
     else return ((q < 4 ? t.x : t.y) >> (8 * (q & 3))) & 0xFF;
 }
 
-template <int L>
-__global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
+template <int L, int G, int U>
+__global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
                                                           const float *__restrict__ vkey, int C,
                                                           int HW, long long total, int c_per,
                                                           Rec *__restrict__ part,
@@ -140,8 +142,8 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
 {
     typedef typename TimesVec<L>::type TV;
     constexpr int NL = 64 * L;  // locations of a block
-    __shared__ int s_t[kG4][NL], s_c[kG4][NL];
-    __shared__ float s_v[kG4][NL];
+    __shared__ int s_t[G][NL], s_c[G][NL];
+    __shared__ float s_v[G][NL];
     const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
     const long long i0 = (long long)blockIdx.x * NL + L * lane;  // b*HW + p, p % L == 0
     const bool ok = i0 < total;
@@ -172,19 +174,19 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
         const int c_lo = (int)blockIdx.y * c_per, c_hi = min(C, c_lo + c_per);
         // a batch past c_hi loads map c_hi - 1 again (no branch around a load)
         // and skips it
-        for (int c = c_lo + grp; c < c_hi; c += kU * kG4) {
-            TV t[kU];
-            float4 v[kU][L / 4];
+        for (int c = c_lo + grp; c < c_hi; c += U * G) {
+            TV t[U];
+            float4 v[U][L / 4];
 #pragma unroll
-            for (int u = 0; u < kU; u++) {
-                const size_t at = base + (size_t)min(c + u * kG4, c_hi - 1) * HW;
+            for (int u = 0; u < U; u++) {
+                const size_t at = base + (size_t)min(c + u * G, c_hi - 1) * HW;
                 t[u] = *reinterpret_cast<const TV *>(times + at);
 #pragma unroll
                 for (int r = 0; r < L / 4; r++) v[u][r] = *reinterpret_cast<const float4 *>(vkey + at + 4 * r);
             }
 #pragma unroll
-            for (int u = 0; u < kU; u++)
-                if (c + u * kG4 < c_hi) take(c + u * kG4, t[u], v[u]);
+            for (int u = 0; u < U; u++)
+                if (c + u * G < c_hi) take(c + u * G, t[u], v[u]);
         }
     }
 #pragma unroll
@@ -194,11 +196,11 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
         s_c[grp][L * lane + q] = bc[q];
     }
     __syncthreads();
-    // the block's locations, one thread each, merge the kG4 partial winners in wave order
+    // the block's locations, one thread each, merge the G partial winners in wave order
     for (int j = threadIdx.x; j < NL; j += blockDim.x) {
         int t0 = s_t[0][j], c0 = s_c[0][j];
         float v0 = s_v[0][j];
-        for (int g = 1; g < kG4; g++) {
+        for (int g = 1; g < G; g++) {
             const int t = s_t[g][j], c = s_c[g][j];
             const float v = s_v[g][j];
             if (c >= 0 && (c0 < 0 || earlier(t, v, c, t0, v0, c0))) {
@@ -226,7 +228,7 @@ __global__ __launch_bounds__(64 * kG4) void k_pointwise_v(const uint8_t *times,
                 wt[q] = s_t[0][L * lane + q];
                 wc[q] = s_c[0][L * lane + q];
             }
-            for (int c = grp; c < C; c += kG4) {
+            for (int c = grp; c < C; c += G) {
                 uint32_t o[2] = {0u, 0u};
 #pragma unroll
                 for (int q = 0; q < L; q++)
@@ -316,24 +318,34 @@ __global__ __launch_bounds__(kThreads) void k_pw_merge(const Rec *__restrict__ p
 }
 
 // How a location sweep is laid out: L locations per lane (0: the scalar
-// kernel), X location blocks and S map splits of c_per maps each.  A wave
-// issues the loads of kU maps together, so a block whose waves have several
-// such batches waits several memory latencies: when there are fewer than
-// 1024 location blocks, the maps are split so that each wave has one batch.
+// kernel), G waves per block with U maps in flight per wave, X location
+// blocks and S map splits of c_per maps each.  A wave issues the loads of U
+// maps together, so a block whose waves have several such batches waits
+// several memory latencies.  Layers with few location blocks take the wide
+// form (16 waves, 8 maps in flight); when even that leaves more than two
+// batches per wave, the maps are split so that each wave has one.
 struct PwPlan {
-    int L;
+    int L, G, U;
     long long X;
     int S, c_per;
 };
 
 PwPlan pw_plan(long long total, int C, int HW, bool aligned, bool may_split)
 {
-    PwPlan pl{0, spk::ceil_div(total, 64), 1, C};
+    PwPlan pl{0, kGroups, 1, spk::ceil_div(total, 64), 1, C};
     if (!aligned || HW % 4 != 0) return pl;
     pl.L = HW % 8 == 0 ? 8 : 4;
+    pl.G = kG4;
+    pl.U = kU;
     pl.X = spk::ceil_div(total, 64 * pl.L);
-    if (may_split && pl.X < 1024 && C > kG4 * kU) {
-        pl.c_per = kG4 * kU;
+    if (spk::ceil_div(total, 64 * 4) < 256) {
+        pl.L = 4;
+        pl.G = kGW;
+        pl.U = kUW;
+        pl.X = spk::ceil_div(total, 64 * 4);
+    }
+    if (may_split && pl.X < 1024 && C > 2 * pl.G * pl.U) {
+        pl.c_per = pl.G * pl.U;
         pl.S = spk::ceil_div(C, pl.c_per);
     }
     return pl;
@@ -355,11 +367,14 @@ void launch_pointwise(const uint8_t *times, const float *vkey, int C, int HW, lo
     Rec *pp = pl.S > 1 ? part : nullptr;
     const dim3 grid((unsigned)pl.X, pl.S);
     if (pl.L == 8)
-        hipLaunchKernelGGL(k_pointwise_v<8>, grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total, pl.c_per,
-                           pp, recs, inhibited);
+        hipLaunchKernelGGL((k_pointwise_v<8, kG4, kU>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
+                           pl.c_per, pp, recs, inhibited);
+    else if (pl.L == 4 && pl.G == kGW)
+        hipLaunchKernelGGL((k_pointwise_v<4, kGW, kUW>), grid, dim3(64 * kGW), 0, s, times, vkey, C, HW, total,
+                           pl.c_per, pp, recs, inhibited);
     else if (pl.L == 4)
-        hipLaunchKernelGGL(k_pointwise_v<4>, grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total, pl.c_per,
-                           pp, recs, inhibited);
+        hipLaunchKernelGGL((k_pointwise_v<4, kG4, kU>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
+                           pl.c_per, pp, recs, inhibited);
     else
         hipLaunchKernelGGL(k_pointwise, dim3((unsigned)pl.X), dim3(64 * kGroups), 0, s, times, vkey, C, HW,
                            total, recs, inhibited);

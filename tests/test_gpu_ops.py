@@ -215,7 +215,7 @@ def test_inhibit_wta_hand_example():
     (4, 200, 5, 5, 1, 0, 0.0, "readout"), (2, 20, 6, 6, 5, 1, 0.0, "readout"),
     (2, 8, 8, 8, 0, 1, 0.3, "pointwise"), (2, 5, 6, 6, 3, 1, 0.0, "pointwise"),
     (2, 6, 80, 90, 6, 2, 0.05, "pointwise"), (2, 12, 20, 30, 7, 1, 0.2, "fired"),
-    (2, 40, 16, 16, 3, 1, 0.0, "readout"),
+    (2, 40, 16, 16, 3, 1, 0.0, "readout"), (2, 600, 6, 6, 3, 1, 0.2, "pointwise"),
 ])
 def test_inhibit_wta_matches_oracle(B, C, H, W, k, r, dens, mode):
     dev = gpu()
@@ -247,10 +247,12 @@ def test_inhibit_in_place():
     np.testing.assert_array_equal(np_(tt), oracle.inhibit(times, vkey))
 
 
-@pytest.mark.parametrize("shape", [(2, 9, 6, 7), (3, 128, 8, 8), (2, 30, 28, 28), (1, 5, 3, 5), (2, 7, 2, 6)])
+@pytest.mark.parametrize("shape", [(2, 9, 6, 7), (3, 128, 8, 8), (2, 30, 28, 28), (1, 5, 3, 5), (2, 7, 2, 6),
+                                   (2, 3, 202, 202), (2, 3, 256, 160), (2, 600, 6, 6)])
 def test_inhibit_alone_matches_oracle(shape):
-    """spk_inhibit: the vectorized pass (H*W % 4 == 0) and the per-location
-    one, to a new map and in place, with ties in time and potential."""
+    """spk_inhibit: the vectorized pass (H*W % 4 == 0: the wide form for few
+    locations, 4 or 8 locations per lane for many) and the per-location one,
+    to a new map and in place, with ties in time and potential."""
     dev = gpu()
     rng = np.random.default_rng(sum(shape))
     times = random_times(rng, shape, 6, 0.5)
