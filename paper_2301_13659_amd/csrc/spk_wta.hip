@@ -730,8 +730,8 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     const long long n_cand = pointwise ? (long long)HW : (long long)C * HW;
     if (k > 0 && n_cand <= 64 * 4) {
         launch_select_reg<4, 1>(B, s, times, vkey, recs, a, winners, n_winners);
-    } else if (k > 0 && n_cand <= 64 * 16) {
-        launch_select_reg<16, 1>(B, s, times, vkey, recs, a, winners, n_winners);
+    } else if (k > 0 && n_cand <= 256 * 4) {
+        launch_select_reg<4, 4>(B, s, times, vkey, recs, a, winners, n_winners);
     } else if (k > 0 && n_cand <= 256 * 16) {
         launch_select_reg<16, 4>(B, s, times, vkey, recs, a, winners, n_winners);
     } else if (k > 0 && n_cand <= 256 * 20) {
