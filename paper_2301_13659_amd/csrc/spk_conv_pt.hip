@@ -293,10 +293,14 @@ __device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words,
 
 // Staged words to LDS as halves 1024 + t, plus a flag per word: does any of
 // its 16 times fire within the window (clamped times: any byte below T)?
-// Returns, uniform over the wave, whether under 80% of the wave's words of
-// the range [0, nw) are flagged: a sparse range, worth testing slices in.
+// Returns, uniform over the wave, whether the range [0, nw) is sparse enough
+// to test slices in: a tile's slice can be skipped only when none of the
+// tile's pt positions has a firing input in it, so with a fraction u of the
+// wave's words unflagged about u^pt of the slices are skipped; testing pays
+// when that is above 40 % (below it the tests cost more than the skipped
+// products save).
 __device__ __forceinline__ bool store_range(const Staged &st, uint8_t *hal, uint8_t *flags,
-                                            uint32_t never4, int nw, int hw)
+                                            uint32_t never4, int nw, int hw, int pt)
 {
     int flagged = 0, words = 0;
 #pragma unroll
@@ -317,7 +321,10 @@ __device__ __forceinline__ bool store_range(const Staged &st, uint8_t *hal, uint
         flagged += __builtin_popcountll(__builtin_amdgcn_ballot_w64(f && k < nw));
         words += __builtin_popcountll(__builtin_amdgcn_ballot_w64(k < nw));
     }
-    return flagged * 5 < words * 4;
+    const float u = words > 0 ? (float)(words - flagged) / (float)words : 0.0f;
+    float skip = u;
+    for (int i = 1; i < pt; i++) skip *= u;
+    return skip > 0.4f;
 }
 
 // Staged results of positions [gs, min(gs + 64, p_end)) to the outputs:
@@ -440,7 +447,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw);
+        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw, PT);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -544,7 +551,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            sparse = store_range(nxt, hal, flags, never4, nxt_words, g.hw);
+            sparse = store_range(nxt, hal, flags, never4, nxt_words, g.hw, PT);
         }
     }
     __syncthreads();  // the last group is staged
@@ -594,7 +601,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        (void)store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw);
+        (void)store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw, 1);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -692,7 +699,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            (void)store_range(nxt, hal, flags, never4, nxt_words, g.hw);
+            (void)store_range(nxt, hal, flags, never4, nxt_words, g.hw, 1);
         }
     }
     __syncthreads();  // the last group is staged
