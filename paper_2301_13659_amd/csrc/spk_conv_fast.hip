@@ -250,7 +250,12 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
             for (int e = threadIdx.x; e < kSlack; e += blockDim.x) row[g.rowb + e] = (uint8_t)spk::kNever;
         return;
     }
-    const int o = blockIdx.x - nb_in;
+    // map of this block: the maps are dealt to the XCDs in contiguous runs
+    // (block L runs on XCD L % 8), so the blocks whose 16-byte fragment
+    // stores share a cache line mostly share an L2 and the line leaves it whole
+    const int n_maps = (int)gridDim.x - nb_in, wb = (int)blockIdx.x - nb_in;
+    const int xcd = wb & 7, per_x = n_maps >> 3, extra = n_maps & 7;
+    const int o = xcd * per_x + min(xcd, extra) + (wb >> 3);
     const int taps = g.Ci * g.Kh * g.Kw;
     float *wl = reinterpret_cast<float *>(sm);
     {
@@ -281,16 +286,17 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
         const int lane = col + (kBig ? 32 : 16) * h;
         const int kb = (s * per + h) * 8;
         h8 hi, lo;
-        // tap kb = ky*R8 + j, j = kx*Ci + c; the 8 taps step through (ky, j, kx, c)
+        // tap kb = ky*R8 + j, j = kx*Ci + c; the 8 taps step through (ky, j, kx, c).
+        // The 8 LDS addresses first (padding taps read word 0), then the
+        // reads together, then the conversions: no branch around a read.
         int ky = kb / g.R8, j = kb - ky * g.R8;
         int kx = j / g.Ci, c = j - kx * g.Ci;
+        int at[8];
+        bool live[8];
 #pragma unroll
         for (int e = 0; e < 8; e++) {
-            float w = 0.0f;
-            if (ky < g.Kh && j < g.run) w = wl[(c * g.Kh + ky) * g.Kw + kx];
-            const _Float16 hw = (_Float16)w;
-            hi[e] = hw;
-            lo[e] = (_Float16)(w - (float)hw);
+            live[e] = ky < g.Kh && j < g.run;
+            at[e] = live[e] ? (c * g.Kh + ky) * g.Kw + kx : 0;
             if (++j == g.R8) {
                 j = 0;
                 ky++;
@@ -300,6 +306,16 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
                 c = 0;
                 kx++;
             }
+        }
+        float wv8[8];
+#pragma unroll
+        for (int e = 0; e < 8; e++) wv8[e] = wl[at[e]];
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            const float w = live[e] ? wv8[e] : 0.0f;
+            const _Float16 hw = (_Float16)w;
+            hi[e] = hw;
+            lo[e] = (_Float16)(w - (float)hw);
         }
         const size_t ts = (size_t)nt * NS + s;
         bp[(ts * NP) * 64 + lane] = hi;

@@ -226,12 +226,23 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
         const int s = f >> 1, half = f & 1;
         const int ky = s / g.Q16, jq = s - ky * g.Q16;
         h8 hi, lo;
+        // addresses first (padding taps read word 0), then the reads together:
+        // no branch around a read
+        int at[8];
+        bool live[8];
 #pragma unroll
         for (int e = 0; e < 8; e++) {
             const int j = jq * 16 + half * 8 + e;
             const int kx = j / g.Cp, c = j - kx * g.Cp;
-            float w = 0.0f;
-            if (s < g.SK && j < g.run && c < g.Ci) w = wl[(c * g.Kh + ky) * g.Kw + kx];
+            live[e] = s < g.SK && j < g.run && c < g.Ci;
+            at[e] = live[e] ? (c * g.Kh + ky) * g.Kw + kx : 0;
+        }
+        float wv8[8];
+#pragma unroll
+        for (int e = 0; e < 8; e++) wv8[e] = wl[at[e]];
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            const float w = live[e] ? wv8[e] : 0.0f;
             const _Float16 hw = (_Float16)w;
             hi[e] = hw;
             lo[e] = (_Float16)(w - (float)hw);
