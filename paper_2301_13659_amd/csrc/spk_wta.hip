@@ -118,7 +118,8 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
 // the result of k_pointwise; with several, each block writes its winner per
 // location to part[y][location] and k_pw_merge finishes.
 constexpr int kG4 = 8;   // waves of a block, and
-constexpr int kU = 4;    // maps in flight per wave, of the usual form;
+constexpr int kU = 4;    // maps in flight per wave, of the usual form
+constexpr int kU8 = 3;   // (three with L = 8: 60 registers, four blocks per CU);
 constexpr int kGW = 16;  // those of the wide form (L = 4) for layers with
 constexpr int kUW = 8;   // few location blocks
 
@@ -142,19 +143,20 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
 {
     typedef typename TimesVec<L>::type TV;
     constexpr int NL = 64 * L;  // locations of a block
-    __shared__ int s_t[G][NL], s_c[G][NL];
+    __shared__ uint32_t s_tc[G][NL];  // time << 24 | map (time NEVER: none)
     __shared__ float s_v[G][NL];
     const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
     const long long i0 = (long long)blockIdx.x * NL + L * lane;  // b*HW + p, p % L == 0
     const bool ok = i0 < total;
     const long long b = ok ? i0 / HW : 0, p = i0 - b * HW;
     const size_t base = (size_t)b * C * HW + p;
-    int bt[L], bc[L];
+    // per location: time << 24 | map of the best so far (time NEVER: none),
+    // one register instead of two, and its potential
+    uint32_t btc[L];
     float bv[L];
 #pragma unroll
     for (int q = 0; q < L; q++) {
-        bt[q] = spk::kNever;
-        bc[q] = -1;
+        btc[q] = ~0u;
         bv[q] = 0.0f;
     }
     if (ok) {
@@ -164,10 +166,10 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
                 const int t = (int)time_at<L>(t4, q);
                 const float4 &vq = v4[q >> 2];
                 const float v = (q & 3) == 0 ? vq.x : (q & 3) == 1 ? vq.y : (q & 3) == 2 ? vq.z : vq.w;
-                if (t != spk::kNever && (t < bt[q] || (t == bt[q] && v > bv[q]))) {
-                    bt[q] = t;
+                const int bt = (int)(btc[q] >> 24);
+                if (t != spk::kNever && (t < bt || (t == bt && v > bv[q]))) {
+                    btc[q] = ((uint32_t)t << 24) | (uint32_t)c;
                     bv[q] = v;
-                    bc[q] = c;
                 }
             }
         };
@@ -191,28 +193,32 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
     }
 #pragma unroll
     for (int q = 0; q < L; q++) {
-        s_t[grp][L * lane + q] = bt[q];
+        s_tc[grp][L * lane + q] = btc[q];
         s_v[grp][L * lane + q] = bv[q];
-        s_c[grp][L * lane + q] = bc[q];
     }
     __syncthreads();
-    // the block's locations, one thread each, merge the G partial winners in wave order
+    // the block's locations, one thread each, merge the G partial winners as
+    // a minimum of 64-bit keys ordered as `earlier` (no branches)
     for (int j = threadIdx.x; j < NL; j += blockDim.x) {
-        int t0 = s_t[0][j], c0 = s_c[0][j];
-        float v0 = s_v[0][j];
-        for (int g = 1; g < G; g++) {
-            const int t = s_t[g][j], c = s_c[g][j];
+        uint64_t best = ~0ull;
+        float v0 = 0.0f;
+        for (int g = 0; g < G; g++) {
+            const uint32_t tc = s_tc[g][j];
             const float v = s_v[g][j];
-            if (c >= 0 && (c0 < 0 || earlier(t, v, c, t0, v0, c0))) {
-                t0 = t;
-                v0 = v;
-                c0 = c;
-            }
+            const uint64_t key = (tc >> 24) == (uint32_t)spk::kNever
+                                     ? ~0ull
+                                     : ((uint64_t)(tc >> 24) << 56) | ((uint64_t)order_desc(v) << 24) |
+                                           (uint64_t)(tc & 0xFFFFFFu);
+            const bool better = key < best;
+            best = better ? key : best;
+            v0 = better ? v : v0;
         }
-        s_t[0][j] = t0;
-        s_c[0][j] = c0;
+        const bool any = best != ~0ull;
+        const uint32_t tc0 = any ? (uint32_t)(best >> 56) << 24 | (uint32_t)(best & 0xFFFFFFu)
+                                 : (uint32_t)spk::kNever << 24;
+        s_tc[0][j] = tc0;
         const long long i = (long long)blockIdx.x * NL + j;
-        const Rec r{((uint32_t)(c0 < 0 ? (int)spk::kNever : t0) << 24) | (uint32_t)(c0 < 0 ? 0 : c0), v0};
+        const Rec r{tc0, any ? v0 : 0.0f};
         if (part) {
             if (i < total) part[(size_t)blockIdx.y * total + i] = r;
         } else if (recs && i < total) {
@@ -225,8 +231,9 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
             int wt[L], wc[L];
 #pragma unroll
             for (int q = 0; q < L; q++) {
-                wt[q] = s_t[0][L * lane + q];
-                wc[q] = s_c[0][L * lane + q];
+                const uint32_t tc = s_tc[0][L * lane + q];
+                wt[q] = (int)(tc >> 24);
+                wc[q] = wt[q] == (int)spk::kNever ? -1 : (int)(tc & 0xFFFFFFu);
             }
             for (int c = grp; c < C; c += G) {
                 uint32_t o[2] = {0u, 0u};
@@ -336,7 +343,7 @@ PwPlan pw_plan(long long total, int C, int HW, bool aligned, bool may_split)
     if (!aligned || HW % 4 != 0) return pl;
     pl.L = HW % 8 == 0 ? 8 : 4;
     pl.G = kG4;
-    pl.U = kU;
+    pl.U = pl.L == 8 ? kU8 : kU;
     pl.X = spk::ceil_div(total, 64 * pl.L);
     if (spk::ceil_div(total, 64 * 4) < 256) {
         pl.L = 4;
@@ -367,7 +374,7 @@ void launch_pointwise(const uint8_t *times, const float *vkey, int C, int HW, lo
     Rec *pp = pl.S > 1 ? part : nullptr;
     const dim3 grid((unsigned)pl.X, pl.S);
     if (pl.L == 8)
-        hipLaunchKernelGGL((k_pointwise_v<8, kG4, kU>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
+        hipLaunchKernelGGL((k_pointwise_v<8, kG4, kU8>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
                            pl.c_per, pp, recs, inhibited);
     else if (pl.L == 4 && pl.G == kGW)
         hipLaunchKernelGGL((k_pointwise_v<4, kGW, kUW>), grid, dim3(64 * kGW), 0, s, times, vkey, C, HW, total,
