@@ -10,6 +10,7 @@
 namespace {
 
 constexpr int kThreads = 256;
+typedef float nf4 __attribute__((ext_vector_type(4)));
 
 __global__ void k_threshold(float *__restrict__ x, int64_t n, float threshold, float value)
 {
@@ -62,7 +63,9 @@ __global__ void k_fire4(const float *__restrict__ V, int B, int T, int64_t n, fl
         float4 v[6];
 #pragma unroll
         for (int u = 0; u < 6; u++)
-            if (t0 + u < T) v[u] = *reinterpret_cast<const float4 *>(src + (size_t)(t0 + u) * n);
+            if (t0 + u < T)  // read once: streaming (non-temporal) loads
+                v[u] = __builtin_bit_cast(float4, __builtin_nontemporal_load(
+                                                      reinterpret_cast<const nf4 *>(src + (size_t)(t0 + u) * n)));
 #pragma unroll
         for (int u = 0; u < 6; u++) {
             if (t0 + u < T) {

@@ -182,9 +182,17 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const size_t at = base + (size_t)min(c + u * G, c_hi - 1) * HW;
-                t[u] = *reinterpret_cast<const TV *>(times + at);
+                // read once: streaming (non-temporal) loads
+                typedef float nf4 __attribute__((ext_vector_type(4)));
+                typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
+                if constexpr (L == 4)
+                    t[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(times + at));
+                else
+                    t[u] = __builtin_bit_cast(TV, __builtin_nontemporal_load(reinterpret_cast<const nu2 *>(times + at)));
 #pragma unroll
-                for (int r = 0; r < L / 4; r++) v[u][r] = *reinterpret_cast<const float4 *>(vkey + at + 4 * r);
+                for (int r = 0; r < L / 4; r++)
+                    v[u][r] = __builtin_bit_cast(
+                        float4, __builtin_nontemporal_load(reinterpret_cast<const nf4 *>(vkey + at + 4 * r)));
             }
 #pragma unroll
             for (int u = 0; u < U; u++)
@@ -240,10 +248,12 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
 #pragma unroll
                 for (int q = 0; q < L; q++)
                     o[q >> 2] |= (uint32_t)(c == wc[q] ? wt[q] : spk::kNever) << (8 * (q & 3));
+                typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
                 if constexpr (L == 4)
-                    *reinterpret_cast<uint32_t *>(inhibited + base + (size_t)c * HW) = o[0];
+                    __builtin_nontemporal_store(o[0], reinterpret_cast<uint32_t *>(inhibited + base + (size_t)c * HW));
                 else
-                    *reinterpret_cast<uint2 *>(inhibited + base + (size_t)c * HW) = make_uint2(o[0], o[1]);
+                    __builtin_nontemporal_store(nu2{o[0], o[1]},
+                                                reinterpret_cast<nu2 *>(inhibited + base + (size_t)c * HW));
             }
         }
     }
