@@ -17,7 +17,9 @@
  *    fires.  Hence T <= SPK_MAX_T (254).
  *  - The library never allocates device memory and never synchronises.  Calls
  *    that need scratch take a caller workspace (ws, ws_bytes) sized by the
- *    matching *_workspace_size query; ws may be NULL when that size is 0.
+ *    matching *_workspace_size query; ws may be NULL when that size is 0.  A
+ *    workspace must be 256-byte aligned (hipMalloc's and torch's are);
+ *    SPK_E_ARG otherwise.
  *  - Every call enqueues its kernels on `stream` (a hipStream_t; NULL is the
  *    null stream) and returns before they run.  Faults of the kernels surface
  *    at the caller's next synchronisation.

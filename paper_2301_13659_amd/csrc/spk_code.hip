@@ -389,6 +389,7 @@ extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int 
     const size_t need = mode == SPK_CODE_RANK ? ws_layout(B, n, &off_b, &off_cnt) : 0;
     SPK_REQUIRE(ws_bytes >= need && (need == 0 || ws), SPK_E_WORKSPACE,
                 "spk_latency_code: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_latency_code");
     hipStream_t s = spk::stream_of(stream);
 
     if (mode == SPK_CODE_LINEAR) {

@@ -129,6 +129,7 @@ extern "C" spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int C
                                                      potentials != nullptr);
     SPK_REQUIRE(ws_bytes >= need && (need == 0 || ws), SPK_E_WORKSPACE,
                 "spk_conv_fire: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_conv_fire");
     SPK_REQUIRE((long long)B * Ho * Wo < (1LL << 31) && (long long)Ci * Hi * Wi < (1LL << 31),
                 SPK_E_SHAPE, "spk_conv_fire: layer too large");
     if (spk::conv_pt_supported(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, half_w, readout,

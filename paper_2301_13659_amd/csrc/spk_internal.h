@@ -71,6 +71,12 @@ spk_status readout_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
         }                                   \
     } while (0)
 
+// Workspaces hold 16-byte vectors and the sources of direct-to-LDS loads:
+// they must be 256-byte aligned (hipMalloc and torch allocations are).
+#define SPK_REQUIRE_WS_ALIGNED(ws, what)                                                     \
+    SPK_REQUIRE(((uintptr_t)(ws) & 255u) == 0u, SPK_E_ARG, "%s: workspace not 256-byte aligned", \
+                what)
+
 #define SPK_LAUNCHED(what)                                  \
     do {                                                    \
         spk_status st_ = spk::check_launch(what);           \

@@ -368,6 +368,7 @@ extern "C" spk_status spk_rate_code(const float *x, const float *u, int B, int64
     SPK_REQUIRE(min_value >= 0.0f, SPK_E_ARG, "spk_rate_code: min_value must be >= 0");
     SPK_REQUIRE(ws_bytes >= (size_t)B * 4, SPK_E_WORKSPACE, "spk_rate_code: workspace %zu < %zu bytes",
                 ws_bytes, (size_t)B * 4);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_rate_code");
     hipStream_t s = spk::stream_of(stream);
     uint32_t *m = static_cast<uint32_t *>(ws);
     hipLaunchKernelGGL(k_rate_zero, dim3((B + 255) / 256), dim3(256), 0, s, m, B);
@@ -416,6 +417,7 @@ extern "C" spk_status spk_conv_if_rate(const uint8_t *frames, int B, int T, int 
     const size_t need = xb + spk::align_up((size_t)g.NT * g.SK * np * 64 * sizeof(h8), 256);
     SPK_REQUIRE(ws_bytes >= need, SPK_E_WORKSPACE, "spk_conv_if_rate: workspace %zu < %zu bytes",
                 ws_bytes, need);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_conv_if_rate");
     g.vec = (g.HoWo % 4 == 0) && ((uintptr_t)out_frames % 4 == 0);
     uint16_t *fp = static_cast<uint16_t *>(ws);
     h8 *bp = reinterpret_cast<h8 *>(static_cast<uint8_t *>(ws) + xb);

@@ -737,6 +737,7 @@ extern "C" spk_status spk_times_to_spikes(const uint8_t *times, int B, int C, in
     const size_t need = spk_times_to_spikes_workspace_size(B, C, H, W, T);
     SPK_REQUIRE(ws_bytes >= need, SPK_E_WORKSPACE, "spk_times_to_spikes: workspace %zu < %zu bytes",
                 ws_bytes, need);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_times_to_spikes");
     SPK_REQUIRE(B <= 65535, SPK_E_SHAPE, "spk_times_to_spikes: B=%d > 65535", B);
     const int nb = (int)std::max<int64_t>(1, std::min<int64_t>((n + 16383) / 16384,
                                                                8192 / ((int64_t)kCvWaves * T)));
@@ -833,6 +834,7 @@ extern "C" spk_status spk_conv_fire_sparse(const uint32_t *spikes, const int32_t
     const size_t need = ev_xp_bytes(g) + spk::align_up((size_t)g.NCH * g.wchunk, 256);
     SPK_REQUIRE(ws_bytes >= need, SPK_E_WORKSPACE, "spk_conv_fire_sparse: workspace %zu < %zu bytes",
                 ws_bytes, need);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_conv_fire_sparse");
     g.vec = (g.HoWo % 4 == 0) && ((uintptr_t)out_times % 4 == 0) && ((uintptr_t)out_vkey % 16 == 0);
     uint8_t *xp = static_cast<uint8_t *>(ws);
     uint8_t *wt = xp + ev_xp_bytes(g);

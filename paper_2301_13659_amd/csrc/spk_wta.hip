@@ -727,6 +727,7 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     const size_t need = pointwise ? spk_inhibit_winners_workspace_size(B, C, H, W) : 0;
     SPK_REQUIRE(ws_bytes >= need && (need == 0 || ws), SPK_E_WORKSPACE,
                 "spk_inhibit_winners: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_inhibit_winners");
     hipStream_t s = spk::stream_of(stream);
     const int HW = H * W;
     Rec *recs = (Rec *)ws;

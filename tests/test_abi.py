@@ -204,3 +204,18 @@ def test_rate_and_batch_limits_validation():
          spk.SPK_E_WORKSPACE, "workspace")
     _err(L.spk_rate_pool(P1, P1, 1, 10, 3, 4, 4, 5, 5, 1, 0, P1, P1, None), spk.SPK_E_SHAPE, "empty")
     assert L.spk_conv_if_rate_workspace_size(2, 300, 6, 28, 28, 25, 5, 5, 1, 2, F16) > 0
+
+
+def test_misaligned_workspace_is_rejected():
+    """Workspaces must be 256-byte aligned: every call that takes one says so
+    before launching anything."""
+    L = spk.load()
+    bad = ctypes.c_void_p(256 + 16)
+    _err(L.spk_latency_code(P1, 32, 6, 160, 250, 30, 0.01, 0, P1, None, bad, 1 << 30, None),
+         spk.SPK_E_ARG, "aligned")
+    _err(L.spk_conv_fire(P1, 1, 5, 2, 8, 8, P1, 0, 3, 3, 3, 1, 1, 1.0, P1, P1, None, bad, 1 << 30,
+                         None), spk.SPK_E_ARG, "aligned")
+    _err(L.spk_inhibit_winners(P1, P1, 2, 4, 5, 5, 15, 1, 2, 1, 0, None, P1, P1, bad, 1 << 20, None),
+         spk.SPK_E_ARG, "aligned")
+    _err(L.spk_rate_code(P1, P1, 2, 10, 5, 0.0, P1, bad, 1 << 20, None), spk.SPK_E_ARG, "aligned")
+
