@@ -114,9 +114,12 @@ __global__ __launch_bounds__(64 * kGroups) void k_pointwise(const uint8_t *times
 // L = 4 or 8): each load of a wave brings 64*L time bytes and 256*L bytes of
 // potentials.  Block (x, y) takes the maps [y*c_per, (y+1)*c_per); its G
 // waves split them (c = g, g + G, ...), with U maps' loads in flight at a
-// time, and meet in LDS.  One split (gridDim.y == 1, part == nullptr) gives
-// the result of k_pointwise; with several, each block writes its winner per
-// location to part[y][location] and k_pw_merge finishes.
+// time, and meet in LDS.  kNT: the loads and the map's stores are
+// non-temporal (large layers, whose data is touched once; a small layer's
+// maps are still in the caches from the conv and go on to the pooling).  One
+// split (gridDim.y == 1, part == nullptr) gives the result of k_pointwise;
+// with several, each block writes its winner per location to
+// part[y][location] and k_pw_merge finishes.
 constexpr int kG4 = 8;   // waves of a block, and
 constexpr int kU = 4;    // maps in flight per wave, of the usual form
 constexpr int kU8 = 3;   // (three with L = 8: 60 registers, four blocks per CU);
@@ -134,7 +137,7 @@ __device__ __forceinline__ uint32_t time_at(const typename TimesVec<L>::type &t,
     else return ((q < 4 ? t.x : t.y) >> (8 * (q & 3))) & 0xFF;
 }
 
-template <int L, int G, int U>
+template <int L, int G, int U, bool kNT>
 __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
                                                           const float *__restrict__ vkey, int C,
                                                           int HW, long long total, int c_per,
@@ -182,17 +185,20 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const size_t at = base + (size_t)min(c + u * G, c_hi - 1) * HW;
-                // read once: streaming (non-temporal) loads
+                // kNT: read once, streaming (non-temporal) loads
                 typedef float nf4 __attribute__((ext_vector_type(4)));
                 typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
-                if constexpr (L == 4)
+                if constexpr (!kNT)
+                    t[u] = *reinterpret_cast<const TV *>(times + at);
+                else if constexpr (L == 4)
                     t[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(times + at));
                 else
                     t[u] = __builtin_bit_cast(TV, __builtin_nontemporal_load(reinterpret_cast<const nu2 *>(times + at)));
 #pragma unroll
                 for (int r = 0; r < L / 4; r++)
-                    v[u][r] = __builtin_bit_cast(
-                        float4, __builtin_nontemporal_load(reinterpret_cast<const nf4 *>(vkey + at + 4 * r)));
+                    v[u][r] = kNT ? __builtin_bit_cast(float4, __builtin_nontemporal_load(
+                                                                   reinterpret_cast<const nf4 *>(vkey + at + 4 * r)))
+                                  : *reinterpret_cast<const float4 *>(vkey + at + 4 * r);
             }
 #pragma unroll
             for (int u = 0; u < U; u++)
@@ -249,11 +255,15 @@ __global__ __launch_bounds__(64 * G) void k_pointwise_v(const uint8_t *times,
                 for (int q = 0; q < L; q++)
                     o[q >> 2] |= (uint32_t)(c == wc[q] ? wt[q] : spk::kNever) << (8 * (q & 3));
                 typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
-                if constexpr (L == 4)
-                    __builtin_nontemporal_store(o[0], reinterpret_cast<uint32_t *>(inhibited + base + (size_t)c * HW));
+                uint8_t *dst = inhibited + base + (size_t)c * HW;
+                if constexpr (!kNT && L == 4)
+                    *reinterpret_cast<uint32_t *>(dst) = o[0];
+                else if constexpr (!kNT)
+                    *reinterpret_cast<uint2 *>(dst) = make_uint2(o[0], o[1]);
+                else if constexpr (L == 4)
+                    __builtin_nontemporal_store(o[0], reinterpret_cast<uint32_t *>(dst));
                 else
-                    __builtin_nontemporal_store(nu2{o[0], o[1]},
-                                                reinterpret_cast<nu2 *>(inhibited + base + (size_t)c * HW));
+                    __builtin_nontemporal_store(nu2{o[0], o[1]}, reinterpret_cast<nu2 *>(dst));
             }
         }
     }
@@ -384,13 +394,13 @@ void launch_pointwise(const uint8_t *times, const float *vkey, int C, int HW, lo
     Rec *pp = pl.S > 1 ? part : nullptr;
     const dim3 grid((unsigned)pl.X, pl.S);
     if (pl.L == 8)
-        hipLaunchKernelGGL((k_pointwise_v<8, kG4, kU8>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
+        hipLaunchKernelGGL((k_pointwise_v<8, kG4, kU8, true>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
                            pl.c_per, pp, recs, inhibited);
     else if (pl.L == 4 && pl.G == kGW)
-        hipLaunchKernelGGL((k_pointwise_v<4, kGW, kUW>), grid, dim3(64 * kGW), 0, s, times, vkey, C, HW, total,
+        hipLaunchKernelGGL((k_pointwise_v<4, kGW, kUW, false>), grid, dim3(64 * kGW), 0, s, times, vkey, C, HW, total,
                            pl.c_per, pp, recs, inhibited);
     else if (pl.L == 4)
-        hipLaunchKernelGGL((k_pointwise_v<4, kG4, kU>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
+        hipLaunchKernelGGL((k_pointwise_v<4, kG4, kU, true>), grid, dim3(64 * kG4), 0, s, times, vkey, C, HW, total,
                            pl.c_per, pp, recs, inhibited);
     else
         hipLaunchKernelGGL(k_pointwise, dim3((unsigned)pl.X), dim3(64 * kGroups), 0, s, times, vkey, C, HW,
