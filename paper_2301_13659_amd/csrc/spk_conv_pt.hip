@@ -402,8 +402,11 @@ __device__ __forceinline__ void tile_epilogue(const f16v &acc, float theta, int 
 }
 
 // SK: slices of the instance (all in registers), NP: 2 = hi/lo products of a
-// float master, 1 = half weights; kMode: alignment of the window runs.
-template <int SK, int NP, int kMode>
+// float master, 1 = half weights; kMode: alignment of the window runs; QC:
+// slices per kernel row when the instance is made for it (SK = Kh * QC), else
+// 0.  With QC known, a slice's offset is one register per kernel row plus a
+// constant, which the LDS reads take as their immediate offset.
+template <int SK, int NP, int kMode, int QC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__restrict__ bp, PGeom g,
                float theta, int nranges,
@@ -439,8 +442,12 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
     int off2[SK];
 #pragma unroll
     for (int s = 0; s < SK; s++) {
-        const int ky = s / g.Q16, jq = s - ky * g.Q16;
-        off2[s] = s < g.SK ? 2 * (ky * g.rowb + jq * 16) : 0;
+        if constexpr (QC > 0) {
+            off2[s] = 2 * (s / QC) * g.rowb + 32 * (s % QC);
+        } else {
+            const int ky = s / g.Q16, jq = s - ky * g.Q16;
+            off2[s] = s < g.SK ? 2 * (ky * g.rowb + jq * 16) : 0;
+        }
     }
     // this lane's slice for the fire flags of a tile (lanes past SK: none)
     const int my_off = lane < g.SK ? (lane / g.Q16) * g.rowb + (lane % g.Q16) * 16 : -1;
@@ -532,6 +539,13 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
                     const u4 x = win[s % kAhead];
                     if (s + kAhead < SK) win[s % kAhead] = rd(s + kAhead);
                     step(s, x);
+                    if constexpr (QC > 0 && kMode == 3) {
+                        // keep kAhead reads in flight: per slice, one LDS read,
+                        // then the fragment's four VALU ops, then the products
+                        if (s + kAhead < SK) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x008, NP, 0);
+                    }
                 }
             } else {
 #pragma unroll
@@ -751,13 +765,26 @@ void launch_deep(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t
 typedef void (*PtLaunch)(dim3, size_t, hipStream_t, const uint8_t *, size_t, const h8 *, const PGeom &,
                          float, int, uint8_t *, float *);
 
-template <int SK, int NP, int kMode>
+template <int SK, int NP, int kMode, int QC = 0>
 void launch_pt(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t xw, const h8 *bp,
                const PGeom &g, float theta, int nranges, uint8_t *ot, float *ov)
 {
-    hipLaunchKernelGGL((k_fire_pt<SK, NP, kMode>), grid, dim3(kThreads), lds, s, xp, xw, bp, g, theta,
+    hipLaunchKernelGGL((k_fire_pt<SK, NP, kMode, QC>), grid, dim3(kThreads), lds, s, xp, xw, bp, g, theta,
                        nranges, ot, ov);
 }
+
+// Instances made for one slice layout: (SK, QC, NP, kMode) of a layer whose
+// Kh * Q16 equals the instance's slices.  3x3 over 32 padded channels with
+// float masters, 5x5 over 6 channels, 3x3 over 64 channels with half weights.
+struct PtExact {
+    int SK, QC, NP, mode;
+    PtLaunch fn;
+};
+const PtExact kExact[] = {
+    {18, 6, 2, 3, &launch_pt<18, 2, 3, 6>},
+    {10, 2, 2, 1, &launch_pt<10, 2, 1, 2>},
+    {36, 12, 1, 3, &launch_pt<36, 1, 3, 12>},
+};
 
 #define SPK_PT(S, N) {&launch_pt<S, N, 0>, &launch_pt<S, N, 1>, &launch_pt<S, N, 2>, &launch_pt<S, N, 3>}
 const PtLaunch kLaunch2[9][4] = {SPK_PT(2, 2),  SPK_PT(4, 2),  SPK_PT(6, 2),  SPK_PT(8, 2), SPK_PT(10, 2),
@@ -876,6 +903,10 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
         int idx = 0;
         while ((half_w ? kSK1 : kSK2)[idx] != g.SKp) idx++;
         launch = (half_w ? kLaunch1 : kLaunch2)[idx][read_mode(g.Cp)];
+        for (const PtExact &e : kExact)
+            if (e.SK == g.SK && g.SKp == g.SK && e.QC == g.Q16 && e.NP == (half_w ? 1 : 2) &&
+                e.mode == read_mode(g.Cp))
+                launch = e.fn;
     } else {
         launch = kDeep[half_w ? 0 : 1][read_mode(g.Cp)];
     }
