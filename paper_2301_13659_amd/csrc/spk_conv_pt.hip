@@ -405,8 +405,9 @@ __device__ __forceinline__ void tile_epilogue(const f16v &acc, float theta, int 
 // float master, 1 = half weights; kMode: alignment of the window runs; QC:
 // slices per kernel row when the instance is made for it (SK = Kh * QC), else
 // 0.  With QC known, a slice's offset is one register per kernel row plus a
-// constant, which the LDS reads take as their immediate offset.
-template <int SK, int NP, int kMode, int QC>
+// constant, which the LDS reads take as their immediate offset.  TPC: steps
+// per position in a tile when the instance is made for it, else 0.
+template <int SK, int NP, int kMode, int QC, int TPC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__restrict__ bp, PGeom g,
                float theta, int nranges,
@@ -454,10 +455,11 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
 
     // row (p, t) of this lane: slot p = r / TP, step t = r % TP (capped at T - 1)
     const int r = lane & 31, hh = lane >> 5;
-    const int pl = r >> g.lgTP, tt = r & (g.TP - 1);
+    const int lgTP = TPC == 8 ? 3 : (TPC == 16 ? 4 : (TPC == 32 ? 5 : g.lgTP));
+    const int pl = r >> lgTP, tt = r & ((1 << lgTP) - 1);
     const uint32_t cbv = 0x6401u + (uint32_t)min(tt, g.T - 1);
     const h2 cc = as_h2(cbv | (cbv << 16));
-    const int PT = 32 >> g.lgTP;  // positions per tile
+    const int PT = 32 >> lgTP;  // positions per tile
     const uint32_t never4 = 0x01010101u * (uint32_t)g.T;
 
     bool sparse;
@@ -539,10 +541,12 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
                     const u4 x = win[s % kAhead];
                     if (s + kAhead < SK) win[s % kAhead] = rd(s + kAhead);
                     step(s, x);
-                    if constexpr (QC > 0 && kMode == 3) {
-                        // keep kAhead reads in flight: per slice, one LDS read,
-                        // then the fragment's four VALU ops, then the products
-                        if (s + kAhead < SK) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    if constexpr (QC > 0 && kMode >= 1) {
+                        // keep kAhead reads in flight: per slice, the LDS reads of
+                        // one window piece, then the fragment's four VALU ops,
+                        // then the products
+                        constexpr int kReads = kMode == 1 ? 2 : 1;  // paired b32 reads merge
+                        if (s + kAhead < SK) __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
                         __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
                         __builtin_amdgcn_sched_group_barrier(0x008, NP, 0);
                     }
@@ -559,8 +563,8 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
             if (tp0 + wstep < wp1) xo_next = tab[min(tp0 + wstep - gs + pl, cnt - 1)].xoff;
             uint32_t st[4] = {0u, 0u, 0u, 0u};
             float sv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-            if (g.lgTP == 3) tile_epilogue<8>(acc, theta, hh, st, sv);
-            else if (g.lgTP == 4) tile_epilogue<16>(acc, theta, hh, st, sv);
+            if (lgTP == 3) tile_epilogue<8>(acc, theta, hh, st, sv);
+            else if (lgTP == 4) tile_epilogue<16>(acc, theta, hh, st, sv);
             else tile_epilogue<32>(acc, theta, hh, st, sv);
             const int o = lane & 31;
             if (hh == 0) {
@@ -765,25 +769,27 @@ void launch_deep(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t
 typedef void (*PtLaunch)(dim3, size_t, hipStream_t, const uint8_t *, size_t, const h8 *, const PGeom &,
                          float, int, uint8_t *, float *);
 
-template <int SK, int NP, int kMode, int QC = 0>
+template <int SK, int NP, int kMode, int QC = 0, int TPC = 0>
 void launch_pt(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t xw, const h8 *bp,
                const PGeom &g, float theta, int nranges, uint8_t *ot, float *ov)
 {
-    hipLaunchKernelGGL((k_fire_pt<SK, NP, kMode, QC>), grid, dim3(kThreads), lds, s, xp, xw, bp, g, theta,
-                       nranges, ot, ov);
+    hipLaunchKernelGGL((k_fire_pt<SK, NP, kMode, QC, TPC>), grid, dim3(kThreads), lds, s, xp, xw, bp, g,
+                       theta, nranges, ot, ov);
 }
 
-// Instances made for one slice layout: (SK, QC, NP, kMode) of a layer whose
-// Kh * Q16 equals the instance's slices.  3x3 over 32 padded channels with
-// float masters, 5x5 over 6 channels, 3x3 over 64 channels with half weights.
+// Instances made for one slice layout and tile shape: (SK, QC, NP, kMode, TP)
+// of a layer whose Kh * Q16 equals the instance's slices.  3x3 over 32 padded
+// channels with float masters, 5x5 over 6 channels, 3x3 over 64 channels with
+// half weights; 16 or 32 steps per position.
 struct PtExact {
-    int SK, QC, NP, mode;
+    int SK, QC, NP, mode, TP;
     PtLaunch fn;
 };
 const PtExact kExact[] = {
-    {18, 6, 2, 3, &launch_pt<18, 2, 3, 6>},
-    {10, 2, 2, 1, &launch_pt<10, 2, 1, 2>},
-    {36, 12, 1, 3, &launch_pt<36, 1, 3, 12>},
+    {18, 6, 2, 3, 16, &launch_pt<18, 2, 3, 6, 16>},
+    {10, 2, 2, 1, 16, &launch_pt<10, 2, 1, 2, 16>},
+    {10, 2, 2, 1, 32, &launch_pt<10, 2, 1, 2, 32>},
+    {36, 12, 1, 3, 32, &launch_pt<36, 1, 3, 12, 32>},
 };
 
 #define SPK_PT(S, N) {&launch_pt<S, N, 0>, &launch_pt<S, N, 1>, &launch_pt<S, N, 2>, &launch_pt<S, N, 3>}
@@ -905,7 +911,7 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
         launch = (half_w ? kLaunch1 : kLaunch2)[idx][read_mode(g.Cp)];
         for (const PtExact &e : kExact)
             if (e.SK == g.SK && g.SKp == g.SK && e.QC == g.Q16 && e.NP == (half_w ? 1 : 2) &&
-                e.mode == read_mode(g.Cp))
+                e.mode == read_mode(g.Cp) && e.TP == g.TP)
                 launch = e.fn;
     } else {
         launch = kDeep[half_w ? 0 : 1][read_mode(g.Cp)];
