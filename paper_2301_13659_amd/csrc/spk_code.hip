@@ -9,9 +9,11 @@
 // written as never firing up front.
 //
 //  - Samples of up to kSmall values are ranked by one workgroup each: the
-//    eligible keys are compacted, every thread sorts 8 of them in registers,
-//    then merge-path levels in LDS merge the runs (no padding to a power of
-//    two).
+//    eligible keys are counted into buckets of their value word, a prefix sum
+//    of the counts gives each bucket's first rank and a scan of its members
+//    the rest.  Samples with a crowded bucket are sorted instead: every
+//    thread sorts 8 keys in registers, then merge levels in LDS merge the
+//    runs (no padding to a power of two).
 //  - Larger samples: workgroups sort kSmall-key chunks in LDS, then merge
 //    passes double the sorted runs (merge-path split per thread) until each
 //    sample is one run; the ping-pong buffers live in the caller workspace.
@@ -143,45 +145,13 @@ __device__ void merge_level_rank(const uint64_t *src, uint64_t *dst, int n, int 
     }
 }
 
-// Whole sample in one workgroup.  The eligible keys are compacted first (in
-// index order, by a block prefix sum), then only those are sorted: register
-// sort of 8, LDS merge levels by rank; rank r of the N sorted keys fires at
-// r*T/N.
-// n <= 8 * blockDim.
-__global__ __launch_bounds__(kThreads) void k_code_small(const float *__restrict__ x, int n, int T,
-                                                         float min_value,
-                                                         uint8_t *__restrict__ times)
+// Sorts the N compacted keys of one sample held in src (dst: a second buffer
+// of N keys) and writes each one's step: register sort of 8 per thread, then
+// LDS merge levels by rank; rank r of the N sorted keys fires at r*T/N.
+__device__ void sort_and_time(uint64_t *src, uint64_t *dst, int N, int T, uint8_t *__restrict__ ts)
 {
-    extern __shared__ uint64_t keys[];  // two buffers of n keys
-    __shared__ int red[kThreads / 64];
-    const int b = blockIdx.x;
-    const float *xs = x + (size_t)b * n;
-    uint8_t *ts = times + (size_t)b * n;
-    uint64_t k8[8];
-    int mine = 0;
     const int first = threadIdx.x * 8;
-    float xv[8];
-#pragma unroll
-    for (int j = 0; j < 8; j++) xv[j] = xs[min(first + j, n - 1)];  // all loads first
-#pragma unroll
-    for (int j = 0; j < 8; j++) {
-        const int i = first + j;
-        uint64_t key = kDead;
-        if (i < n) {
-            key = make_key(xv[j], min_value, (uint32_t)i);
-            if (key == kDead) ts[i] = spk::kNever;
-            else mine++;
-        }
-        k8[j] = key;
-    }
-    int N;
-    int w = block_exclusive_scan(mine, red, N);
-    uint64_t *src = keys, *dst = keys + n;
-#pragma unroll
-    for (int j = 0; j < 8; j++)
-        if (k8[j] != kDead) src[w++] = k8[j];
-    __syncthreads();
-    if (N == 0) return;
+    uint64_t k8[8];
     if (first < N) {
 #pragma unroll
         for (int j = 0; j < 8; j++) k8[j] = first + j < N ? src[first + j] : kDead;
@@ -200,6 +170,117 @@ __global__ __launch_bounds__(kThreads) void k_code_small(const float *__restrict
     }
     for (int r = threadIdx.x; r < N; r += blockDim.x)
         ts[(uint32_t)src[r]] = (uint8_t)(((long long)r * T) / N);
+}
+
+// Whole sample in one workgroup, ranked by bucketing.  A key's rank is the
+// number of eligible keys below it: the keys whose value word lies in a lower
+// bucket, plus those of its own bucket that are smaller.  Buckets split the
+// sample's span of value words [lo, hi] into kBk equal runs of 2^sh words
+// (a monotone map), so the first term is a prefix sum of the bucket counts
+// and the second a scan of the bucket's members once the keys are scattered
+// in bucket order.  When a bucket holds more than kBkMax keys (many equal or
+// nearly equal values) the scattered keys are sorted instead.  n <= 8 * blockDim.
+constexpr int kBk = 4096;
+constexpr int kBkMax = 96;
+
+__global__ __launch_bounds__(kThreads) void k_code_bucket(const float *__restrict__ x, int n, int T,
+                                                          float min_value, uint8_t *__restrict__ times)
+{
+    extern __shared__ uint64_t keys[];  // two buffers of n keys (the second for the sort)
+    __shared__ int cnt[kBk + 1];        // bucket counts, then their first slots
+    __shared__ int red[kThreads / 64];
+    __shared__ uint32_t mm[3];          // lowest and highest value word, largest bucket
+    const int b = blockIdx.x;
+    const float *xs = x + (size_t)b * n;
+    uint8_t *ts = times + (size_t)b * n;
+    const int tid = threadIdx.x, lane = tid & 63;
+
+    float xv[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) xv[j] = xs[min(tid + kThreads * j, n - 1)];  // coalesced, all loads first
+    for (int e = tid; e <= kBk; e += kThreads) cnt[e] = 0;
+    if (tid == 0) {
+        mm[0] = ~0u;
+        mm[1] = 0u;
+        mm[2] = 0u;
+    }
+    uint64_t k8[8];
+    uint32_t lo = ~0u, hi = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+        const int i = tid + kThreads * j;
+        uint64_t key = kDead;
+        if (i < n) {
+            key = make_key(xv[j], min_value, (uint32_t)i);
+            if (key == kDead) {
+                ts[i] = spk::kNever;
+            } else {
+                lo = min(lo, (uint32_t)(key >> 32));
+                hi = max(hi, (uint32_t)(key >> 32));
+            }
+        }
+        k8[j] = key;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = min(lo, (uint32_t)__shfl_xor((int)lo, o, 64));
+        hi = max(hi, (uint32_t)__shfl_xor((int)hi, o, 64));
+    }
+    __syncthreads();  // counts and mm initialised
+    if (lane == 0) {
+        atomicMin(&mm[0], lo);
+        atomicMax(&mm[1], hi);
+    }
+    __syncthreads();
+    const uint32_t w0 = mm[0], w1 = mm[1];
+    if (w0 > w1) return;  // no eligible value (uniform over the block)
+    const uint32_t span = w1 - w0;
+    const int sh = (span >> 12) == 0u ? 0 : 32 - __clz((int)span) - 12;  // (span >> sh) < kBk
+    int bk[8], slot[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+        bk[j] = 0;
+        slot[j] = 0;
+        if (k8[j] != kDead) {
+            bk[j] = (int)(((uint32_t)(k8[j] >> 32) - w0) >> sh);
+            slot[j] = atomicAdd(&cnt[bk[j]], 1);
+        }
+    }
+    __syncthreads();
+    // exclusive prefix sum of the counts (4 consecutive buckets per thread)
+    int c4[4], sum = 0, big = 0;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        c4[q] = cnt[4 * tid + q];
+        sum += c4[q];
+        big = max(big, c4[q]);
+    }
+    for (int o = 32; o > 0; o >>= 1) big = max(big, __shfl_xor(big, o, 64));
+    if (lane == 0) atomicMax(&mm[2], (uint32_t)big);
+    int N;
+    int at = block_exclusive_scan(sum, red, N);  // has barriers: every count is read
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        cnt[4 * tid + q] = at;
+        at += c4[q];
+    }
+    if (tid == 0) cnt[kBk] = N;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 8; j++)
+        if (k8[j] != kDead) keys[cnt[bk[j]] + slot[j]] = k8[j];
+    __syncthreads();
+    if ((int)mm[2] > kBkMax) {  // uniform: sort the scattered keys
+        sort_and_time(keys, keys + n, N, T, ts);
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+        if (k8[j] == kDead) continue;
+        const int s0 = cnt[bk[j]], s1 = cnt[bk[j] + 1];
+        int r = s0;
+        for (int m = s0; m < s1; m++) r += keys[m] < k8[j] ? 1 : 0;
+        ts[tid + kThreads * j] = (uint8_t)(((long long)r * T) / N);
+    }
 }
 
 // Large samples, step 1: keys, never-firing outputs, eligible counts.
@@ -398,9 +479,9 @@ extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int 
     } else if (n <= kSmall) {
         const size_t lds = 2 * (size_t)n * sizeof(uint64_t);
         if (lds > 64 * 1024)
-            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_code_small),
+            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_code_bucket),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k_code_small, dim3(B), dim3(kThreads), lds, s, x, n, T, min_value, times);
+        hipLaunchKernelGGL(k_code_bucket, dim3(B), dim3(kThreads), lds, s, x, n, T, min_value, times);
         SPK_LAUNCHED("spk_latency_code");
     } else {
         uint64_t *ka = (uint64_t *)ws;

@@ -63,6 +63,20 @@ def test_latency_code_bit_exact(shape, T):
     np.testing.assert_array_equal(got, oracle.latency_code(x, T, 0.01))
 
 
+def test_latency_code_crowded_and_spread_samples():
+    # bucketed ranks for spread values, the sort for samples with many equal values
+    dev = gpu()
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((5, 6, 28, 28)).astype(np.float32)
+    x[1] = 0.5                                        # one value: a single crowded bucket
+    x[2] = np.where(rng.random((6, 28, 28)) < 0.5, 0.25, 2.0).astype(np.float32)
+    x[3, :3] = 1.0                                    # half the sample tied, half spread
+    x[4] = np.exp(rng.uniform(-20, 20, (6, 28, 28))).astype(np.float32)  # a wide span of exponents
+    for T in (15, 30, 254):
+        got = np_(spk.spk_latency_code(_t(x, dev), T, 0.01))
+        np.testing.assert_array_equal(got, oracle.latency_code(x, T, 0.01))
+
+
 def test_latency_code_frames_and_linear_mode():
     dev = gpu()
     rng = np.random.default_rng(11)
