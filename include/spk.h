@@ -150,8 +150,10 @@ spk_status spk_latency_code(const float *x, int B, int C, int H, int W, int T,
  *   potentials nullable float B x T x Co x Ho x Wo (device): every V_t
  *              (the paper's dense interface, §II-B).
  *   ws         workspace of spk_conv_fire_workspace_size(..., theta, potentials
- *              != NULL) bytes (non-zero only for readout calls: theta = +inf
- *              without dense potentials).
+ *              != NULL) bytes: a padded channels-last copy of the input and
+ *              the weights packed as matrix-core operands (and, for readout
+ *              calls, per-split partial sums).  Its contents on entry do not
+ *              matter; it holds nothing the caller needs afterwards.
  * Potentials are accumulated in float from products that are exact: binary
  * spikes times half weights, or times the two halves hi + lo of a float
  * weight (hi = half(w), lo = half(w - hi)).
@@ -215,9 +217,15 @@ spk_status spk_inhibit_winners(const uint8_t *times, const float *vkey,
  * padding): t_pre <= t_post takes a_causal, otherwise a_anticausal.  With the
  * stabiliser dW = (a * (W - L)) * (U - W), without it dW = a, always from the
  * weights before the call.  The batch rule equals the single-sample rule
- * (§II-F.1): the dW of all winners are summed in float in the order (b
- * ascending, slot ascending), then W = min(U, max(L, W + sum)) for every
- * weight that received a change.
+ * (§II-F.1): the dW of all winners are summed in float, then W = min(U,
+ * max(L, W + sum)) for every weight that received a change.  The order of
+ * the float sum is fixed, so repeated calls agree bit for bit: the winners
+ * of map o are listed in (b ascending, slot ascending) order and taken in
+ * chunks of the 1024 (b, slot) entries; within a chunk, a kernel of at
+ * most 512 synapses splits its n winners into G = min(n, 1024 / synapses)
+ * strided groups (winners g, g + G, g + 2G, ... of the chunk's list), sums
+ * each group from zero and adds the G sums in group order; otherwise it adds
+ * the winners one by one in list order.
  *   w          float Co x Ci x Kh x Kw master weights (device, in/out).
  *   w_f16      nullable IEEE-half Co x Ci x Kh x Kw (device): refreshed with
  *              the round-to-nearest-even half of every updated weight.

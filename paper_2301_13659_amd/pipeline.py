@@ -102,23 +102,12 @@ class Pipeline:
                 l.w16.copy_(w16)
 
     def step(self, keep: bool = False, learn: bool = True, timers: dict | None = None,
-             only: set | None = None) -> StepOutputs | None:
-        """One pass over the batch.  timers: stage name -> list of (start, end)
-        torch.cuda.Event pairs recorded on the current stream around each stage
-        (or only around the stages named in `only`)."""
+             only: set | None = None, gate=None, reps: int = 1) -> StepOutputs | None:
+        """One pass over the batch.  timers, only, gate, reps: see _stage_timer."""
         wl = self.wl
         out = StepOutputs() if keep else None
 
-        def timed(name, fn):
-            if timers is None or (only is not None and name not in only):
-                return fn()
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record()
-            r = fn()
-            b.record()
-            timers.setdefault(name, []).append((a, b))
-            return r
+        timed = _stage_timer(timers, only, gate, reps)
 
         if self.wl.lr_schedule is not None and learn:
             f = self.rate_factor()
@@ -188,6 +177,37 @@ class Pipeline:
         return out
 
 
+
+def _stage_timer(timers: dict | None, only: set | None, gate, reps: int):
+    """Wraps each stage of a step.  With timers given, a stage (or only those
+    named in `only`) is bracketed by a pair of torch.cuda.Event records on the
+    current stream, appended to timers[name] as (start, end, reps).  gate
+    (optional) is called before the start event: a GPU delay that lets the
+    host enqueue the whole stage before the GPU reaches it, so the pair
+    measures the stage's kernels and not the host's launch overhead.  reps > 1
+    runs the stage that many times between the events (same inputs; a
+    learning stage then updates its weights reps times)."""
+    def timed(name, fn):
+        if timers is None or (only is not None and name not in only):
+            return fn()
+        if gate is not None:
+            gate()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        r = fn()
+        for _ in range(reps - 1):
+            r = fn()
+        b.record()
+        timers.setdefault(name, []).append((a, b, reps))
+        return r
+    return timed
+
+
+def stage_ms(timers: dict) -> dict:
+    """Average milliseconds per call of each timed stage."""
+    return {k: sum(a.elapsed_time(b) for a, b, _ in v) / sum(r for _, _, r in v) for k, v in timers.items()}
+
 def conv_flops(wl: wls.Workload) -> list:
     """Dense-interface work per conv layer and batch: 2*B*T*Ho*Wo*Co*Ci*Kh*Kw."""
     return [f for f, _ in conv_work(wl, dense=True)]
@@ -242,20 +262,12 @@ class RatePipeline:
             self.layers.append(LayerState(spec, w, w16))
         self.filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
 
-    def step(self, keep: bool = False, timers: dict | None = None, only: set | None = None):
+    def step(self, keep: bool = False, timers: dict | None = None, only: set | None = None, gate=None,
+             reps: int = 1):
         wl = self.wl
         out = StepOutputs() if keep else None
 
-        def timed(name, fn):
-            if timers is None or (only is not None and name not in only):
-                return fn()
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record()
-            r = fn()
-            b.record()
-            timers.setdefault(name, []).append((a, b))
-            return r
+        timed = _stage_timer(timers, only, gate, reps)
 
         if wl.log_stds:
             x = timed("dog", lambda: spk.spk_log_filter(self.images, wl.log_stds, wl.log_ksize))

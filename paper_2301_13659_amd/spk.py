@@ -140,8 +140,29 @@ def _stream(device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
+_sentinel = False
+
+
+def set_output_sentinel(on: bool) -> None:
+    """Test aid: while on, every output and workspace these wrappers allocate
+    is filled before the call (floats with NaN, every other type with 0xAB
+    bytes), so an element a kernel fails to write cannot match a reference."""
+    global _sentinel
+    _sentinel = bool(on)
+
+
+def _empty(shape, dtype, device) -> torch.Tensor:
+    t = torch.empty(shape, dtype=dtype, device=device)
+    if _sentinel:
+        if t.is_floating_point():
+            t.fill_(float("nan"))
+        elif t.numel():
+            t.view(torch.uint8).fill_(0xAB)
+    return t
+
+
 def _workspace(nbytes: int, device) -> torch.Tensor | None:
-    return torch.empty(nbytes, dtype=torch.uint8, device=device) if nbytes else None
+    return _empty(nbytes, dtype=torch.uint8, device=device) if nbytes else None
 
 
 def out_extent(n: int, k: int, stride: int, pad: int) -> int:
@@ -161,7 +182,7 @@ def spk_dog_filter(img, filters, pad: int = -1, out=None):
     K0 = int(filters[0][0])
     Ho, Wo = (H, W) if pad < 0 else (H + 2 * pad - K0 + 1, W + 2 * pad - K0 + 1)
     if out is None:
-        out = torch.empty((B, C * len(filters), Ho, Wo), dtype=torch.float32, device=img.device)
+        out = _empty((B, C * len(filters), Ho, Wo), dtype=torch.float32, device=img.device)
     _dev(out, torch.float32, "out", 4)
     _check(load().spk_dog_filter(_ptr(img), B, C, H, W, descs, len(filters), pad, _ptr(out),
                                  _stream(img.device)))
@@ -173,11 +194,11 @@ def spk_latency_code(x, T: int, min_value: float = 0.01, mode: int = SPK_CODE_RA
     _dev(x, torch.float32, "x", 4)
     B, C, H, W = x.shape
     if times is None:
-        times = torch.empty((B, C, H, W), dtype=torch.uint8, device=x.device)
+        times = _empty((B, C, H, W), dtype=torch.uint8, device=x.device)
     _dev(times, torch.uint8, "times", 4)
     fr = None
     if frames is True:
-        fr = torch.empty((B, T, C, H, W), dtype=torch.uint8, device=x.device)
+        fr = _empty((B, T, C, H, W), dtype=torch.uint8, device=x.device)
     elif isinstance(frames, torch.Tensor):
         fr = _dev(frames, torch.uint8, "frames", 5)
     L = load()
@@ -203,14 +224,14 @@ def spk_conv_fire(in_times, w, T: int, stride: int = 1, pad: int = 0, theta: flo
     Ho, Wo = L.spk_out_extent(Hi, Kh, stride, pad), L.spk_out_extent(Wi, Kw, stride, pad)
     dev = in_times.device
     if out_times is None:
-        out_times = torch.empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.uint8, device=dev)
+        out_times = _empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.uint8, device=dev)
     if out_vkey is None:
-        out_vkey = torch.empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.float32, device=dev)
+        out_vkey = _empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.float32, device=dev)
     _dev(out_times, torch.uint8, "out_times", 4)
     _dev(out_vkey, torch.float32, "out_vkey", 4)
     V = None
     if potentials is True:
-        V = torch.empty((B, T, Co, Ho, Wo), dtype=torch.float32, device=dev)
+        V = _empty((B, T, Co, Ho, Wo), dtype=torch.float32, device=dev)
     elif isinstance(potentials, torch.Tensor):
         V = _dev(potentials, torch.float32, "potentials", 5)
     nbytes = L.spk_conv_fire_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, float(theta),
@@ -231,7 +252,7 @@ def spk_pool(in_times, k, stride: int | None = None, pad: int = 0, out=None):
     L = load()
     Ho, Wo = L.spk_out_extent(Hi, kh, stride, pad), L.spk_out_extent(Wi, kw, stride, pad)
     if out is None:
-        out = torch.empty((B, C, max(Ho, 1), max(Wo, 1)), dtype=torch.uint8, device=in_times.device)
+        out = _empty((B, C, max(Ho, 1), max(Wo, 1)), dtype=torch.uint8, device=in_times.device)
     _dev(out, torch.uint8, "out", 4)
     _check(L.spk_pool(_ptr(in_times), B, C, Hi, Wi, kh, kw, stride, pad, _ptr(out),
                       _stream(in_times.device)))
@@ -246,14 +267,14 @@ def spk_inhibit_winners(times, vkey, T: int, k: int, radius: int, pointwise: boo
     B, C, H, W = times.shape
     dev = times.device
     if winners is None:
-        winners = torch.empty((B, k, 5), dtype=torch.int32, device=dev)
+        winners = _empty((B, k, 5), dtype=torch.int32, device=dev)
     if n_winners is None:
-        n_winners = torch.empty((B,), dtype=torch.int32, device=dev)
+        n_winners = _empty((B,), dtype=torch.int32, device=dev)
     _dev(winners, torch.int32, "winners", 3)
     _dev(n_winners, torch.int32, "n_winners", 1)
     inh = None
     if inhibited is True:
-        inh = torch.empty_like(times)
+        inh = _empty(times.shape, dtype=times.dtype, device=times.device)
     elif isinstance(inhibited, torch.Tensor):
         inh = _dev(inhibited, torch.uint8, "inhibited", 4)
     L = load()
@@ -301,7 +322,7 @@ def spk_rstdp_select(winners, n_winners, labels, group: int, out=None):
     _dev(labels, torch.int32, "labels", 1)
     B, k = winners.shape[:2]
     if out is None:
-        out = torch.empty((B, k), dtype=torch.int32, device=winners.device)
+        out = _empty((B, k), dtype=torch.int32, device=winners.device)
     _check(load().spk_rstdp_select(_ptr(winners), _ptr(n_winners), B, k, _ptr(labels), group,
                                    _ptr(out), _stream(winners.device)))
     return out
@@ -312,7 +333,7 @@ def spk_frames_to_times(frames, out=None):
     B, T = frames.shape[:2]
     n = frames[0, 0].numel()
     if out is None:
-        out = torch.empty((B,) + tuple(frames.shape[2:]), dtype=torch.uint8, device=frames.device)
+        out = _empty((B,) + tuple(frames.shape[2:]), dtype=torch.uint8, device=frames.device)
     _check(load().spk_frames_to_times(_ptr(frames), B, T, n, _ptr(out), _stream(frames.device)))
     return out
 
@@ -322,7 +343,7 @@ def spk_times_to_frames(times, T: int, out=None):
     B = times.shape[0]
     n = times[0].numel()
     if out is None:
-        out = torch.empty((B, T) + tuple(times.shape[1:]), dtype=torch.uint8, device=times.device)
+        out = _empty((B, T) + tuple(times.shape[1:]), dtype=torch.uint8, device=times.device)
     _check(load().spk_times_to_frames(_ptr(times), B, T, n, _ptr(out), _stream(times.device)))
     return out
 
@@ -330,7 +351,7 @@ def spk_times_to_frames(times, T: int, out=None):
 def spk_cast_f16(x, out=None):
     _dev(x, torch.float32, "x")
     if out is None:
-        out = torch.empty(x.shape, dtype=torch.float16, device=x.device)
+        out = _empty(x.shape, dtype=torch.float16, device=x.device)
     _check(load().spk_cast_f16(_ptr(x), _ptr(out), x.numel(), _stream(x.device)))
     return out
 
@@ -346,9 +367,9 @@ def spk_fc_fire(in_times, w, T: int, theta: float = math.inf, potentials=False):
     if I != I2:
         raise ValueError(f"w has {I2} inputs, input has {I}")
     dev = in_times.device
-    out_times = torch.empty((B, O), dtype=torch.uint8, device=dev)
-    out_vkey = torch.empty((B, O), dtype=torch.float32, device=dev)
-    V = torch.empty((B, T, O), dtype=torch.float32, device=dev) if potentials else None
+    out_times = _empty((B, O), dtype=torch.uint8, device=dev)
+    out_vkey = _empty((B, O), dtype=torch.float32, device=dev)
+    V = _empty((B, T, O), dtype=torch.float32, device=dev) if potentials else None
     L = load()
     nbytes = L.spk_fc_fire_workspace_size(B, T, I, O, float(theta), int(V is not None))
     ws = _workspace(nbytes, dev)
@@ -364,8 +385,8 @@ def spk_fc_winners(times, vkey, T: int, k: int, radius: int, readout: bool = Fal
     _dev(vkey, torch.float32, "vkey", 2)
     B, O = times.shape
     dev = times.device
-    winners = torch.empty((B, k, 5), dtype=torch.int32, device=dev)
-    n_winners = torch.empty((B,), dtype=torch.int32, device=dev)
+    winners = _empty((B, k, 5), dtype=torch.int32, device=dev)
+    n_winners = _empty((B,), dtype=torch.int32, device=dev)
     _check(load().spk_fc_winners(_ptr(times), _ptr(vkey), B, O, T, k, radius, int(bool(readout)),
                                  _ptr(winners), _ptr(n_winners), _stream(dev)))
     return winners, n_winners
@@ -413,8 +434,8 @@ def spk_times_to_spikes(times, T: int, cap: int | None = None):
     B, C, H, W = times.shape
     cap = C * H * W if cap is None else int(cap)
     dev = times.device
-    spikes = torch.empty((B, cap), dtype=torch.int32, device=dev)
-    offsets = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+    spikes = _empty((B, cap), dtype=torch.int32, device=dev)
+    offsets = _empty((B, T + 1), dtype=torch.int32, device=dev)
     L = load()
     nbytes = L.spk_times_to_spikes_workspace_size(B, C, H, W, T)
     ws = _workspace(max(nbytes, 1), dev)
@@ -429,7 +450,7 @@ def spk_spikes_to_times(spikes, offsets, shape, T: int):
     _dev(offsets, torch.int32, "offsets", 2)
     B, cap = spikes.shape
     C, H, W = shape
-    times = torch.empty((B, C, H, W), dtype=torch.uint8, device=spikes.device)
+    times = _empty((B, C, H, W), dtype=torch.uint8, device=spikes.device)
     _check(load().spk_spikes_to_times(_ptr(spikes), _ptr(offsets), cap, B, C, H, W, T, _ptr(times),
                                       _stream(spikes.device)))
     return times
@@ -451,8 +472,8 @@ def spk_conv_fire_sparse(spikes, offsets, in_shape, w, T: int, stride: int = 1, 
         raise ValueError(f"w has {Ci2} input channels, input has {Ci}")
     Ho, Wo = out_extent(Hi, Kh, stride, pad), out_extent(Wi, Kw, stride, pad)
     dev = spikes.device
-    out_times = torch.empty((B, Co, Ho, Wo), dtype=torch.uint8, device=dev)
-    out_vkey = torch.empty((B, Co, Ho, Wo), dtype=torch.float32, device=dev)
+    out_times = _empty((B, Co, Ho, Wo), dtype=torch.uint8, device=dev)
+    out_vkey = _empty((B, Co, Ho, Wo), dtype=torch.float32, device=dev)
     dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
     L = load()
     nbytes = L.spk_conv_fire_sparse_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, dt)
@@ -472,7 +493,7 @@ def spk_log_filter(img, stds, ksize: int, pad: int = -1):
     n = len(stds)
     Ho = H if pad < 0 else H + 2 * pad - ksize + 1
     Wo = W if pad < 0 else W + 2 * pad - ksize + 1
-    out = torch.empty((B, C * 2 * n, Ho, Wo), dtype=torch.float32, device=img.device)
+    out = _empty((B, C * 2 * n, Ho, Wo), dtype=torch.float32, device=img.device)
     arr = (ctypes.c_float * n)(*[float(s) for s in stds])
     _check(load().spk_log_filter(_ptr(img), B, C, H, W, arr, n, ksize, pad, _ptr(out),
                                  _stream(img.device)))
@@ -501,7 +522,7 @@ def spk_quantize(w, lower: float, mid: float, upper: float, w_f16=None):
 def spk_gather(times, T: int):
     """Feature values of a time map: float32, T - t where fired, else 0."""
     _dev(times, torch.uint8, "times")
-    out = torch.empty(times.shape, dtype=torch.float32, device=times.device)
+    out = _empty(times.shape, dtype=torch.float32, device=times.device)
     _check(load().spk_gather(_ptr(times), times.numel(), T, _ptr(out), _stream(times.device)))
     return out
 
@@ -516,7 +537,7 @@ def spk_rate_code(x, u, T: int, min_value: float = 0.01):
     n = x[0].numel()
     if tuple(u.shape) != (B, T) + tuple(x.shape[1:]):
         raise ValueError("u must be B x T x (the shape of one sample of x)")
-    frames = torch.empty(u.shape, dtype=torch.uint8, device=x.device)
+    frames = _empty(u.shape, dtype=torch.uint8, device=x.device)
     ws = _workspace(4 * B, x.device)
     _check(load().spk_rate_code(_ptr(x), _ptr(u), B, n, T, float(min_value), _ptr(frames), _ptr(ws),
                                 4 * B, _stream(x.device)))
@@ -535,8 +556,8 @@ def spk_conv_if_rate(frames, w, stride: int = 1, pad: int = 0, theta: float = 1.
         raise ValueError(f"w has {Ci2} input channels, frames have {Ci}")
     Ho, Wo = out_extent(Hi, Kh, stride, pad), out_extent(Wi, Kw, stride, pad)
     dev = frames.device
-    out = torch.empty((B, T, Co, Ho, Wo), dtype=torch.uint8, device=dev)
-    counts = torch.empty((B, Co, Ho, Wo), dtype=torch.int32, device=dev)
+    out = _empty((B, T, Co, Ho, Wo), dtype=torch.uint8, device=dev)
+    counts = _empty((B, Co, Ho, Wo), dtype=torch.int32, device=dev)
     dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
     L = load()
     nbytes = L.spk_conv_if_rate_workspace_size(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, dt)
@@ -553,8 +574,8 @@ def spk_rate_pool(frames, counts, k, stride=None, pad: int = 0):
     kh, kw = (k, k) if isinstance(k, int) else k
     stride = kh if stride is None else stride
     Ho, Wo = out_extent(Hi, kh, stride, pad), out_extent(Wi, kw, stride, pad)
-    out = torch.empty((B, T, C, Ho, Wo), dtype=torch.uint8, device=frames.device)
-    oc = torch.empty((B, C, Ho, Wo), dtype=torch.int32, device=frames.device)
+    out = _empty((B, T, C, Ho, Wo), dtype=torch.uint8, device=frames.device)
+    oc = _empty((B, C, Ho, Wo), dtype=torch.int32, device=frames.device)
     _check(load().spk_rate_pool(_ptr(frames), _ptr(counts), B, T, C, Hi, Wi, kh, kw, stride, pad,
                                 _ptr(out), _ptr(oc), _stream(frames.device)))
     return out, oc
@@ -562,7 +583,7 @@ def spk_rate_pool(frames, counts, k, stride=None, pad: int = 0):
 
 def spk_rate_features(counts, T: int):
     _dev(counts, torch.int32, "counts")
-    out = torch.empty(counts.shape, dtype=torch.float32, device=counts.device)
+    out = _empty(counts.shape, dtype=torch.float32, device=counts.device)
     _check(load().spk_rate_features(_ptr(counts), counts.numel(), T, _ptr(out), _stream(counts.device)))
     return out
 
@@ -573,8 +594,8 @@ def spk_fire(potentials, theta: float):
     B, T = potentials.shape[:2]
     n = potentials[0, 0].numel()
     shape = (B,) + tuple(potentials.shape[2:])
-    out_t = torch.empty(shape, dtype=torch.uint8, device=potentials.device)
-    out_v = torch.empty(shape, dtype=torch.float32, device=potentials.device)
+    out_t = _empty(shape, dtype=torch.uint8, device=potentials.device)
+    out_v = _empty(shape, dtype=torch.float32, device=potentials.device)
     _check(load().spk_fire(_ptr(potentials), B, T, n, float(theta), _ptr(out_t), _ptr(out_v),
                            _stream(potentials.device)))
     return out_t, out_v
@@ -586,7 +607,7 @@ def spk_inhibit(times, vkey, out=None):
     _dev(vkey, torch.float32, "vkey", 4)
     B, C, H, W = times.shape
     if out is None:
-        out = torch.empty_like(times)
+        out = _empty(times.shape, dtype=times.dtype, device=times.device)
     _dev(out, torch.uint8, "out", 4)
     _check(load().spk_inhibit(_ptr(times), _ptr(vkey), B, C, H, W, _ptr(out), _stream(times.device)))
     return out

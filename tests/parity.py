@@ -37,7 +37,7 @@ def excused_from_potentials(V, theta):
 def check_potentials(got, ref, what="potentials"):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
-    bad = np.abs(got - ref) > V_REL * np.abs(ref) + V_ABS
+    bad = ~(np.abs(got - ref) <= V_REL * np.abs(ref) + V_ABS)  # NaN (an unwritten sentinel) is bad
     assert not bad.any(), (f"{what}: {bad.sum()} of {bad.size} outside tolerance, e.g. "
                            f"{got[bad][:5]} vs {ref[bad][:5]}")
 

@@ -134,6 +134,8 @@ CONV_CASES = [
     (2, 3, 21, 19, 40, 3, 1, 0, 16, 1.5, 0.3, "f16"),       # unaligned channels, half weights, T = 16
     (2, 112, 6, 6, 40, 3, 1, 1, 12, 60.0, 0.3, "f16"),      # 1008 taps: exactly 32 subtiles of 32
     (3, 1000, 1, 1, 65, 1, 1, 0, 30, 60.0, 0.2, "f32"),     # 1 x 1 kernel over 1000 channels (an FC layer)
+    (32, 30, 14, 14, 250, 3, 1, 1, 15, 10.0, 0.85, "f32"),  # the three-layer net's conv2 at B = 32: more
+                                                            # than 64 positions per block range
 ]
 
 

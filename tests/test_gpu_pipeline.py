@@ -2,46 +2,79 @@
 
 Every stage of the GPU step is checked against the oracle run on the inputs
 that stage received on the GPU (stage isolation), so a neuron that sits on its
-threshold cannot cascade into later stages.  Reduced batches are compared in
-full; the full-size steps compare DoG, codes, pooling, winners and weights in
-full and the convolutions on sampled neurons.
+threshold cannot cascade into later stages.  Every output is compared in full,
+at reduced batches and at each workload's real batch; the outputs the binding
+allocates start filled with sentinels (see conftest.py), so one a kernel leaves
+unwritten fails.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from parity import (NEVER, W_ABS, check_fire, check_potentials, excused_from_potentials, gpu,
-                    np_, winners_list)
+from parity import (NEVER, V_ABS, V_REL, W_ABS, check_fire, check_potentials,
+                    excused_from_potentials, gpu, np_, winners_list)
 from paper_2301_13659_amd import spk, workloads
 from paper_2301_13659_amd.pipeline import Pipeline
 
 pytestmark = pytest.mark.gpu
 
 
-def _sample_neurons(tf, rng, n):
-    """Random neurons plus neurons that fired (the interesting ones)."""
-    shape = tf.shape
-    idx = [tuple(int(v) for v in np.unravel_index(i, shape))
-           for i in rng.choice(tf.size, size=min(n, tf.size), replace=False)]
-    fired = np.argwhere(tf != NEVER)
-    if len(fired):
-        pick = rng.choice(len(fired), size=min(n // 2, len(fired)), replace=False)
-        idx += [tuple(int(v) for v in fired[i]) for i in pick]
-    return idx
+def _oracle_conv_spikes(t_in, w, spec, T):
+    """The oracle's event form of the layer (every arrival's weights scattered
+    into the change of potential at its step, then the running sum over the
+    steps and the first crossing), run over every sample.  Samples are
+    independent: chunks of them run on threads (the C calls release the GIL)."""
+    B = t_in.shape[0]
+    nthreads = max(1, min(16, os.cpu_count() or 1, B))
+    chunks = [c for c in np.array_split(np.arange(B), nthreads) if len(c)]
+
+    def run(idx):
+        x = np.ascontiguousarray(t_in[idx[0]:idx[-1] + 1])
+        sp, off = oracle.times_to_spikes(x, T)
+        return oracle.conv_fire_spikes(sp, off, x.shape[1:], w, T, spec.stride, spec.pad, spec.theta)
+
+    with ThreadPoolExecutor(len(chunks)) as ex:
+        res = list(ex.map(run, chunks))
+    return np.concatenate([r[0] for r in res]), np.concatenate([r[1] for r in res])
 
 
-def _check_conv_sampled(t_in, w, spec, T, g_tf, g_vk, rng, n=300):
-    for (b, o, y, x) in _sample_neurons(g_tf, rng, n):
-        V = oracle.conv_neuron(t_in, w, T, spec.stride, spec.pad, b, o, y, x)
-        tf, vk = oracle.fire_neuron(V, spec.theta)
-        excused = np.isfinite(spec.theta) and np.any(np.abs(V - spec.theta) <= 1e-4 * abs(spec.theta))
-        if not excused:
-            assert g_tf[b, o, y, x] == tf, (b, o, y, x, g_tf[b, o, y, x], tf)
-            check_potentials(np.array([g_vk[b, o, y, x]]), np.array([vk]), "v_key")
+def _check_conv_full(t_in, w, spec, T, g_tf, g_vk):
+    """Every output neuron of the layer against the oracle.  A neuron whose
+    time or V_key disagrees is looked at on its own: it is excused only if its
+    oracle potential comes within 1e-4 |theta| of theta at some step.
+    Half-weight layers (multiples of 2^-11 summing below 2^13: exact in any
+    order) must match bit for bit.  Returns the number of excused neurons."""
+    assert np.all((g_tf < T) | (g_tf == NEVER)), "spike times outside [0, T) that are not NEVER"
+    assert np.all(np.isfinite(g_vk)), "non-finite V_key (an output left unwritten?)"
+    o_tf, o_vk = _oracle_conv_spikes(t_in, w, spec, T)
+    if spec.w_dtype == "f16":
+        np.testing.assert_array_equal(g_tf, o_tf)
+        np.testing.assert_array_equal(g_vk, o_vk)
+        return 0
+    if not np.isfinite(spec.theta):
+        assert np.all(g_tf == NEVER)
+        check_potentials(g_vk, o_vk, "readout v_key")
+        return 0
+    vbad = ~(np.abs(g_vk.astype(np.float64) - o_vk) <= V_REL * np.abs(o_vk.astype(np.float64)) + V_ABS)
+    mism = np.argwhere((g_tf != o_tf) | vbad)
+    assert len(mism) <= max(50, g_tf.size // 1000), f"{len(mism)} of {g_tf.size} neurons disagree"
+    for (b, o, y, x) in mism:
+        V = oracle.conv_neuron(t_in, w, T, spec.stride, spec.pad, int(b), int(o), int(y), int(x))
+        excused = np.any(np.abs(V - spec.theta) <= 1e-4 * abs(spec.theta))
+        assert excused, ((b, o, y, x), int(g_tf[b, o, y, x]), int(o_tf[b, o, y, x]),
+                         float(g_vk[b, o, y, x]), float(o_vk[b, o, y, x]))
+    return len(mism)
 
 
-def _run_and_check(wl, full_conv: bool, density_index: int = 1, samples_seen: int = 0):
+def _run_and_check(wl, dense_oracle: bool, density_index: int = 1, samples_seen: int = 0):
+    """One step of the workload, every stage against the oracle on the inputs
+    that stage received.  dense_oracle: the conv oracle also computes every
+    potential of every step (small batches); otherwise its event form checks
+    every output neuron."""
     dev = gpu()
     pipe = Pipeline(wl, dev, density_index=density_index)
     pipe.samples_seen = samples_seen
@@ -49,7 +82,6 @@ def _run_and_check(wl, full_conv: bool, density_index: int = 1, samples_seen: in
     master_before = [np_(l.w).copy() for l in pipe.layers]
     out = pipe.step(keep=True)
     torch.cuda.synchronize()
-    rng = np.random.default_rng(wl.index)
     filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
     if wl.log_stds:
         filters = oracle.log_filters(wl.log_stds, wl.log_ksize)
@@ -76,12 +108,12 @@ def _run_and_check(wl, full_conv: bool, density_index: int = 1, samples_seen: in
             continue
         t_in = np_(out.layer_in[li])
         g_tf, g_vk = (np_(a) for a in out.layer_out[li])
-        if full_conv:
+        if dense_oracle:
             o_tf, o_vk, o_V = oracle.conv_fire(t_in, w_before[li], wl.T, s.stride, s.pad, s.theta,
                                                potentials=True)
             excused_total += check_fire(g_tf, g_vk, o_tf, o_vk, excused_from_potentials(o_V, s.theta))
         else:
-            _check_conv_sampled(t_in, w_before[li], s, wl.T, g_tf, g_vk, rng)
+            excused_total += _check_conv_full(t_in, w_before[li], s, wl.T, g_tf, g_vk)
         if li in out.winners:
             win, n = out.winners[li]
             g_win, g_n = spk.winners_numpy(win), np_(n)
@@ -110,7 +142,7 @@ def _run_and_check(wl, full_conv: bool, density_index: int = 1, samples_seen: in
 @pytest.mark.parametrize("cfg,batch", [(1, 8), (2, 2), (3, 3), (4, 1)])
 def test_workload_step_reduced_batch(cfg, batch):
     wl = workloads.get(cfg).with_batch(batch)
-    excused = _run_and_check(wl, full_conv=True)
+    excused = _run_and_check(wl, dense_oracle=True)
     assert excused <= 5
 
 
@@ -119,7 +151,7 @@ def test_demo_step_reduced_batch(samples_seen):
     """The paper's example network: LoG bank, threshold, two learning layers
     with the learning-rate schedule at three points of training, gather."""
     wl = workloads.get(6).with_batch(2)
-    _run_and_check(wl, full_conv=True, samples_seen=samples_seen)
+    _run_and_check(wl, dense_oracle=True, samples_seen=samples_seen)
 
 
 def test_demo_quantize_after_training():
@@ -135,13 +167,25 @@ def test_demo_quantize_after_training():
 @pytest.mark.parametrize("density_index", [0, 1, 2])
 def test_cfg5_step_reduced_batch(density_index):
     wl = workloads.get(5).with_batch(1)
-    _run_and_check(wl, full_conv=False, density_index=density_index)
+    assert _run_and_check(wl, dense_oracle=False, density_index=density_index) == 0
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 6])
 def test_workload_step_full_size(cfg):
+    """Every workload at its real batch, in the launch configuration bench.py
+    times: every output neuron of every conv layer against the oracle."""
     wl = workloads.get(cfg)
-    _run_and_check(wl, full_conv=(cfg == 1), density_index=1)
+    excused = _run_and_check(wl, dense_oracle=(cfg == 1), density_index=1)
+    assert excused <= 200
+
+
+@pytest.mark.parametrize("density_index", [0, 1, 2])
+def test_cfg5_step_full_size(density_index):
+    """The spike-input layer at B = 128 and each input density: its half
+    weights are multiples of 2^-11 with sums below 2^13, exact in any order,
+    so every neuron must agree with the oracle bit for bit."""
+    wl = workloads.get(5)
+    assert _run_and_check(wl, dense_oracle=False, density_index=density_index) == 0
 
 
 def test_step_is_deterministic():
@@ -155,6 +199,11 @@ def test_step_is_deterministic():
         outs.append((np_(o.times0), [np_(a[0]) for a in o.layer_out], [np_(a[1]) for a in o.layer_out],
                      [np_(l.w) for l in pipe.layers]))
     a, b = outs
+    # the outputs were allocated filled with sentinels (NaN, 0xAB bytes): none may remain
+    for tf in a[1]:
+        assert np.all((tf < wl.T) | (tf == NEVER))
+    for v in a[2] + a[3]:
+        assert np.all(np.isfinite(v))
     np.testing.assert_array_equal(a[0], b[0])
     for x, y in zip(a[1] + a[2] + a[3], b[1] + b[2] + b[3]):
         np.testing.assert_array_equal(x, y)
