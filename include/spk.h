@@ -170,6 +170,32 @@ spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int Hi, 
                          void *ws, size_t ws_bytes, spk_stream stream);
 
 /*
+ * spk_conv_fire_noalloc -- spk_conv_fire for callers that cannot allocate
+ * device memory (code under stream capture, serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, results and errors as spk_conv_fire,
+ * without the workspace: its scratch is a static device array of
+ * SPK_CONV_FIRE_NOALLOC_MAX_BYTES that the library holds on each GPU it runs
+ * on until the process ends.  The call allocates and frees nothing.
+ *  - Layers whose spk_conv_fire_workspace_size exceeds the maximum are
+ *    rejected with SPK_E_WORKSPACE before anything is launched (64 MiB covers
+ *    every layer of the workloads here; the largest, a 200-map 5x5 readout
+ *    over 250 x 5 x 5 at batch 256, needs 44.5 MiB).
+ *  - The scratch of the current device is used: `stream` must belong to it.
+ *    Its address is looked up on the first call on each device
+ *    (hipGetSymbolAddress); a failure there is SPK_E_HIP.
+ *  - Every call on one GPU shares that GPU's array: calls that overlap in
+ *    time on one GPU (on different streams, or from several host threads
+ *    without ordering) race and may corrupt each other's results.  Calls
+ *    ordered on one stream are safe.
+ */
+#define SPK_CONV_FIRE_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+spk_status spk_conv_fire_noalloc(const uint8_t *in_times, int B, int T, int Ci, int Hi, int Wi,
+                                 const void *w, spk_dtype w_dtype, int Co, int Kh, int Kw,
+                                 int stride, int pad, float theta,
+                                 uint8_t *out_times, float *out_vkey, float *potentials,
+                                 spk_stream stream);
+
+/*
  * spk_pool -- max-pooling of spikes under rank-order coding, §II-E.3 (Eq. 3
  * for the size): each output keeps the earliest spike of its Kh x Kw window,
  * i.e. the minimum input time; window cells in the padding never fire.

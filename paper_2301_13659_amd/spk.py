@@ -56,6 +56,8 @@ _SIGNATURES = {
     "spk_conv_fire_workspace_size": ([_I] * 10 + [_F, _I], _Z),
     "spk_conv_fire": ([_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P,
                        _Z, _P], _I),
+    "spk_conv_fire_noalloc": ([_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P,
+                               _P], _I),
     "spk_pool": ([_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P], _I),
     "spk_inhibit_winners_workspace_size": ([_I, _I, _I, _I], _Z),
     "spk_inhibit_winners": ([_P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _Z, _P],
@@ -242,6 +244,35 @@ def spk_conv_fire(in_times, w, T: int, stride: int = 1, pad: int = 0, theta: flo
                            float(theta), _ptr(out_times), _ptr(out_vkey), _ptr(V), _ptr(ws), nbytes,
                            _stream(dev)))
     return (out_times, out_vkey, V) if V is not None else (out_times, out_vkey)
+
+
+def spk_conv_fire_noalloc(in_times, w, T: int, stride: int = 1, pad: int = 0,
+                          theta: float = math.inf, out_times=None, out_vkey=None):
+    """spk_conv_fire with the library's static scratch instead of a workspace
+    (for callers that cannot allocate): pass preallocated outputs to keep the
+    call free of allocations."""
+    _dev(in_times, torch.uint8, "in_times", 4)
+    if w.dtype not in (torch.float32, torch.float16):
+        raise ValueError("w: expected float32 or float16")
+    _dev(w, w.dtype, "w", 4)
+    B, Ci, Hi, Wi = in_times.shape
+    Co, Ci2, Kh, Kw = w.shape
+    if Ci != Ci2:
+        raise ValueError(f"w has {Ci2} input channels, input has {Ci}")
+    L = load()
+    Ho, Wo = L.spk_out_extent(Hi, Kh, stride, pad), L.spk_out_extent(Wi, Kw, stride, pad)
+    dev = in_times.device
+    if out_times is None:
+        out_times = _empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.uint8, device=dev)
+    if out_vkey is None:
+        out_vkey = _empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.float32, device=dev)
+    _dev(out_times, torch.uint8, "out_times", 4)
+    _dev(out_vkey, torch.float32, "out_vkey", 4)
+    dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
+    _check(L.spk_conv_fire_noalloc(_ptr(in_times), B, T, Ci, Hi, Wi, _ptr(w), dt, Co, Kh, Kw, stride,
+                                   pad, float(theta), _ptr(out_times), _ptr(out_vkey), None,
+                                   _stream(dev)))
+    return out_times, out_vkey
 
 
 def spk_pool(in_times, k, stride: int | None = None, pad: int = 0, out=None):

@@ -219,3 +219,13 @@ def test_misaligned_workspace_is_rejected():
          spk.SPK_E_ARG, "aligned")
     _err(L.spk_rate_code(P1, P1, 2, 10, 5, 0.0, P1, bad, 1 << 20, None), spk.SPK_E_ARG, "aligned")
 
+
+
+def test_conv_fire_noalloc_rejects_layers_beyond_its_scratch():
+    """The no-allocation conv checks the layer's scratch need against its
+    static maximum before it touches the device."""
+    L = spk.load()
+    # the spike-input layer at batch 1024 needs about 275 MiB of scratch
+    st = L.spk_conv_fire_noalloc(P1, 1024, 30, 64, 64, 64, P1, spk.SPK_F16, 128, 3, 3, 1, 1, 20.0,
+                                 P1, P1, None, None)
+    _err(st, spk.SPK_E_WORKSPACE, "static")
