@@ -306,10 +306,11 @@ __device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words,
 // its 16 times fire within the window (clamped times: any byte below T)?
 // Returns, uniform over the wave, whether the range [0, nw) is sparse enough
 // to test slices in: a tile's slice can be skipped only when none of the
-// tile's pt positions has a firing input in it, so with a fraction u of the
-// wave's words unflagged about u^pt of the slices are skipped; testing pays
-// when that is above 40 % (below it the tests cost more than the skipped
-// products save).
+// tile's words under it fires, so with a fraction u of the wave's words
+// unflagged about u^pt of the slices are skipped, pt being the words a
+// slice of the tile covers (one per position when window runs are 16-byte
+// aligned, two otherwise); testing pays when that is above 40 % (below it the
+// tests cost more than the skipped products save).
 __device__ __forceinline__ bool store_range(const Staged &st, uint8_t *hal, uint8_t *flags,
                                             uint32_t never4, int nw, int hw, int pt)
 {
@@ -461,13 +462,16 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
     const h2 cc = as_h2(cbv | (cbv << 16));
     const int PT = 32 >> lgTP;  // positions per tile
     const uint32_t never4 = 0x01010101u * (uint32_t)g.T;
+    // words a slice of the tile covers (see store_range)
+    const int skip_pow = PT * ((g.Cp & 15) == 0 ? 1 : 2);
 
     bool sparse;
     {
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw, PT);
+        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw,
+                             skip_pow);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -556,7 +560,9 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
                 for (int s = 0; s < SK; s++) {
                     const u4 x = win[s % kAhead];
                     if (s + kAhead < SK) win[s % kAhead] = rd(s + kAhead);
-                    if (__builtin_expect((live >> s) & 1ull, 1)) step(s, x);
+                    // (the bit test on a 32-bit half is one scalar instruction)
+                    const uint32_t lw = s < 32 ? (uint32_t)live : (uint32_t)(live >> 32);
+                    if (__builtin_expect((lw >> (s & 31)) & 1u, 1)) step(s, x);
                 }
             }
             // the next tile's window origin, read while this one finishes
@@ -580,7 +586,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            sparse = store_range(nxt, hal, flags, never4, nxt_words, g.hw, PT);
+            sparse = store_range(nxt, hal, flags, never4, nxt_words, g.hw, skip_pow);
         }
     }
     __syncthreads();  // the last group is staged
