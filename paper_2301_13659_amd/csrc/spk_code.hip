@@ -14,9 +14,11 @@
 //    the rest.  Samples with a crowded bucket are sorted instead: every
 //    thread sorts 8 keys in registers, then merge levels in LDS merge the
 //    runs (no padding to a power of two).
-//  - Larger samples: workgroups sort kSmall-key chunks in LDS, then merge
-//    passes double the sorted runs (merge-path split per thread) until each
-//    sample is one run; the ping-pong buffers live in the caller workspace.
+//  - Larger samples: no sort.  Only the keys at the T - 1 ranks where the
+//    step changes are needed; they are selected with a histogram of the top
+//    key bits and a radix selection inside the buckets that hold them, and
+//    every value then counts the boundary keys at or below its own (see
+//    below).  The working arrays live in the caller workspace.
 #include <cstring>
 
 #include "spk_internal.h"
@@ -25,7 +27,6 @@ namespace {
 
 constexpr int kSmall = 8192;    // keys per LDS sort (2 x 64 KB)
 constexpr int kThreads = 1024;
-constexpr int kMergePerThread = 8;
 constexpr uint64_t kDead = ~0ull;
 
 __device__ __forceinline__ uint32_t order_desc(float v)
@@ -97,30 +98,6 @@ __device__ __forceinline__ void sort8(uint64_t *k)
     cswap(k[0], k[4]); cswap(k[1], k[5]); cswap(k[2], k[6]); cswap(k[3], k[7]);
     cswap(k[2], k[4]); cswap(k[3], k[5]);
     cswap(k[1], k[2]); cswap(k[3], k[4]); cswap(k[5], k[6]);
-}
-
-// Merge runs of `width` sorted keys pairwise (src -> dst, n keys); thread t
-// produces outputs [8t, 8t + 8) from a merge-path split.
-__device__ void merge_level(const uint64_t *src, uint64_t *dst, int n, int width)
-{
-    const int first = threadIdx.x * 8;
-    if (first >= n) return;
-    const int lo = (first / (2 * width)) * 2 * width;
-    const int na = min(width, n - lo), nb = max(0, min(width, n - lo - width));
-    const uint64_t *A = src + lo, *Bv = src + lo + na;
-    const int p = first - lo;
-    int ilo = max(0, p - nb), ihi = min(p, na);
-    while (ilo < ihi) {
-        const int i = (ilo + ihi) >> 1;
-        if (A[i] < Bv[p - i - 1]) ilo = i + 1;
-        else ihi = i;
-    }
-    int i = ilo, j = p - ilo;
-    const int end = min(p + 8, na + nb);
-    for (int q = p; q < end; q++) {
-        const bool takeA = (j >= nb) || (i < na && A[i] < Bv[j]);
-        dst[lo + q] = takeA ? A[i++] : Bv[j++];
-    }
 }
 
 // Merge runs of `width` sorted keys pairwise (src -> dst, n keys), one key
@@ -283,99 +260,276 @@ __global__ __launch_bounds__(kThreads) void k_code_bucket(const float *__restric
     }
 }
 
-// Large samples, step 1: keys, never-firing outputs, eligible counts.
-__global__ void k_code_keys(const float *__restrict__ x, int B, int n, float min_value,
-                            uint64_t *__restrict__ keys, uint8_t *__restrict__ times,
-                            int *__restrict__ count)
-{
-    __shared__ int red[256 / 64];
-    const int b = blockIdx.y;
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    int mine = 0;
-    if (i < n) {
-        uint64_t key = make_key(x[(size_t)b * n + i], min_value, (uint32_t)i);
-        keys[(size_t)b * n + i] = key;
-        if (key == kDead) times[(size_t)b * n + i] = spk::kNever;
-        else mine = 1;
-    }
-    int tot = block_sum(mine, red);
-    if (threadIdx.x == 0 && tot) atomicAdd(&count[b], tot);
-}
+// ------------------------------------------------------------------------
+// Samples of more than kSmall values.  A value's step depends on its rank r
+// only through floor(r*T/N): with R_k = ceil(k*N/T), t >= k exactly when
+// r >= R_k.  So only the T - 1 keys at ranks R_k (the boundaries between
+// steps) are needed, not a sort: t = the number of boundary keys at or below
+// the value's key.  The boundaries are found by selection:
+//  1. a histogram of the top 16 bits of the keys (the sign, exponent and 7
+//     mantissa bits of the value word) per sample;
+//  2. its prefix sum gives the bucket holding each R_k and the boundary's
+//     rank inside that bucket;
+//  3. the keys of those buckets are gathered into lists;
+//  4. per boundary, a radix select (8-bit digits over the remaining 48 key
+//     bits) finds the key of that rank in its bucket's list;
+//  5. every value counts the boundary keys at or below its own.
+// Work is a few passes over the values plus the keys of T - 1 buckets,
+// whatever the sample size; equal values only make a bucket larger.
+constexpr int kHB = 65536;  // histogram buckets (top 16 key bits)
+constexpr int kCl = 8;      // values per thread in the streaming passes
+constexpr int kClT = 256;   // threads of the streaming passes
+constexpr int kMaxB = SPK_MAX_T;  // boundaries per sample (T - 1 <= 253)
 
-__global__ void k_zero_int(int *p, int n)
+struct ClBound {   // one boundary k of one sample
+    int bucket;    // -1: R_k >= N, the boundary is past every key
+    int local;     // its rank inside the bucket
+    int list;      // index of the bucket's list in the sample's table
+};
+
+struct ClList {    // one distinct boundary bucket of a sample
+    int bucket, offset, size;
+};
+
+// 0. clear the histograms and counts (B x kHB + B) and the list fill counters
+__global__ void k_cl_zero(int *__restrict__ p, long long n)
 {
-    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = 0;
 }
 
-// Large samples, step 2: sort kSmall-key chunks (register sort of 8, then
-// merge levels in LDS).
-__global__ __launch_bounds__(kThreads) void k_code_chunks(uint64_t *__restrict__ keys, int n)
+// 1. histogram of the eligible keys' top 16 bits, and the eligible count
+__global__ __launch_bounds__(kClT) void k_cl_hist(const float *__restrict__ x, int n, float min_value,
+                                                  int *__restrict__ hist, int *__restrict__ count)
 {
-    extern __shared__ uint64_t s[];  // two buffers of kSmall keys
+    __shared__ int red[kClT / 64];
     const int b = blockIdx.y;
-    const int base = blockIdx.x * kSmall;
-    const int len = min(kSmall, n - base);
-    uint64_t *g = keys + (size_t)b * n + base;
-    uint64_t k8[8];
-    const int first = threadIdx.x * 8;
+    const float *xs = x + (size_t)b * n;
+    int *h = hist + (size_t)b * kHB;
+    const int base = blockIdx.x * kClT * kCl + threadIdx.x;
+    float v[kCl];
 #pragma unroll
-    for (int j = 0; j < 8; j++) k8[j] = (first + j < len) ? g[first + j] : kDead;
-    sort8(k8);
-    uint64_t *src = s, *dst = s + kSmall;
+    for (int j = 0; j < kCl; j++) v[j] = xs[min(base + kClT * j, n - 1)];
+    int mine = 0;
 #pragma unroll
-    for (int j = 0; j < 8; j++)
-        if (first + j < len) src[first + j] = k8[j];
-    __syncthreads();
-    for (int width = 8; width < len; width *= 2) {
-        merge_level(src, dst, len, width);
-        __syncthreads();
-        uint64_t *t = src;
-        src = dst;
-        dst = t;
+    for (int j = 0; j < kCl; j++) {
+        if (base + kClT * j < n && v[j] > min_value) {
+            atomicAdd(&h[order_desc(v[j]) >> 16], 1);
+            mine++;
+        }
     }
-    for (int i = threadIdx.x; i < len; i += blockDim.x) g[i] = src[i];
+    const int tot = block_sum(mine, red);
+    if (threadIdx.x == 0 && tot) atomicAdd(&count[b], tot);
 }
 
-// Large samples, step 3: merge sorted runs of `width` pairwise, src -> dst.
-__global__ void k_code_merge(const uint64_t *__restrict__ src, uint64_t *__restrict__ dst, int n,
-                             int width)
+// 2. one block per sample: prefix sum of the histogram, the bucket and local
+// rank of every boundary, and the table of distinct boundary buckets (with
+// their list offsets inside the sample's list area and a membership bitmap).
+// The histogram is scanned in chunks of 4 * blockDim buckets, each thread
+// reading 4 consecutive counts (one 16-byte load, coalesced over the block).
+__global__ __launch_bounds__(kThreads) void k_cl_bounds(const int *__restrict__ hist,
+                                                        const int *__restrict__ count, int T,
+                                                        ClBound *__restrict__ bnd, ClList *__restrict__ lists,
+                                                        int *__restrict__ nlists, uint32_t *__restrict__ bitmap,
+                                                        int *__restrict__ fill)
 {
-    const int b = blockIdx.y;
-    const long long first = ((long long)blockIdx.x * blockDim.x + threadIdx.x) * kMergePerThread;
-    if (first >= n) return;
-    const uint64_t *S = src + (size_t)b * n;
-    uint64_t *D = dst + (size_t)b * n;
-    const int lo = (int)(first / (2LL * width)) * 2 * width;
-    const int na = min(width, n - lo);
-    const int nb = max(0, min(width, n - lo - width));
-    const uint64_t *A = S + lo, *Bv = S + lo + na;
-    const int p = (int)first - lo;
-    // co-rank: number i of A keys among the first p merged keys
-    int ilo = max(0, p - nb), ihi = min(p, na);
-    while (ilo < ihi) {
-        int i = (ilo + ihi) >> 1;
-        if (A[i] < Bv[p - i - 1]) ilo = i + 1;
-        else ihi = i;
-    }
-    int i = ilo, j = p - ilo;
-    const int end = min(p + kMergePerThread, na + nb);
-    for (int q = p; q < end; q++) {
-        bool takeA = (j >= nb) || (i < na && A[i] < Bv[j]);
-        D[lo + q] = takeA ? A[i++] : Bv[j++];
-    }
-}
-
-// Large samples, step 4: rank -> time.
-__global__ void k_code_scatter(const uint64_t *__restrict__ keys, int n, int T,
-                               const int *__restrict__ count, uint8_t *__restrict__ times)
-{
-    const int b = blockIdx.y;
-    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    constexpr int kChunk = 4 * kThreads;
+    __shared__ int red[kThreads / 64];
+    __shared__ int s_bucket[kMaxB], s_local[kMaxB];
+    const int b = blockIdx.x;
+    const int *h = hist + (size_t)b * kHB;
     const int N = count[b];
-    if (r >= N) return;
-    uint32_t idx = (uint32_t)keys[(size_t)b * n + r];
-    times[(size_t)b * n + idx] = (uint8_t)(((long long)r * T) / N);
+    uint32_t *bm = bitmap + (size_t)b * (kHB / 32);
+    for (int i = threadIdx.x; i < kHB / 32; i += kThreads) bm[i] = 0u;
+    for (int k = threadIdx.x; k < T - 1; k += kThreads) {
+        s_bucket[k] = -1;  // R_k >= N: past every key
+        s_local[k] = 0;
+    }
+    int chunk_base = 0;  // keys in the chunks before
+    for (int c0 = 0; c0 < kHB; c0 += kChunk) {
+        const int4 c4 = reinterpret_cast<const int4 *>(h + c0)[threadIdx.x];
+        const int c[4] = {c4.x, c4.y, c4.z, c4.w};
+        const int sum = c[0] + c[1] + c[2] + c[3];
+        int total;
+        const int start = chunk_base + block_exclusive_scan(sum, red, total);  // has barriers
+        // each boundary rank R_k in this thread's four buckets
+        if (sum > 0) {
+            // k with start <= R_k < start + sum, R_k = ceil(k N / T): the
+            // first has k > T (start - 1) / N
+            const int k0 = max(1, (int)((long long)(start - 1) * T / N));
+            for (int k = k0; k < T; k++) {
+                const long long R = ((long long)k * N + T - 1) / T;
+                if (R >= (long long)start + sum) break;
+                if (R < start) continue;
+                int at = start;
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    if (R >= at && R < at + c[q]) {
+                        s_bucket[k - 1] = c0 + 4 * threadIdx.x + q;
+                        s_local[k - 1] = (int)(R - at);
+                    }
+                    at += c[q];
+                }
+            }
+        }
+        chunk_base += total;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        // buckets are nondecreasing in k: consecutive equal ones share a list
+        int nl = 0, off = 0, prev = -1;
+        for (int k = 0; k < T - 1; k++) {
+            const int bk = s_bucket[k];
+            ClBound r{bk, s_local[k], -1};
+            if (bk >= 0) {
+                if (bk != prev) {
+                    const int sz = h[bk];
+                    lists[(size_t)b * kMaxB + nl] = ClList{bk, off, sz};
+                    fill[(size_t)b * kMaxB + nl] = 0;
+                    bm[bk >> 5] |= 1u << (bk & 31);
+                    off += sz;
+                    nl++;
+                    prev = bk;
+                }
+                r.list = nl - 1;
+            }
+            bnd[(size_t)b * kMaxB + k] = r;
+        }
+        nlists[b] = nl;
+    }
+}
+
+// 3. the keys of the boundary buckets into their lists (any order)
+__global__ __launch_bounds__(kClT) void k_cl_gather(const float *__restrict__ x, int n, float min_value,
+                                                    const ClList *__restrict__ lists,
+                                                    const int *__restrict__ nlists,
+                                                    const uint32_t *__restrict__ bitmap,
+                                                    int *__restrict__ fill, uint64_t *__restrict__ keys)
+{
+    __shared__ uint32_t bm[kHB / 32];
+    __shared__ int s_bk[kMaxB];
+    const int b = blockIdx.y;
+    const int nl = nlists[b];
+    if (nl == 0) return;  // uniform: no boundary (no eligible value)
+    for (int i = threadIdx.x; i < kHB / 32; i += kClT) bm[i] = bitmap[(size_t)b * (kHB / 32) + i];
+    for (int i = threadIdx.x; i < nl; i += kClT) s_bk[i] = lists[(size_t)b * kMaxB + i].bucket;
+    __syncthreads();
+    const float *xs = x + (size_t)b * n;
+    const int base = blockIdx.x * kClT * kCl + threadIdx.x;
+    float v[kCl];
+#pragma unroll
+    for (int j = 0; j < kCl; j++) v[j] = xs[min(base + kClT * j, n - 1)];
+#pragma unroll
+    for (int j = 0; j < kCl; j++) {
+        const int i = base + kClT * j;
+        if (i >= n || !(v[j] > min_value)) continue;
+        const uint32_t w = order_desc(v[j]);
+        const int bk = (int)(w >> 16);
+        if (!((bm[bk >> 5] >> (bk & 31)) & 1u)) continue;
+        int lo = 0, hi = nl - 1;  // the list of bucket bk (buckets ascend with the list index)
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (s_bk[mid] < bk) lo = mid + 1;
+            else hi = mid;
+        }
+        const ClList L = lists[(size_t)b * kMaxB + lo];
+        const int slot = atomicAdd(&fill[(size_t)b * kMaxB + lo], 1);
+        keys[(size_t)b * n + L.offset + slot] = ((uint64_t)w << 32) | (uint32_t)i;
+    }
+}
+
+// 4. one block per (boundary, sample): the key of rank `local` in its bucket's
+// list, by radix selection over the 48 bits below the bucket's (8-bit digits,
+// most significant first).  Boundaries past every key get the all-ones key.
+__global__ __launch_bounds__(kClT) void k_cl_select(const ClBound *__restrict__ bnd,
+                                                    const ClList *__restrict__ lists,
+                                                    const uint64_t *__restrict__ keys, int n,
+                                                    uint64_t *__restrict__ bkeys)
+{
+    __shared__ int hist[256];
+    __shared__ uint64_t s_prefix;
+    __shared__ int s_rank;
+    const int k = blockIdx.x, b = blockIdx.y;
+    const ClBound r = bnd[(size_t)b * kMaxB + k];
+    if (r.bucket < 0) {
+        if (threadIdx.x == 0) bkeys[(size_t)b * kMaxB + k] = kDead;
+        return;
+    }
+    const ClList L = lists[(size_t)b * kMaxB + r.list];
+    const uint64_t *ks = keys + (size_t)b * n + L.offset;
+    uint64_t prefix = (uint64_t)r.bucket << 48;  // decided bits
+    int rank = r.local;
+    for (int shift = 40; shift >= 0; shift -= 8) {
+        const uint64_t mask = ~0ull << (shift + 8);  // bits decided so far
+        for (int i = threadIdx.x; i < 256; i += kClT) hist[i] = 0;
+        __syncthreads();
+        for (int i = threadIdx.x; i < L.size; i += kClT) {
+            const uint64_t key = ks[i];
+            if ((key & mask) == prefix) atomicAdd(&hist[(int)((key >> shift) & 255u)], 1);
+        }
+        __syncthreads();
+        if (threadIdx.x < 64) {  // one wave: the digit whose run holds the rank
+            int c4[4], s = 0;
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                c4[q] = hist[threadIdx.x * 4 + q];
+                s += c4[q];
+            }
+            int incl = s;
+            for (int o = 1; o < 64; o <<= 1) {
+                const int t = __shfl_up(incl, o, 64);
+                if ((int)threadIdx.x >= o) incl += t;
+            }
+            int at = incl - s;
+            for (int q = 0; q < 4; q++) {
+                if (rank >= at && rank < at + c4[q]) {
+                    s_prefix = prefix | ((uint64_t)(threadIdx.x * 4 + q) << shift);
+                    s_rank = rank - at;
+                }
+                at += c4[q];
+            }
+        }
+        __syncthreads();
+        prefix = s_prefix;
+        rank = s_rank;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) bkeys[(size_t)b * kMaxB + k] = prefix;
+}
+
+// 5. every value's step: the number of boundary keys at or below its key
+// (they ascend with k); values at or below min_value never fire.
+__global__ __launch_bounds__(kClT) void k_cl_final(const float *__restrict__ x, int n, int T,
+                                                   float min_value, const uint64_t *__restrict__ bkeys,
+                                                   uint8_t *__restrict__ times)
+{
+    __shared__ uint64_t bk[kMaxB];
+    const int b = blockIdx.y;
+    for (int i = threadIdx.x; i < T - 1; i += kClT) bk[i] = bkeys[(size_t)b * kMaxB + i];
+    __syncthreads();
+    const float *xs = x + (size_t)b * n;
+    uint8_t *ts = times + (size_t)b * n;
+    const int base = blockIdx.x * kClT * kCl + threadIdx.x;
+    float v[kCl];
+#pragma unroll
+    for (int j = 0; j < kCl; j++) v[j] = xs[min(base + kClT * j, n - 1)];
+#pragma unroll
+    for (int j = 0; j < kCl; j++) {
+        const int i = base + kClT * j;
+        if (i >= n) continue;
+        uint8_t t = spk::kNever;
+        if (v[j] > min_value) {
+            const uint64_t key = ((uint64_t)order_desc(v[j]) << 32) | (uint32_t)i;
+            int lo = 0, hi = T - 1;  // first boundary above the key
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (bk[mid] <= key) lo = mid + 1;
+                else hi = mid;
+            }
+            t = (uint8_t)lo;
+        }
+        ts[i] = t;
+    }
 }
 
 // Linear mode (sort disabled): one workgroup per sample.
@@ -428,25 +582,43 @@ __global__ void k_code_frames(const uint8_t *__restrict__ times, int T, int n,
     frames[((size_t)b * T + t) * n + i] = (uint8_t)(times[(size_t)b * n + i] <= t);
 }
 
-size_t ws_layout(int B, long long n, size_t *off_b, size_t *off_cnt)
+// Workspace of the large-sample path: histograms, counts, boundary records,
+// list tables, bitmaps, fill counters, boundary keys and the lists (at most
+// the sample's values).
+struct ClWs {
+    size_t hist, count, bnd, lists, nlists, bitmap, fill, bkeys, keys, total;
+};
+
+ClWs cl_layout(int B, long long n)
 {
-    if (n <= kSmall) {
-        *off_b = *off_cnt = 0;
-        return 0;
-    }
-    size_t keys = spk::align_up((size_t)B * n * sizeof(uint64_t), 256);
-    *off_b = keys;
-    *off_cnt = 2 * keys;
-    return 2 * keys + spk::align_up((size_t)B * sizeof(int), 256);
+    ClWs w{};
+    size_t at = 0;
+    auto take = [&](size_t bytes) {
+        const size_t here = at;
+        at += spk::align_up(bytes, 256);
+        return here;
+    };
+    w.hist = take((size_t)B * kHB * sizeof(int));
+    w.count = take((size_t)B * sizeof(int));
+    w.bnd = take((size_t)B * kMaxB * sizeof(ClBound));
+    w.lists = take((size_t)B * kMaxB * sizeof(ClList));
+    w.nlists = take((size_t)B * sizeof(int));
+    w.bitmap = take((size_t)B * (kHB / 32) * sizeof(uint32_t));
+    w.fill = take((size_t)B * kMaxB * sizeof(int));
+    w.bkeys = take((size_t)B * kMaxB * sizeof(uint64_t));
+    w.keys = take((size_t)B * n * sizeof(uint64_t));
+    w.total = at;
+    return w;
 }
+
+size_t ws_layout(int B, long long n) { return n <= kSmall ? 0 : cl_layout(B, n).total; }
 
 }  // namespace
 
 extern "C" size_t spk_latency_code_workspace_size(int B, int C, int H, int W)
 {
     if (B <= 0 || C <= 0 || H <= 0 || W <= 0) return 0;
-    size_t a, c;
-    return ws_layout(B, (long long)C * H * W, &a, &c);
+    return ws_layout(B, (long long)C * H * W);
 }
 
 extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int W, int T,
@@ -466,8 +638,7 @@ extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int 
                 "spk_latency_code: sample of %lld values too large", nl);
     SPK_REQUIRE(B <= 65535, SPK_E_SHAPE, "spk_latency_code: B=%d > 65535", B);
     const int n = (int)nl;
-    size_t off_b, off_cnt;
-    const size_t need = mode == SPK_CODE_RANK ? ws_layout(B, n, &off_b, &off_cnt) : 0;
+    const size_t need = mode == SPK_CODE_RANK ? ws_layout(B, n) : 0;
     SPK_REQUIRE(ws_bytes >= need && (need == 0 || ws), SPK_E_WORKSPACE,
                 "spk_latency_code: workspace of %zu bytes needed, %zu given", need, ws_bytes);
     SPK_REQUIRE_WS_ALIGNED(ws, "spk_latency_code");
@@ -484,29 +655,32 @@ extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int 
         hipLaunchKernelGGL(k_code_bucket, dim3(B), dim3(kThreads), lds, s, x, n, T, min_value, times);
         SPK_LAUNCHED("spk_latency_code");
     } else {
-        uint64_t *ka = (uint64_t *)ws;
-        uint64_t *kb = (uint64_t *)((char *)ws + off_b);
-        int *cnt = (int *)((char *)ws + off_cnt);
-        hipLaunchKernelGGL(k_zero_int, dim3(spk::ceil_div(B, 256)), dim3(256), 0, s, cnt, B);
+        const ClWs L = cl_layout(B, n);
+        char *w = (char *)ws;
+        int *hist = (int *)(w + L.hist), *count = (int *)(w + L.count);
+        ClBound *bnd = (ClBound *)(w + L.bnd);
+        ClList *lists = (ClList *)(w + L.lists);
+        int *nlists = (int *)(w + L.nlists), *fill = (int *)(w + L.fill);
+        uint32_t *bitmap = (uint32_t *)(w + L.bitmap);
+        uint64_t *bkeys = (uint64_t *)(w + L.bkeys), *keys = (uint64_t *)(w + L.keys);
+        // histograms and counts are adjacent: one clearing pass
+        const long long nz = (long long)(L.count - L.hist) / 4 + B;
+        hipLaunchKernelGGL(k_cl_zero, dim3(spk::ceil_div(nz, 256)), dim3(256), 0, s, hist, nz);
         SPK_LAUNCHED("spk_latency_code");
-        hipLaunchKernelGGL(k_code_keys, dim3(spk::ceil_div(n, 256), B), dim3(256), 0, s, x, B, n,
-                           min_value, ka, times, cnt);
+        const dim3 sgrid(spk::ceil_div(n, kClT * kCl), B);
+        hipLaunchKernelGGL(k_cl_hist, sgrid, dim3(kClT), 0, s, x, n, min_value, hist, count);
         SPK_LAUNCHED("spk_latency_code");
-        const size_t clds = 2 * (size_t)kSmall * sizeof(uint64_t);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_code_chunks),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)clds);
-        hipLaunchKernelGGL(k_code_chunks, dim3(spk::ceil_div(n, kSmall), B), dim3(kThreads), clds, s,
-                           ka, n);
+        hipLaunchKernelGGL(k_cl_bounds, dim3(B), dim3(kThreads), 0, s, hist, count, T, bnd, lists, nlists,
+                           bitmap, fill);
         SPK_LAUNCHED("spk_latency_code");
-        uint64_t *src = ka, *dst = kb;
-        for (long long width = kSmall; width < n; width *= 2) {
-            dim3 grid(spk::ceil_div(spk::ceil_div(n, kMergePerThread), 256), B);
-            hipLaunchKernelGGL(k_code_merge, grid, dim3(256), 0, s, src, dst, n, (int)width);
+        hipLaunchKernelGGL(k_cl_gather, sgrid, dim3(kClT), 0, s, x, n, min_value, lists, nlists, bitmap,
+                           fill, keys);
+        SPK_LAUNCHED("spk_latency_code");
+        if (T > 1) {
+            hipLaunchKernelGGL(k_cl_select, dim3(T - 1, B), dim3(kClT), 0, s, bnd, lists, keys, n, bkeys);
             SPK_LAUNCHED("spk_latency_code");
-            std::swap(src, dst);
         }
-        hipLaunchKernelGGL(k_code_scatter, dim3(spk::ceil_div(n, 256), B), dim3(256), 0, s, src, n,
-                           T, cnt, times);
+        hipLaunchKernelGGL(k_cl_final, sgrid, dim3(kClT), 0, s, x, n, T, min_value, bkeys, times);
         SPK_LAUNCHED("spk_latency_code");
     }
     if (frames) {

@@ -68,7 +68,8 @@ def test_latency_code_validation_and_workspace():
     _err(L.spk_latency_code(P1, 1, 1, 4, 4, 5, 0.01, 7, P1, None, None, 0, None), spk.SPK_E_ARG, "mode")
     assert L.spk_latency_code_workspace_size(64, 6, 28, 28) == 0           # whole sample in LDS
     need = L.spk_latency_code_workspace_size(32, 6, 160, 250)
-    assert need >= 2 * 32 * 6 * 160 * 250 * 8
+    # the bucket lists (up to one key per value) and a 65536-bucket histogram per sample
+    assert need >= 32 * 6 * 160 * 250 * 8 + 32 * 65536 * 4
     _err(L.spk_latency_code(P1, 32, 6, 160, 250, 30, 0.01, 0, P1, None, P1, need - 1, None),
          spk.SPK_E_WORKSPACE, "workspace")
 

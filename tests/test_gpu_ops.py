@@ -77,6 +77,28 @@ def test_latency_code_crowded_and_spread_samples():
         np.testing.assert_array_equal(got, oracle.latency_code(x, T, 0.01))
 
 
+def test_latency_code_large_samples_crowded_and_sparse():
+    # samples over 8192 values: the boundary selection with one bucket holding
+    # every key (ties ordered by index), two values, half tied, a wide span of
+    # exponents, fewer eligible values than steps, one, and none
+    dev = gpu()
+    rng = np.random.default_rng(33)
+    shape = (7, 6, 160, 250)
+    x = rng.standard_normal(shape).astype(np.float32)
+    x[0] = 0.5
+    x[1] = np.where(rng.random(shape[1:]) < 0.5, 0.25, 2.0).astype(np.float32)
+    x[2, :3] = 1.0
+    x[3] = np.exp(rng.uniform(-20, 20, shape[1:])).astype(np.float32)
+    x[4] = -1.0
+    x[4].reshape(-1)[[3, 5, 100, 7000, 239999]] = [0.5, 1.0, 2.0, 2.0, 3.0]
+    x[5] = -1.0
+    x[5, 2, 80, 125] = 4.0
+    x[6] = np.nan
+    for T in (15, 30, 254):
+        got = np_(spk.spk_latency_code(_t(x, dev), T, 0.01))
+        np.testing.assert_array_equal(got, oracle.latency_code(x, T, 0.01))
+
+
 def test_latency_code_frames_and_linear_mode():
     dev = gpu()
     rng = np.random.default_rng(11)
