@@ -67,21 +67,34 @@ constexpr uint32_t kSelHi = 0x04030402u;       // bytes 2,3 -> halves 1024 + b
 constexpr size_t kStvOff = 0;
 constexpr size_t kSttOff = kStvOff + 2 * 32 * kStageStride * sizeof(float);
 constexpr size_t kTabOff = (kSttOff + 2 * 32 * kStageStride + 15) / 16 * 16;
-constexpr size_t kTabBytes = 3 * kG * 2 * sizeof(int);
+constexpr size_t kTabBytes = 3 * kG * 3 * sizeof(int);
 constexpr size_t kFlagOff = kTabOff + kTabBytes;
 constexpr size_t kHalOff = (kFlagOff + kRange / 16 + 15) / 16 * 16;
 
+// Layers with few maps take their output positions in blocks of by x bx
+// (1 x 1 otherwise): a tile's 32 columns are then (position of the block,
+// map) pairs, so four maps fill a tile with 2 x 4 positions instead of
+// leaving 28 of its 32 columns empty.  A block is one position of a virtual
+// layer with by*bx*Co maps, a window of Khv x Kwv input pixels (the union of
+// its positions' windows) and strides by*stride, bx*stride; the weight of
+// virtual map (jy, jx, o) at virtual tap (c, kyv, kxv) is W[o, c, kyv -
+// jy*stride, kxv - jx*stride] inside the real window and 0 outside it.
 struct PGeom {
     int B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo;
+    int by, bx;    // output positions per block
+    int Hv, Wv;    // blocks: ceil(Ho / by) x ceil(Wo / bx)
+    int Khv, Kwv;  // input window of a block
+    int Cv;        // virtual maps: by * bx * Co
     int Cp;    // channels per padded pixel of Xp
     int Hp, Wp;
     int rowb;  // Wp * Cp: bytes of one padded input row
-    int run;   // Kw * Cp: taps of one kernel row
+    int slack; // readable bytes past the last padded row
+    int run;   // Kwv * Cp: taps of one kernel row
     int Q16;   // ceil(run / 16): 16-tap slices per kernel row
-    int SK;    // Kh * Q16: slices of the layer
+    int SK;    // Khv * Q16: slices of the layer
     int SKp;   // slices of the kernel instance (>= SK; the extra ones are zero)
-    int P;     // B * Ho * Wo
-    int NT;    // ceil(Co / 32)
+    int P;     // B * Hv * Wv blocks (positions when the blocks are 1 x 1)
+    int NT;    // ceil(Cv / 32)
     int hw;    // input words (16 bytes) the LDS halves of a launch hold
     int TP;    // steps per position in a tile: 8, 16 or 32
     int lgTP;
@@ -93,31 +106,70 @@ int choose_cp(int Ci, int Kw)
     return (Kw * c8 + 15) / 16 == (Kw * Ci + 15) / 16 ? c8 : Ci;
 }
 
-PGeom make_pgeom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride, int pad,
-                 int Ho, int Wo)
+PGeom make_pgeom_blocked(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
+                         int pad, int Ho, int Wo, int by, int bx)
 {
     PGeom g{};
     g.B = B; g.T = T; g.Ci = Ci; g.Hi = Hi; g.Wi = Wi; g.Co = Co; g.Kh = Kh; g.Kw = Kw;
     g.stride = stride; g.pad = pad; g.Ho = Ho; g.Wo = Wo;
-    g.Cp = choose_cp(Ci, Kw);
+    g.by = by; g.bx = bx;
+    g.Hv = (Ho + by - 1) / by;
+    g.Wv = (Wo + bx - 1) / bx;
+    g.Khv = (by - 1) * stride + Kh;
+    g.Kwv = (bx - 1) * stride + Kw;
+    g.Cv = by * bx * Co;
+    g.Cp = choose_cp(Ci, g.Kwv);
     g.Hp = Hi + 2 * pad;
     g.Wp = Wi + 2 * pad;
     g.rowb = g.Wp * g.Cp;
-    g.run = Kw * g.Cp;
+    // a block past the last row or column reads up to by*stride rows and a
+    // row's width beyond the padded input (only for its positions that are
+    // past the output, whose weights there are zero)
+    g.slack = kSlackPT + (by > 1 || bx > 1 ? (by * stride + 1) * g.rowb : 0);
+    g.run = g.Kwv * g.Cp;
     g.Q16 = (g.run + 15) / 16;
-    g.SK = Kh * g.Q16;
+    g.SK = g.Khv * g.Q16;
     g.SKp = g.SK;
-    g.P = B * Ho * Wo;
-    g.NT = (Co + 31) / 32;
+    g.P = B * g.Hv * g.Wv;
+    g.NT = (g.Cv + 31) / 32;
     g.TP = T <= 8 ? 8 : (T <= 16 ? 16 : 32);
     g.lgTP = T <= 8 ? 3 : (T <= 16 ? 4 : 5);
     return g;
 }
 
+// Geometry of a layer: 1 x 1 blocks, or for layers of at most 16 maps the
+// block shape with the least work (slices x blocks x column tiles) among
+// those that fill at most 32 columns and whose slices still fit the
+// in-register kernels (18 with float weights, 36 with half weights), when it
+// saves at least a fifth of the work.
+PGeom make_pgeom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride, int pad,
+                 int Ho, int Wo, bool half_w)
+{
+    const PGeom one = make_pgeom_blocked(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, 1, 1);
+    if (Co > 16) return one;
+    static const int kShapes[][2] = {{1, 2}, {2, 1}, {2, 2}, {1, 4}, {4, 1}, {2, 4},
+                                     {4, 2}, {4, 4}, {2, 8}, {8, 2}, {4, 8}, {8, 4}};
+    const int limit = half_w ? 36 : 18;
+    const long long base = (long long)one.SK * one.NT * one.P;
+    PGeom best = one;
+    long long best_work = base;
+    for (const auto &sh : kShapes) {
+        if (sh[0] * sh[1] * Co > 32 || sh[0] > Ho || sh[1] > Wo) continue;
+        const PGeom g = make_pgeom_blocked(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, sh[0], sh[1]);
+        if (g.SK > limit) continue;
+        const long long work = (long long)g.SK * g.NT * g.P;
+        if (work < best_work) {
+            best = g;
+            best_work = work;
+        }
+    }
+    return best_work * 5 <= base * 4 ? best : one;
+}
+
 // Alignment of every window run in the staged halves: 16, 8, 4 or 2 bytes.
 int read_mode(int Cp) { return Cp % 8 == 0 ? 3 : (Cp % 4 == 0 ? 2 : (Cp % 2 == 0 ? 1 : 0)); }
 
-size_t xp_bytes(const PGeom &g) { return spk::align_up((size_t)g.B * g.Hp * g.rowb + kSlackPT, 256); }
+size_t xp_bytes(const PGeom &g) { return spk::align_up((size_t)g.B * g.Hp * g.rowb + g.slack, 256); }
 size_t bp_bytes(const PGeom &g, int np) { return (size_t)g.NT * g.SKp * np * 64 * sizeof(h8); }
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
@@ -163,11 +215,11 @@ __device__ __forceinline__ u4 lds_read16(const uint8_t *base, int at)
 // Padded input rows [r0, r1) hold the windows of output positions [p0, p1].
 __host__ __device__ inline void group_rows(const PGeom &g, int p0, int p1, int &r0, int &r1)
 {
-    const int HoWo = g.Ho * g.Wo;
-    const int b0 = p0 / HoWo, y0 = (p0 - b0 * HoWo) / g.Wo;
-    const int b1 = p1 / HoWo, y1 = (p1 - b1 * HoWo) / g.Wo;
-    r0 = b0 * g.Hp + y0 * g.stride;
-    r1 = b1 * g.Hp + y1 * g.stride + g.Kh;
+    const int HvWv = g.Hv * g.Wv;
+    const int b0 = p0 / HvWv, y0 = (p0 - b0 * HvWv) / g.Wv;
+    const int b1 = p1 / HvWv, y1 = (p1 - b1 * HvWv) / g.Wv;
+    r0 = b0 * g.Hp + y0 * g.by * g.stride;
+    r1 = b1 * g.Hp + y1 * g.by * g.stride + g.Khv;
 }
 
 // ------------------------------------------------------------------ packing
@@ -204,13 +256,16 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
             for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = never;
         }
         if ((int)blockIdx.x == nb_in - 1)
-            for (int e = threadIdx.x; e < kSlackPT; e += blockDim.x) row[g.rowb + e] = never;
+            for (int e = threadIdx.x; e < g.slack; e += blockDim.x) row[g.rowb + e] = never;
         return;
     }
-    const int o = blockIdx.x - nb_in;
+    // virtual map ov = (jy*bx + jx)*Co + o: real map o of block position (jy, jx)
+    const int ov = blockIdx.x - nb_in;
+    const int jb = ov / g.Co, o = ov - jb * g.Co;
+    const int jy = jb / g.bx, jx = jb - jy * g.bx;
     const int taps = g.Ci * g.Kh * g.Kw;
     float *wl = reinterpret_cast<float *>(sm);
-    const bool real = o < g.Co;
+    const bool real = ov < g.Cv;
     for (int e = threadIdx.x; e < taps; e += blockDim.x) {
         float w = 0.0f;
         if (real) {
@@ -221,10 +276,11 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
         wl[e] = w;
     }
     __syncthreads();
-    const int nt = o / 32, col = o & 31;
+    const int nt = ov / 32, col = ov & 31;
     for (int f = threadIdx.x; f < g.SKp * 2; f += blockDim.x) {
         const int s = f >> 1, half = f & 1;
-        const int ky = s / g.Q16, jq = s - ky * g.Q16;
+        const int kyv = s / g.Q16, jq = s - kyv * g.Q16;
+        const int ky = kyv - jy * g.stride;
         h8 hi, lo;
         // addresses first (padding taps read word 0), then the reads together:
         // no branch around a read
@@ -233,8 +289,10 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
 #pragma unroll
         for (int e = 0; e < 8; e++) {
             const int j = jq * 16 + half * 8 + e;
-            const int kx = j / g.Cp, c = j - kx * g.Cp;
-            live[e] = s < g.SK && j < g.run && c < g.Ci;
+            const int kxv = j / g.Cp, c = j - kxv * g.Cp;
+            const int kx = kxv - jx * g.stride;
+            live[e] = s < g.SK && j < g.run && c < g.Ci && (unsigned)ky < (unsigned)g.Kh &&
+                      (unsigned)kx < (unsigned)g.Kw;
             at[e] = live[e] ? (c * g.Kh + ky) * g.Kw + kx : 0;
         }
         float wv8[8];
@@ -257,8 +315,9 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
 // -------------------------------------------------------------------- firing
 
 struct Tab {
-    int xoff;   // Xp offset of the position's window origin
-    int obase;  // output offset of the position for map 0: b*Co*Ho*Wo + y*Wo + x
+    int xoff;   // Xp offset of the block's window origin
+    int obase;  // output offset of its first position for map 0: b*Co*Ho*Wo + y0*Wo + x0
+    int yx;     // y0 << 16 | x0, its first position
 };
 
 // Per-group position table (threads 0..kG-1; slots past the group repeat its last).
@@ -267,12 +326,14 @@ __device__ __forceinline__ void fill_table(const PGeom &g, int gs, int cnt, Tab 
     const int i = threadIdx.x;
     if (i < kG) {
         const int p = gs + min(i, cnt - 1);
-        const int HoWo = g.Ho * g.Wo;
-        const int b = p / HoWo, rem = p - b * HoWo;
-        const int y = rem / g.Wo, x = rem - y * g.Wo;
+        const int HvWv = g.Hv * g.Wv;
+        const int b = p / HvWv, rem = p - b * HvWv;
+        const int yb = rem / g.Wv, xb = rem - yb * g.Wv;
+        const int y0 = yb * g.by, x0 = xb * g.bx;
         Tab t;
-        t.xoff = (b * g.Hp + y * g.stride) * g.rowb + x * g.stride * g.Cp;
-        t.obase = b * g.Co * HoWo + rem;
+        t.xoff = (b * g.Hp + y0 * g.stride) * g.rowb + x0 * g.stride * g.Cp;
+        t.obase = b * g.Co * g.Ho * g.Wo + y0 * g.Wo + x0;
+        t.yx = (y0 << 16) | x0;
         tab[i] = t;
     }
 }
@@ -347,11 +408,21 @@ __device__ __forceinline__ void write_out(const PGeom &g, int nt, int gs, int p_
 {
     const int HoWo = g.Ho * g.Wo;
     const int cnt = min(p_end, gs + kG) - gs;
+    const bool blocked = g.by * g.bx > 1;
     for (int idx = threadIdx.x; idx < 32 * kG; idx += kThreads) {
         const int pi = idx & (kG - 1), oc = idx / kG;
-        const int o = nt * 32 + oc;
-        if (pi < cnt && o < g.Co) {
-            const int n = tab[pi].obase + o * HoWo;
+        const int ov = nt * 32 + oc;
+        if (pi < cnt && ov < g.Cv) {
+            int n;
+            if (blocked) {  // virtual map (jy*bx + jx)*Co + o
+                const int jb = ov / g.Co, o = ov - jb * g.Co;
+                const int jy = jb / g.bx, jx = jb - jy * g.bx;
+                const int yx = tab[pi].yx;
+                if ((yx >> 16) + jy >= g.Ho || (yx & 0xffff) + jx >= g.Wo) continue;
+                n = tab[pi].obase + o * HoWo + jy * g.Wo + jx;
+            } else {
+                n = tab[pi].obase + ov * HoWo;
+            }
             out_v[n] = stv[oc * kStageStride + pi];
             out_t[n] = stt[oc * kStageStride + pi];
         }
@@ -784,9 +855,10 @@ void launch_pt(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t x
 }
 
 // Instances made for one slice layout and tile shape: (SK, QC, NP, kMode, TP)
-// of a layer whose Kh * Q16 equals the instance's slices.  3x3 over 32 padded
-// channels with float masters, 5x5 over 6 channels, 3x3 over 64 channels with
-// half weights; 16 or 32 steps per position.
+// of a layer whose Khv * Q16 equals the instance's slices.  3x3 over 32
+// padded channels with float masters, 5x5 over 6 channels, the 6 x 8 window
+// of a 2 x 4 block of 5x5 positions over 6 channels (four maps), 3x3 over 64
+// channels with half weights; 16 or 32 steps per position.
 struct PtExact {
     int SK, QC, NP, mode, TP;
     PtLaunch fn;
@@ -795,6 +867,7 @@ const PtExact kExact[] = {
     {18, 6, 2, 3, 16, &launch_pt<18, 2, 3, 6, 16>},
     {10, 2, 2, 1, 16, &launch_pt<10, 2, 1, 2, 16>},
     {10, 2, 2, 1, 32, &launch_pt<10, 2, 1, 2, 32>},
+    {18, 3, 2, 1, 32, &launch_pt<18, 2, 1, 3, 32>},
     {36, 12, 1, 3, 32, &launch_pt<36, 1, 3, 12, 32>},
 };
 
@@ -810,10 +883,10 @@ const PtLaunch kDeep[2][4] = {{&launch_deep<1, 0>, &launch_deep<1, 1>, &launch_d
 // Largest staged row range over the groups of every range (exact, per geometry).
 int max_rows(const PGeom &g, int nranges)
 {
-    typedef std::tuple<int, int, int, int, int, int, int, int, int> Key;
+    typedef std::tuple<int, int, int, int, int, int, int, int, int, int, int> Key;
     static std::mutex mu;
     static std::map<Key, int> memo;
-    const Key key{g.B, g.Hi, g.Wi, g.Kh, g.stride, g.pad, g.Ho, g.Wo, nranges};
+    const Key key{g.B, g.Hi, g.Wi, g.Kh, g.stride, g.pad, g.Ho, g.Wo, nranges, g.by, g.bx};
     {
         std::lock_guard<std::mutex> lock(mu);
         auto it = memo.find(key);
@@ -868,11 +941,10 @@ bool conv_pt_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int
     if (readout || potentials || T < 1 || T > 32 || B < 1 || Ci < 1 || Co < 1 || Ho < 1 || Wo < 1)
         return false;
     const long long Hp = Hi + 2ll * pad, Wp = Wi + 2ll * pad;
-    const int Cp = choose_cp(Ci, Kw);
-    if ((long long)B * Hp * Wp * Cp + kSlackPT >= (1ll << 30)) return false;
     if ((long long)B * Co * Ho * Wo >= (1ll << 31)) return false;
-    if (Wp * Cp > 48 * 1024 || (long long)Ci * Kh * Kw * 4 > 64 * 1024) return false;
-    const PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    if (Wp * (Ci + 8) > 48 * 1024 || (long long)Ci * Kh * Kw * 4 > 64 * 1024) return false;
+    if (B * Hp * Wp * (Ci + 8) + 64 * Wp * (Ci + 8) >= (1ll << 30)) return false;
+    const PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, half_w);
     if (g.SK > 4096) return false;
     // a group's rows, with the 16-byte alignment in front and 32 bytes of over-read
     const long long rows = max_rows(g, n_ranges(g));
@@ -882,16 +954,21 @@ bool conv_pt_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int
 size_t conv_pt_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride,
                          int pad, int Ho, int Wo)
 {
-    PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
-    g.SKp = std::max(packed_sk(g.SK, false), packed_sk(g.SK, true));
-    return xp_bytes(g) + bp_bytes(g, 2);
+    // the geometry (block shape) may differ between float and half weights
+    size_t need = 0;
+    for (int hw = 0; hw < 2; hw++) {
+        PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, hw != 0);
+        g.SKp = std::max(packed_sk(g.SK, false), packed_sk(g.SK, true));
+        need = std::max(need, xp_bytes(g) + bp_bytes(g, 2));
+    }
+    return need;
 }
 
 spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
                         bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
                         float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
 {
-    PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, half_w);
     g.SKp = packed_sk(g.SK, half_w);
     uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
     h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
@@ -909,7 +986,7 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
     g.hw = (int)((max_rows(g, nranges) * (long long)g.rowb + 64 + 47) / 16);
     const int per_xcd = (nranges + 7) / 8;
     const dim3 grid(8 * g.NT * per_xcd);
-    const size_t xw = ((size_t)g.B * g.Hp * g.rowb + kSlackPT) / 16;
+    const size_t xw = ((size_t)g.B * g.Hp * g.rowb + g.slack) / 16;
     PtLaunch launch;
     if (instance_sk(g.SK, half_w)) {
         int idx = 0;

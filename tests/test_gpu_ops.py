@@ -158,6 +158,9 @@ CONV_CASES = [
     (3, 1000, 1, 1, 65, 1, 1, 0, 30, 60.0, 0.2, "f32"),     # 1 x 1 kernel over 1000 channels (an FC layer)
     (32, 30, 14, 14, 250, 3, 1, 1, 15, 10.0, 0.85, "f32"),  # the three-layer net's conv2 at B = 32: more
                                                             # than 64 positions per block range
+    (2, 6, 160, 250, 4, 5, 1, 2, 30, 15.0, 0.05, "f32"),    # four maps: 2 x 4 position blocks, ragged x
+    (2, 3, 21, 23, 5, 3, 2, 1, 12, 2.0, 0.4, "f32"),        # few maps, stride 2, ragged blocks
+    (2, 8, 17, 19, 2, 5, 1, 2, 9, 3.0, 0.3, "f16"),         # two maps, half weights: 4 x 4 blocks
 ]
 
 
