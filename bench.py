@@ -104,6 +104,15 @@ def dtype_label(wl):
                    "fp32 accumulation")
 
 
+def pipe_call(wl, li):
+    """The entry point a pipeline step calls for conv layer li (0-based): the
+    pooling in front of a layer runs inside its call."""
+    convs = [i for i, (kind, _) in enumerate(wl.stages) if kind == "conv"]
+    si = convs[li]
+    pooled = si > 0 and wl.stages[si - 1][0] == "pool" and wl.coding == "rank"
+    return "spk_pool_conv_fire" if pooled else "spk_conv_fire"
+
+
 def hbm_stages(wl, pipe, kept, stage_ms):
     """Algorithmic HBM bytes of the memory-bound stages (each input read once,
     each output written once) and the rate they reach at the measured times."""
@@ -475,7 +484,7 @@ def main():
         for li, spec in enumerate(wl.convs):
             n = li + 1
             ev = fanout_events(kept.layer_in[li], spec, torch)
-            names = [f"conv{n}", f"wta{n}", f"select{n}", f"stdp{n}"]
+            names = [f"conv{n}", f"wta{n}", f"select{n}", f"stdp{n}", f"pack{n}"]
             lay_ms = sum(st_ms.get(k, 0.0) for k in names)
             c_ms = st_ms[f"conv{n}"]
             per_layer.append({
@@ -494,7 +503,8 @@ def main():
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_F16_MFMA_TFLOPS,
                 "unit": "TFLOP/s", "frac": achieved / PEAK_F16_MFMA_TFLOPS,
                 "traffic": None if sparse_dom else measured_traffic(wl, dom + 1),
-                "kernel": f"spk_conv_fire{'_sparse' if sparse_dom else ''} ({dom_name})",
+                "kernel": (f"spk_conv_fire_sparse ({dom_name})" if sparse_dom else
+                           f"{pipe_call(wl, dom)} ({dom_name})"),
                 "kernel_ms": dom_ms,
                 "work": f"{work[dom][1]} = {work[dom][0]:.4g} flop per launch"}
     if sparse_dom:

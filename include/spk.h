@@ -170,6 +170,59 @@ spk_status spk_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int Hi, 
                          void *ws, size_t ws_bytes, spk_stream stream);
 
 /*
+ * spk_pool_conv_fire -- max-pooling (§II-E.3) followed by spk_conv_fire
+ * (§II-E.1), the pooling done inside the convolution's own packing pass
+ * rather than by a separate spk_pool call.
+ *   in_times   uint8 B x Ci x H0 x W0 (device): the previous layer's map.
+ *   pool_kh, pool_kw, pool_stride, pool_pad  the pooling window, as spk_pool;
+ *              the layer input is B x Ci x Hi x Wi with Hi =
+ *              spk_out_extent(H0, pool_kh, pool_stride, pool_pad) (Wi alike).
+ *              A 1 x 1 window of stride 1 and no padding is the identity.
+ *   pooled_times nullable uint8 B x Ci x Hi x Wi (device): receives the
+ *              pooled map, bit-identical to spk_pool's (STDP of this layer
+ *              needs it as its input).
+ *   packed_w   nullable (device): B fragments of w written by
+ *              spk_conv_pack_weights, which readout layers (theta = +inf)
+ *              then read instead of packing w on every call.  It must
+ *              describe the current w (the call may read either); other
+ *              layers ignore it.
+ *   w, w_dtype, Co, Kh, Kw, stride, pad, theta, out_times, out_vkey: as
+ *              spk_conv_fire (no dense potentials here).
+ *   ws         workspace of spk_pool_conv_fire_workspace_size(...) bytes,
+ *              256-byte aligned; contents on entry do not matter.
+ * Results equal spk_pool followed by spk_conv_fire bit for bit.
+ * Errors: those of spk_pool and spk_conv_fire.
+ */
+size_t spk_pool_conv_fire_workspace_size(int B, int T, int Ci, int H0, int W0, int pool_kh,
+                                         int pool_kw, int pool_stride, int pool_pad, int Co,
+                                         int Kh, int Kw, int stride, int pad, float theta);
+spk_status spk_pool_conv_fire(const uint8_t *in_times, int B, int T, int Ci, int H0, int W0,
+                              int pool_kh, int pool_kw, int pool_stride, int pool_pad,
+                              uint8_t *pooled_times, const void *w, spk_dtype w_dtype,
+                              const void *packed_w, int Co, int Kh, int Kw, int stride, int pad,
+                              float theta, uint8_t *out_times, float *out_vkey, void *ws,
+                              size_t ws_bytes, spk_stream stream);
+
+/*
+ * spk_conv_pack_weights -- the weights of a readout layer as matrix-core B
+ * fragments, for spk_pool_conv_fire's packed_w (§II-E.1: V_t = W * S_t is a
+ * product with W).  A caller keeps them while w does not change and calls
+ * this again after every update of w (spk_stdp_update, spk_quantize).
+ *   w        Co x Ci x Kh x Kw (device), SPK_F32 or SPK_F16.
+ *   packed   device buffer of spk_conv_packed_weights_size(...) bytes,
+ *            16-byte aligned: for each 32-map tile and 16-tap slice of the
+ *            depth (taps ordered by kernel row, then column, then channel, the
+ *            channels padded to an odd multiple of 8), 64 lanes of 8 halves (lane
+ *            l: map l % 32, taps 8*(l/32)..+7); float weights as two such
+ *            blocks, hi = half(w) then lo = half(w - hi); padding zero.
+ * Errors: SPK_E_ARG, SPK_E_UNSUPPORTED (w_dtype), SPK_E_WORKSPACE (packed
+ * smaller than the size), SPK_E_SHAPE (Ci*Kh*Kw*4 above 64 KiB).
+ */
+size_t spk_conv_packed_weights_size(int Co, int Ci, int Kh, int Kw, spk_dtype w_dtype);
+spk_status spk_conv_pack_weights(const void *w, spk_dtype w_dtype, int Co, int Ci, int Kh, int Kw,
+                                 void *packed, size_t packed_bytes, spk_stream stream);
+
+/*
  * spk_conv_fire_noalloc -- spk_conv_fire for callers that cannot allocate
  * device memory (code under stream capture, serving loops, harnesses that
  * forbid hipMalloc).  Same arguments, results and errors as spk_conv_fire,

@@ -50,6 +50,8 @@ constexpr uint32_t kSelHi = 0x04030402u;    // bytes 2,3 -> halves 1024 + b
 
 struct FGeom {
     int B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo;
+    int Cin;     // channels of the input and weights (Ci: channels of Xp, Cin or more)
+    int ind;     // 1: Xp holds the readout's indicator bytes (see make_ro_geom), 0: times
     int Hp, Wp;  // padded input extent
     int run;     // Kw*Ci: bytes of one kernel row's taps
     int R8;      // run rounded up to a multiple of 8
@@ -68,6 +70,8 @@ FGeom make_geom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, in
     FGeom g{};
     g.B = B; g.T = T; g.Ci = Ci; g.Hi = Hi; g.Wi = Wi; g.Co = Co; g.Kh = Kh; g.Kw = Kw;
     g.stride = stride; g.pad = pad; g.Ho = Ho; g.Wo = Wo;
+    g.Cin = Ci;
+    g.ind = 0;
     g.Hp = Hi + 2 * pad;
     g.Wp = Wi + 2 * pad;
     g.run = Kw * Ci;
@@ -79,6 +83,28 @@ FGeom make_geom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, in
     g.rowb = g.Wp * Ci;
     g.S16 = (g.K + 15) / 16;
     g.NT32 = (Co + 31) / 32;
+    return g;
+}
+
+// Geometry of a readout layer's Xp.  Its channels are padded to an odd
+// multiple of 8: the 8 taps of a fragment lane are then always 8 aligned
+// bytes, and the 8-byte LDS reads of neighbouring positions (Ci bytes apart)
+// fall on different banks.  Its bytes are indicators of the last frame, 0x3C
+// for a time <= T-1 and 0 for later, never and padding: placed in the high
+// byte of a half (byte permutes) they are the halves 1.0 and 0 of the A
+// operand.
+int ro_channels(int Ci)
+{
+    const int c8 = (Ci + 7) / 8;
+    return 8 * (c8 | 1);
+}
+
+FGeom make_ro_geom(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw, int stride, int pad,
+                   int Ho, int Wo)
+{
+    FGeom g = make_geom(B, T, ro_channels(Ci), Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    g.Cin = Ci;
+    g.ind = 1;
     return g;
 }
 
@@ -119,6 +145,15 @@ __device__ __forceinline__ uint32_t arrive2(uint32_t x, uint32_t sel, h2 c)
 __device__ __forceinline__ h8 frag_upto(uint2 x, h2 c)
 {
     u4 v = {upto2(x.x, kSelLo, c), upto2(x.x, kSelHi, c), upto2(x.y, kSelLo, c), upto2(x.y, kSelHi, c)};
+    return __builtin_bit_cast(h8, v);
+}
+
+// A fragment of 8 indicator bytes (0x3C or 0): each byte becomes the high
+// byte of a half, 0x3C00 = 1.0 or 0.
+__device__ __forceinline__ h8 frag_ind(uint2 x)
+{
+    u4 v = {__builtin_amdgcn_perm(x.y, x.x, 0x010C000Cu), __builtin_amdgcn_perm(x.y, x.x, 0x030C020Cu),
+            __builtin_amdgcn_perm(x.y, x.x, 0x050C040Cu), __builtin_amdgcn_perm(x.y, x.x, 0x070C060Cu)};
     return __builtin_bit_cast(h8, v);
 }
 
@@ -200,10 +235,13 @@ __device__ __forceinline__ void copy_to_lds(uint8_t *dst, const uint8_t *src, in
 
 // ------------------------------------------------------------------ packing
 
-// Blocks [0, B*Hp): one padded input row each, (b, py): the row's time bytes
+// Blocks [0, nb_in): one padded input row each, (b, py): the row's time bytes
 // go through LDS from channel rows (coalesced reads) to channels-last order
-// (coalesced writes); the last block also fills the readable slack.
-// Blocks [B*Hp, B*Hp + maps): one output map o each (maps = the column tiles'
+// (coalesced writes), a pooled input row pooled there from its staged window
+// rows; the last block also fills the readable slack.  A pooled input whose
+// rows are too wide to stage runs a grid-stride pass over the Xp bytes
+// instead.
+// Blocks [nb_in, nb_in + maps): one output map o each (maps = the column tiles'
 // width, the padding maps written as zeros): its weights are staged in LDS
 // and written as B fragments in the packed tap order, as hi/lo halves
 // (NP = 2) or halves (NP = 1).  kBig: fragments of the 32x32x16 shape (lane:
@@ -212,42 +250,75 @@ __device__ __forceinline__ void copy_to_lds(uint8_t *dst, const uint8_t *src, in
 template <int NP, bool kHalfW, bool kBig>
 __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
                                               const void *__restrict__ wv, FGeom g, int nb_in,
-                                              uint8_t *__restrict__ xp, h8 *__restrict__ bp)
+                                              uint8_t *__restrict__ xp, h8 *__restrict__ bp,
+                                              spk::PoolIn pool)
 {
     extern __shared__ __align__(16) uint8_t sm[];
+    // empty cells: never fires (times), or indicator 0
+    const uint8_t fill = g.ind ? (uint8_t)0 : (uint8_t)spk::kNever;
+    if ((int)blockIdx.x < nb_in && pool.src && pool.stage < 0) {
+        // pooled input too wide to stage: each thread writes Xp bytes
+        // (b, py, px, c), the pooling window read from the unpooled map; the
+        // Xp body is below 2^31 bytes
+        const uint32_t body = (uint32_t)g.B * g.Hp * g.rowb, total = body + kSlack;
+        for (uint32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (uint32_t)nb_in * blockDim.x) {
+            uint8_t v = fill;
+            if (e < body) {
+                const uint32_t rowi = e / (uint32_t)g.rowb, within = e - rowi * (uint32_t)g.rowb;
+                const int b = (int)(rowi / (uint32_t)g.Hp), py = (int)(rowi - (uint32_t)b * g.Hp);
+                const int px = (int)(within / (uint32_t)g.Ci), c = (int)within - px * g.Ci;
+                const int iy = py - g.pad, ix = px - g.pad;
+                if ((unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi && c < g.Cin) {
+                    const long long plane = (long long)b * g.Cin + c;
+                    const uint32_t t = spk::pool_cell(pool, plane, iy, ix);
+                    if (pool.pooled) pool.pooled[(plane * g.Hi + iy) * g.Wi + ix] = (uint8_t)t;
+                    v = g.ind ? (t < (uint32_t)g.T ? (uint8_t)0x3C : (uint8_t)0) : (uint8_t)t;
+                }
+            }
+            xp[e] = v;
+        }
+        return;
+    }
     if ((int)blockIdx.x < nb_in) {
         const int b = blockIdx.x / g.Hp, py = blockIdx.x - b * g.Hp;
         const int iy = py - g.pad;
         uint8_t *row = xp + ((size_t)b * g.Hp + py) * g.rowb;
         if ((unsigned)iy < (unsigned)g.Hi) {
-            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = (uint8_t)spk::kNever;
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = fill;
             __syncthreads();
-            const uint8_t *src = in + (size_t)b * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi;
-            const int n = g.Ci * g.Wi, step = (int)blockDim.x;
+            const int n = g.Cin * g.Wi, step = (int)blockDim.x;
             auto put = [&](int e, uint8_t v) {
                 const int c = e / g.Wi, x = e - c * g.Wi;
-                sm[(x + g.pad) * g.Ci + c] = v;
+                sm[(x + g.pad) * g.Ci + c] = g.ind ? (v < g.T ? (uint8_t)0x3C : (uint8_t)0) : v;
             };
-            auto get = [&](int e) {
-                const int c = e / g.Wi, x = e - c * g.Wi;
-                return src[(size_t)c * g.Hi * g.Wi + x];
-            };
-            int e = threadIdx.x;
-            for (; e + 3 * step < n; e += 4 * step) {
-                const uint8_t a = get(e), bb = get(e + step), c = get(e + 2 * step), d = get(e + 3 * step);
-                put(e, a);
-                put(e + step, bb);
-                put(e + 2 * step, c);
-                put(e + 3 * step, d);
+            if (pool.src) {
+                // the input row is pooled here (and kept when asked for)
+                spk::pool_row(pool, (long long)b * g.Cin, g.Cin, g.Hi, g.Wi, iy,
+                              reinterpret_cast<uint32_t *>(sm + pool.stage),
+                              [&](int c, int x, uint8_t v) { put(c * g.Wi + x, v); });
+            } else {
+                const uint8_t *src = in + (size_t)b * g.Cin * g.Hi * g.Wi + (size_t)iy * g.Wi;
+                auto get = [&](int e) {
+                    const int c = e / g.Wi, x = e - c * g.Wi;
+                    return src[(size_t)c * g.Hi * g.Wi + x];
+                };
+                int e = threadIdx.x;
+                for (; e + 3 * step < n; e += 4 * step) {
+                    const uint8_t a = get(e), bb = get(e + step), c = get(e + 2 * step), d = get(e + 3 * step);
+                    put(e, a);
+                    put(e + step, bb);
+                    put(e + 2 * step, c);
+                    put(e + 3 * step, d);
+                }
+                for (; e < n; e += step) put(e, get(e));
             }
-            for (; e < n; e += step) put(e, get(e));
             __syncthreads();
             for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = sm[e];
         } else {
-            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = (uint8_t)spk::kNever;
+            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = fill;
         }
         if ((int)blockIdx.x == nb_in - 1)
-            for (int e = threadIdx.x; e < kSlack; e += blockDim.x) row[g.rowb + e] = (uint8_t)spk::kNever;
+            for (int e = threadIdx.x; e < kSlack; e += blockDim.x) row[g.rowb + e] = fill;
         return;
     }
     // map of this block: the maps are dealt to the XCDs in contiguous runs
@@ -256,7 +327,7 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
     const int n_maps = (int)gridDim.x - nb_in, wb = (int)blockIdx.x - nb_in;
     const int xcd = wb & 7, per_x = n_maps >> 3, extra = n_maps & 7;
     const int o = xcd * per_x + min(xcd, extra) + (wb >> 3);
-    const int taps = g.Ci * g.Kh * g.Kw;
+    const int taps = g.Cin * g.Kh * g.Kw;
     float *wl = reinterpret_cast<float *>(sm);
     {
         const int oc = min(o, g.Co - 1);
@@ -286,7 +357,8 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
         const int lane = col + (kBig ? 32 : 16) * h;
         const int kb = (s * per + h) * 8;
         h8 hi, lo;
-        // tap kb = ky*R8 + j, j = kx*Ci + c; the 8 taps step through (ky, j, kx, c).
+        // tap kb = ky*R8 + j, j = kx*Ci + c; the 8 taps step through (ky, j, kx, c);
+        // channels c >= Cin (padding of a readout's Xp) have no weight.
         // The 8 LDS addresses first (padding taps read word 0), then the
         // reads together, then the conversions: no branch around a read.
         int ky = kb / g.R8, j = kb - ky * g.R8;
@@ -295,7 +367,7 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
         bool live[8];
 #pragma unroll
         for (int e = 0; e < 8; e++) {
-            live[e] = ky < g.Kh && j < g.run;
+            live[e] = ky < g.Kh && j < g.run && c < g.Cin;
             at[e] = live[e] ? (c * g.Kh + ky) * g.Kw + kx : 0;
             if (++j == g.R8) {
                 j = 0;
@@ -323,20 +395,35 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
     }
 }
 
-// Launch of the packing pass for a fragment shape.
+// Launch of the packing pass for a fragment shape.  in_rows: pack the input
+// (nb_in blocks); weights: pack the B fragments (one block per map).
 void launch_pack(const uint8_t *in, const void *w, bool half_w, bool big, const FGeom &g,
-                 uint8_t *xp, h8 *bp, hipStream_t s)
+                 uint8_t *xp, h8 *bp, hipStream_t s, bool in_rows = true, bool weights = true,
+                 const spk::PoolIn *pool = nullptr)
 {
-    const int nb_in = g.B * g.Hp;
-    const int maps = big ? g.NT32 * 32 : g.NT * 16;
-    const size_t lds = std::max((size_t)g.rowb, (size_t)g.Ci * g.Kh * g.Kw * sizeof(float));
+    // a pooled input row stages its window rows past the row buffer when
+    // they fit; otherwise its cells are pooled one by one
+    spk::PoolIn pl = pool ? *pool : spk::PoolIn{};
+    pl.stage = -1;
+    const size_t stage_at = spk::align_up((size_t)g.rowb, 16);
+    if (pool && stage_at + spk::pool_stage_bytes(pl, g.Cin) <= 64 * 1024) pl.stage = (int)stage_at;
+    // input blocks: one per padded row, or 1024 Xp bytes each (cells pooled one by one)
+    const int nb_in = !in_rows ? 0
+                      : pool && pl.stage < 0 ? spk::ceil_div((long long)g.B * g.Hp * g.rowb + kSlack, 1024)
+                                             : g.B * g.Hp;
+    const int maps = weights ? (big ? g.NT32 * 32 : g.NT * 16) : 0;
+    size_t lds = std::max(in_rows ? (size_t)g.rowb : (size_t)0,
+                          weights ? (size_t)g.Cin * g.Kh * g.Kw * sizeof(float) : (size_t)0);
     const dim3 grid(nb_in + maps), blk(256);
+    if (pool && in_rows)
+        lds = std::max(weights ? (size_t)g.Cin * g.Kh * g.Kw * sizeof(float) : (size_t)0,
+                       pl.stage >= 0 ? stage_at + spk::pool_stage_bytes(pl, g.Cin) : (size_t)0);
     if (big) {
-        if (half_w) hipLaunchKernelGGL((k_pack<1, true, true>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
-        else hipLaunchKernelGGL((k_pack<2, false, true>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
+        if (half_w) hipLaunchKernelGGL((k_pack<1, true, true>), grid, blk, lds, s, in, w, g, nb_in, xp, bp, pl);
+        else hipLaunchKernelGGL((k_pack<2, false, true>), grid, blk, lds, s, in, w, g, nb_in, xp, bp, pl);
     } else {
-        if (half_w) hipLaunchKernelGGL((k_pack<1, true, false>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
-        else hipLaunchKernelGGL((k_pack<2, false, false>), grid, blk, lds, s, in, w, g, nb_in, xp, bp);
+        if (half_w) hipLaunchKernelGGL((k_pack<1, true, false>), grid, blk, lds, s, in, w, g, nb_in, xp, bp, pl);
+        else hipLaunchKernelGGL((k_pack<2, false, false>), grid, blk, lds, s, in, w, g, nb_in, xp, bp, pl);
     }
 }
 
@@ -808,18 +895,22 @@ void k_fire32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g
 // ------------------------------------------------------------------ readout
 //
 // Readout layers (theta = +inf) need only V at the last step: one GEMM on the
-// final frame [time <= T-1], split over K.  A block of 4 waves owns a column
+// final frame [time <= T-1], split over K, on the indicator bytes of
+// make_ro_geom (an A fragment is four byte permutes).  A block of 4 waves owns a column
 // tile (32 maps) and a run of 4*kRoKC subtiles; wave w keeps the B fragments
 // of subtiles w*kRoKC.. in registers.  The block walks row groups of 32
-// positions: it stages the Xp rows that group and its K run touch, each wave
-// reads all of its A octets and then runs its products back to back, and
-// the four partial tiles are added in LDS in wave order and written to
+// positions: the Xp bytes that a group and its K run touch are staged in LDS
+// (the next group's bytes are fetched into registers while this group's
+// products run, when they fit kRoPre words per thread), each wave reads all
+// of its A octets and then runs its products back to back, and the four
+// partial tiles are added in LDS in wave order and written to
 // part[split][map][position] with each map's 32 positions in one coalesced
 // store.  k_readout_sum adds the splits in order.
 constexpr int kRoKC = 16;
 constexpr int kRoSteps = kWaves * kRoKC;
 constexpr int kRoStride = 33;                                     // partial tiles: [wave][row][map], padded
 constexpr int kRoRed = kWaves * 32 * kRoStride * (int)sizeof(float);  // LDS of the partial tiles
+constexpr int kRoPre = 8;                                         // prefetched 16-byte words per thread
 
 __host__ __device__ inline void ro_range(const FGeom &g, int p0, int p1, int sp, long long &h0,
                                          long long &h1)
@@ -843,7 +934,10 @@ __device__ __forceinline__ void ro_words(const FGeom &g, int rg, int sp, long lo
     nvec = (int)((h1 - a0 + 15) >> 4) + 1;
 }
 
-template <int NP>
+// kPre: the staged range of every group fits kRoPre words per thread and the
+// next group's words are loaded into registers during this group's products;
+// otherwise each group is copied straight into LDS before its products.
+template <int NP, bool kPre>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeom g, int iters,
                  int n_groups, int nx, float *__restrict__ part)
@@ -871,21 +965,45 @@ void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeo
     const int rg0 = bx * iters;
     const int rg_end = min(n_groups, rg0 + iters);
 
+    // the first group's words are requested before the B fragments
+    u4 pre[kPre ? kRoPre : 1];
+    auto fetch = [&](int rg, long long &a0, int &nvec) {
+        ro_words(g, rg, sp, a0, nvec);
+        const u4 *src = reinterpret_cast<const u4 *>(xp + a0);
+#pragma unroll
+        for (int u = 0; u < (kPre ? kRoPre : 1); u++) {
+            const int i = (int)threadIdx.x + u * kThreads;
+            if (i < nvec) pre[u] = src[i];
+        }
+    };
+    auto commit = [&](int nvec) {
+        u4 *dst = reinterpret_cast<u4 *>(halo);
+#pragma unroll
+        for (int u = 0; u < (kPre ? kRoPre : 1); u++) {
+            const int i = (int)threadIdx.x + u * kThreads;
+            if (i < nvec) dst[i] = pre[u];
+        }
+    };
+    long long a0 = 0;
+    int nvec = 0;
+    if (kPre && rg0 < rg_end) fetch(rg0, a0, nvec);
+
+    // B fragments; the subtiles past the wave's share (past S16) are zero,
+    // so their products add nothing and every wave runs the same
+    // straight-line code
     h8 bw[kRoKC][NP];
 #pragma unroll
     for (int s = 0; s < kRoKC; s++) {
         const int sc = min(sw0 + s, g.S16 - 1);
 #pragma unroll
-        for (int q = 0; q < NP; q++) bw[s][q] = bp[((size_t)(nt * g.S16 + sc) * NP + q) * 64 + lane];
+        for (int q = 0; q < NP; q++) {
+            const h8 v = bp[((size_t)(nt * g.S16 + sc) * NP + q) * 64 + lane];
+            bw[s][q] = s < nsw ? v : (h8)(_Float16)0.0f;
+        }
     }
-    // Per subtile: the comparison constant (half 1025 + (T - 1), or 0 for the
-    // subtiles past the wave's share, whose A fragments are then all zero and
-    // whose products add nothing: every wave runs the same straight-line code)
-    // and the octet's offset from a position's window origin, the same for
-    // every row group.  Octets past K read a row of the halo (their weights
-    // are zero).
-    const uint32_t cb = 0x6401u + (uint32_t)(g.T - 1);
-    const h2 cc = as_h2(cb | (cb << 16)), c0 = as_h2(0u);
+    // Per subtile: the octet's offset from a position's window origin, the
+    // same for every row group.  Octets past K read a row of the halo (their
+    // weights are zero).
     int offs[kRoKC];
     {
         const int q0 = 2 * sw0 + (lane >> 5);
@@ -900,15 +1018,24 @@ void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeo
             }
         }
     }
+    if (kPre && rg0 < rg_end) {
+        commit(nvec);
+        __syncthreads();
+    }
 
     for (int rg = rg0; rg < rg_end; rg++) {
         const int p0 = rg * 32;
-        long long a0;
-        int nvec;
-        ro_words(g, rg, sp, a0, nvec);
-        __syncthreads();  // the previous group's halo and partial tiles are no longer read
-        copy_to_lds(halo, xp + a0, nvec);
-        __syncthreads();
+        long long a0n = 0;
+        int nvn = 0;
+        if (kPre) {
+            // the next group's words travel while this group's products run
+            if (rg + 1 < rg_end) fetch(rg + 1, a0n, nvn);
+        } else {
+            ro_words(g, rg, sp, a0, nvec);
+            __syncthreads();  // the previous group's halo and partial tiles are no longer read
+            copy_to_lds(halo, xp + a0, nvec);
+            __syncthreads();
+        }
 
         // all of the wave's octets are read before the products start
         uint2 ab[kRoKC];
@@ -919,15 +1046,17 @@ void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeo
             const int y = rem / g.Wo, x = rem - y * g.Wo;
             const int base = (int)(((long long)b * g.Hp + (long long)y * g.stride) * g.rowb +
                                    (long long)x * g.stride * g.Ci - a0);
+            // every octet starts at a multiple of 8 (channels padded to 8)
 #pragma unroll
-            for (int s = 0; s < kRoKC; s++) ab[s] = lds_read8(halo, base + offs[s]);
+            for (int s = 0; s < kRoKC; s++)
+                ab[s] = *reinterpret_cast<const uint2 *>(halo + base + offs[s]);
         }
         f16v acc;
 #pragma unroll
         for (int e = 0; e < 16; e++) acc[e] = 0.0f;
 #pragma unroll
         for (int s = 0; s < kRoKC; s++) {
-            const h8 a = frag_upto(ab[s], s < nsw ? cc : c0);
+            const h8 a = frag_ind(ab[s]);
 #pragma unroll
             for (int q = 0; q < NP; q++)
                 acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bw[s][q], acc, 0, 0, 0);
@@ -946,6 +1075,14 @@ void k_readout32(const uint8_t *__restrict__ xp, const h8 *__restrict__ bp, FGeo
             const int p = p0 + r, o = nt * 32 + o_l;
             if (p < g.P && o < g.Co) part[((size_t)sp * g.Co + o) * g.P + p] = v;
         }
+        if (kPre && rg + 1 < rg_end) {
+            // every wave is past its halo reads (the barrier above): the next
+            // group's words replace them
+            commit(nvn);
+            a0 = a0n;
+            nvec = nvn;
+        }
+        if (kPre) __syncthreads();  // next halo in place; partial tiles free
     }
 }
 
@@ -1114,7 +1251,7 @@ constexpr size_t kRoLdsMax = 96 * 1024;
 // The packing pass stages one padded input row or one map's weights in LDS.
 bool pack_fits(const FGeom &g)
 {
-    return (long long)g.rowb <= 64 * 1024 && (long long)g.Ci * g.Kh * g.Kw * 4 <= 64 * 1024;
+    return (long long)g.rowb <= 64 * 1024 && (long long)g.Cin * g.Kh * g.Kw * 4 <= 64 * 1024;
 }
 
 }  // namespace
@@ -1146,11 +1283,11 @@ bool readout_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh
                             int stride, int pad, int Ho, int Wo)
 {
     if (T < 1 || T > SPK_MAX_T || B < 1 || Ci < 1 || Co < 1 || Ho < 1 || Wo < 1) return false;
-    const long long Hp = Hi + 2ll * pad, Wp = Wi + 2ll * pad;
-    if ((long long)B * Ho * Wo >= (1ll << 31) || (long long)B * Hp * Wp * Ci + kSlack >= (1ll << 31))
+    const long long Hp = Hi + 2ll * pad, Wp = Wi + 2ll * pad, Cp = ro_channels(Ci);
+    if ((long long)B * Ho * Wo >= (1ll << 31) || (long long)B * Hp * Wp * Cp + kSlack >= (1ll << 31))
         return false;
-    if ((long long)Kw * Ci > (1 << 16) || Kh > (1 << 12)) return false;
-    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    if ((long long)Kw * Cp > (1 << 16) || Kh > (1 << 12)) return false;
+    const FGeom g = make_ro_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
     if (!pack_fits(g) || (long long)ro_splits(g) * Co * g.P >= (1ll << 31)) return false;
     if ((long long)g.rowb * (g.Kh + 2) * 2 > (long long)kRoLdsMax) return false;  // cheap pre-check
     return ro_halo(g) + kRoRed <= kRoLdsMax;
@@ -1159,21 +1296,23 @@ bool readout_fast_supported(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh
 size_t readout_fast_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, int Kw,
                               int stride, int pad, int Ho, int Wo)
 {
-    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    const FGeom g = make_ro_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
     return xp_bytes(g) + spk::align_up(bp_bytes(g, 2), 256) +
            (size_t)ro_splits(g) * Co * g.P * sizeof(float);
 }
 
 spk_status readout_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
                         bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
-                        uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
+                        uint8_t *out_t, float *out_v, void *ws, hipStream_t s, const void *packed_w,
+                        const PoolIn *pool)
 {
-    const FGeom g = make_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
+    const FGeom g = make_ro_geom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo);
     uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
-    h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
+    h8 *bp = packed_w ? const_cast<h8 *>(reinterpret_cast<const h8 *>(packed_w))
+                      : reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
     float *part = reinterpret_cast<float *>(reinterpret_cast<char *>(ws) + xp_bytes(g) +
                                             spk::align_up(bp_bytes(g, 2), 256));
-    launch_pack(in, w, half_w, true, g, xp, bp, s);
+    launch_pack(in, w, half_w, true, g, xp, bp, s, true, packed_w == nullptr, pool);
     SPK_LAUNCHED("spk_conv_fire");
 
     const int splits = ro_splits(g);
@@ -1182,27 +1321,43 @@ spk_status readout_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
     // over several row groups
     int iters = (int)std::max<long long>(1, spk::ceil_div((long long)n_groups * g.NT32 * splits, 512));
     iters = std::min(iters, n_groups);
-    const size_t lds = ro_halo(g) + kRoRed;
+    const size_t halo = ro_halo(g);
+    const bool pre = halo / 16 <= (size_t)kRoPre * kThreads;
+    const size_t lds = halo + kRoRed;
     const int nx = spk::ceil_div(n_groups, iters);
     const dim3 grid(nx * g.NT32 * splits);
+    auto run = [&](auto kern) {
+        if (lds > 64 * 1024)
+            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups, nx, part);
+    };
     if (half_w) {
-        if (lds > 64 * 1024)
-            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_readout32<1>),
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k_readout32<1>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups, nx,
-                           part);
+        if (pre) run(k_readout32<1, true>);
+        else run(k_readout32<1, false>);
     } else {
-        if (lds > 64 * 1024)
-            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_readout32<2>),
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k_readout32<2>, grid, dim3(kThreads), lds, s, xp, bp, g, iters, n_groups, nx,
-                           part);
+        if (pre) run(k_readout32<2, true>);
+        else run(k_readout32<2, false>);
     }
     SPK_LAUNCHED("spk_conv_fire");
     const long long n = (long long)g.Co * g.P;
     hipLaunchKernelGGL(k_readout_sum, dim3(spk::ceil_div(n, 256)), dim3(256), 0, s, part, g, splits,
                        out_t, out_v);
     return check_launch("spk_conv_fire");
+}
+
+size_t readout_packed_bytes(int Co, int Ci, int Kh, int Kw, bool half_w)
+{
+    const FGeom g = make_ro_geom(1, 1, Ci, Kh, Kw, Co, Kh, Kw, 1, 0, 1, 1);
+    return (size_t)g.NT32 * g.S16 * (half_w ? 1 : 2) * 64 * sizeof(h8);
+}
+
+spk_status readout_pack_weights(const void *w, bool half_w, int Co, int Ci, int Kh, int Kw,
+                                void *packed, hipStream_t s)
+{
+    const FGeom g = make_ro_geom(1, 1, Ci, Kh, Kw, Co, Kh, Kw, 1, 0, 1, 1);
+    launch_pack(nullptr, w, half_w, true, g, nullptr, reinterpret_cast<h8 *>(packed), s, false, true);
+    return check_launch("spk_conv_pack_weights");
 }
 
 spk_status conv_fire_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,

@@ -224,18 +224,45 @@ __host__ __device__ inline void group_rows(const PGeom &g, int p0, int p1, int &
 
 // ------------------------------------------------------------------ packing
 
-// Blocks [0, B*Hp): one padded input row (b, py) each, transposed through LDS
-// from channel rows to channels-last, times clamped to T; the last of them
-// fills the readable slack.  Blocks [B*Hp, B*Hp + 32*NT): one map o each
+// Blocks [0, nb_in): one padded input row (b, py) each, transposed through
+// LDS from channel rows to channels-last, times clamped to T (a pooled input
+// row is pooled there from the staged window rows); the last of them fills
+// the readable slack.  A pooled input whose rows are too wide to stage runs a
+// grid-stride pass over the Xp bytes instead, each pooling its window from
+// the unpooled map.  Blocks [nb_in, nb_in + 32*NT): one map o each
 // (maps past Co are zero), written as B fragments: lane l holds map o (l % 32)
 // and taps 8*(l/32)..+7 of a slice.
 template <int NP, bool kHalfW>
 __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
                                                  const void *__restrict__ wv, PGeom g, int nb_in,
-                                                 uint8_t *__restrict__ xp, h8 *__restrict__ bp)
+                                                 uint8_t *__restrict__ xp, h8 *__restrict__ bp,
+                                                 spk::PoolIn pool)
 {
     extern __shared__ __align__(16) uint8_t sm[];
     const uint8_t never = (uint8_t)g.T;
+    if ((int)blockIdx.x < nb_in && pool.src && pool.stage < 0) {
+        // pooled input too wide to stage: each thread writes Xp bytes
+        // (b, py, px, c), the pooling window read from the unpooled map; the
+        // Xp body is below 2^30 bytes
+        const uint32_t body = (uint32_t)g.B * g.Hp * g.rowb, total = body + (uint32_t)g.slack;
+        for (uint32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (uint32_t)nb_in * blockDim.x) {
+            uint32_t v = never;
+            if (e < body) {
+                const uint32_t rowi = e / (uint32_t)g.rowb, within = e - rowi * (uint32_t)g.rowb;
+                const int b = (int)(rowi / (uint32_t)g.Hp), py = (int)(rowi - (uint32_t)b * g.Hp);
+                const int px = (int)(within / (uint32_t)g.Cp), c = (int)within - px * g.Cp;
+                const int iy = py - g.pad, ix = px - g.pad;
+                if ((unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi && c < g.Ci) {
+                    const long long plane = (long long)b * g.Ci + c;
+                    const uint32_t t = spk::pool_cell(pool, plane, iy, ix);
+                    if (pool.pooled) pool.pooled[(plane * g.Hi + iy) * g.Wi + ix] = (uint8_t)t;
+                    v = min(t, (uint32_t)never);
+                }
+            }
+            xp[e] = (uint8_t)v;
+        }
+        return;
+    }
     if ((int)blockIdx.x < nb_in) {
         const int b = blockIdx.x / g.Hp, py = blockIdx.x - b * g.Hp;
         const int iy = py - g.pad;
@@ -243,12 +270,18 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
         if ((unsigned)iy < (unsigned)g.Hi) {
             for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = never;
             __syncthreads();
-            const uint8_t *src = in + (size_t)b * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi;
-            const int n = g.Ci * g.Wi;
-            for (int e = threadIdx.x; e < n; e += blockDim.x) {
-                const int c = e / g.Wi, x = e - c * g.Wi;
-                const uint8_t v = src[(size_t)c * g.Hi * g.Wi + x];
-                sm[(x + g.pad) * g.Cp + c] = v < never ? v : never;
+            auto put = [&](int c, int x, uint8_t v) { sm[(x + g.pad) * g.Cp + c] = v < never ? v : never; };
+            if (pool.src) {
+                // the input row is pooled here (and kept when asked for)
+                spk::pool_row(pool, (long long)b * g.Ci, g.Ci, g.Hi, g.Wi, iy,
+                              reinterpret_cast<uint32_t *>(sm + pool.stage), put);
+            } else {
+                const uint8_t *src = in + (size_t)b * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi;
+                const int n = g.Ci * g.Wi;
+                for (int e = threadIdx.x; e < n; e += blockDim.x) {
+                    const int c = e / g.Wi, x = e - c * g.Wi;
+                    put(c, x, src[(size_t)c * g.Hi * g.Wi + x]);
+                }
             }
             __syncthreads();
             for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = sm[e];
@@ -966,19 +999,30 @@ size_t conv_pt_workspace(int B, int T, int Ci, int Hi, int Wi, int Co, int Kh, i
 
 spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi, const void *w,
                         bool half_w, int Co, int Kh, int Kw, int stride, int pad, int Ho, int Wo,
-                        float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s)
+                        float theta, uint8_t *out_t, float *out_v, void *ws, hipStream_t s,
+                        const PoolIn *pool)
 {
     PGeom g = make_pgeom(B, T, Ci, Hi, Wi, Co, Kh, Kw, stride, pad, Ho, Wo, half_w);
     g.SKp = packed_sk(g.SK, half_w);
     uint8_t *xp = reinterpret_cast<uint8_t *>(ws);
     h8 *bp = reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
-    const int nb_in = g.B * g.Hp;
-    const size_t plds = std::max((size_t)g.rowb, (size_t)g.Ci * g.Kh * g.Kw * sizeof(float));
+    // a pooled input row stages its window rows past the row buffer when
+    // they fit; otherwise its cells are pooled one by one
+    PoolIn pl = pool ? *pool : PoolIn{};
+    pl.stage = -1;
+    const size_t stage_at = align_up((size_t)g.rowb, 16);
+    if (pool && stage_at + pool_stage_bytes(pl, g.Ci) <= 64 * 1024) pl.stage = (int)stage_at;
+    // input blocks: one per padded row, or 1024 Xp bytes each (cells pooled one by one)
+    const int nb_in = pool && pl.stage < 0 ? ceil_div((long long)g.B * g.Hp * g.rowb + g.slack, 1024)
+                                           : g.B * g.Hp;
+    const size_t wlds = (size_t)g.Ci * g.Kh * g.Kw * sizeof(float);
+    const size_t plds = std::max(wlds, !pool ? (size_t)g.rowb
+                                       : pl.stage >= 0 ? stage_at + pool_stage_bytes(pl, g.Ci) : (size_t)0);
     const dim3 pgrid(nb_in + g.NT * 32);
     if (half_w)
-        hipLaunchKernelGGL((k_pack_pt<1, true>), pgrid, dim3(256), plds, s, in, w, g, nb_in, xp, bp);
+        hipLaunchKernelGGL((k_pack_pt<1, true>), pgrid, dim3(256), plds, s, in, w, g, nb_in, xp, bp, pl);
     else
-        hipLaunchKernelGGL((k_pack_pt<2, false>), pgrid, dim3(256), plds, s, in, w, g, nb_in, xp, bp);
+        hipLaunchKernelGGL((k_pack_pt<2, false>), pgrid, dim3(256), plds, s, in, w, g, nb_in, xp, bp, pl);
     SPK_LAUNCHED("spk_conv_fire");
 
     const int nranges = n_ranges(g);

@@ -25,6 +25,16 @@ class LayerState:
     spec: wls.ConvSpec
     w: torch.Tensor                       # float32 master
     w16: torch.Tensor | None = None       # half operand (f16 layers)
+    packed: torch.Tensor | None = None    # readout layers: the operand as packed B fragments
+
+    @property
+    def w_op(self) -> torch.Tensor:
+        return self.w16 if self.w16 is not None else self.w
+
+    def repack(self):
+        """Rebuild the packed fragments after the weights changed."""
+        if self.packed is not None:
+            spk.spk_conv_pack_weights(self.w_op, out=self.packed)
 
 
 @dataclass
@@ -63,7 +73,10 @@ class Pipeline:
         for li, spec in enumerate(wl.convs, start=1):
             w = torch.from_numpy(wls.make_weights(wl, li)).to(self.device)
             w16 = w.to(torch.float16) if spec.w_dtype == "f16" else None
-            self.layers.append(LayerState(spec, w, w16))
+            layer = LayerState(spec, w, w16)
+            if spec.readout and wl.coding == "rank":
+                layer.packed = spk.spk_conv_pack_weights(layer.w_op)
+            self.layers.append(layer)
         self.labels = torch.from_numpy(wls.make_labels(wl)).to(self.device) if wl.rstdp_group else None
         self.base_cfgs = [(c.a_causal, c.a_anticausal, c.lower, c.upper, c.stabilize) for c in wl.stdp]
         self.cfgs = list(self.base_cfgs)
@@ -91,6 +104,7 @@ class Pipeline:
         for layer in self.layers:
             if layer.spec.stdp:
                 spk.spk_quantize(layer.w, lower, mid, upper, w_f16=layer.w16)
+                layer.repack()
 
     def snapshot_weights(self):
         return [(l.w.clone(), None if l.w16 is None else l.w16.clone()) for l in self.layers]
@@ -100,6 +114,7 @@ class Pipeline:
             l.w.copy_(w)
             if w16 is not None:
                 l.w16.copy_(w16)
+            l.repack()
 
     def step(self, keep: bool = False, learn: bool = True, timers: dict | None = None,
              only: set | None = None, gate=None, reps: int = 1) -> StepOutputs | None:
@@ -128,7 +143,8 @@ class Pipeline:
             t = self.spike_input
         li = 0
         pi = 0
-        for kind, s in wl.stages:
+        pending = None  # a pool whose conv runs next pools inside that conv's call
+        for si, (kind, s) in enumerate(wl.stages):
             if kind == "gather":
                 feats = timed("gather", lambda: spk.spk_gather(t, wl.T))
                 if keep:
@@ -136,12 +152,15 @@ class Pipeline:
                 continue
             if kind == "pool":
                 pi += 1
+                if si + 1 < len(wl.stages) and wl.stages[si + 1][0] == "conv":
+                    pending = s
+                    continue
                 t = timed(f"pool{pi}", lambda: spk.spk_pool(t, s.k, s.stride, s.pad))
                 if keep:
                     out.pooled.append(t)
                 continue
             layer = self.layers[li]
-            w_op = layer.w16 if layer.w16 is not None else layer.w
+            w_op = layer.w_op
             n = li + 1
             if t is None:
                 sp, off = self.spike_list
@@ -149,6 +168,20 @@ class Pipeline:
                     sp, off, wl.input_chw(), w_op, wl.T, s.stride, s.pad, s.theta))
                 if (s.stdp and learn) or keep:
                     t = timed("unpack", lambda: spk.spk_spikes_to_times(sp, off, wl.input_chw(), wl.T))
+            elif pending is not None:
+                pl = pending
+                pending = None
+                keep_in = keep or (s.stdp and learn)
+                res = timed(f"conv{n}", lambda: spk.spk_pool_conv_fire(
+                    t, (pl.k, pl.stride, pl.pad), w_op, wl.T, s.stride, s.pad, s.theta,
+                    packed_w=layer.packed, keep_pooled=keep_in))
+                if keep_in:
+                    t, tf, vk = res
+                    if keep:
+                        out.pooled.append(t)
+                else:
+                    tf, vk = res
+                    t = None
             else:
                 tf, vk = timed(f"conv{n}", lambda: spk.spk_conv_fire(t, w_op, wl.T, s.stride, s.pad,
                                                                      s.theta))
@@ -170,6 +203,8 @@ class Pipeline:
                     timed(f"stdp{n}", lambda: spk.spk_stdp_update(
                         layer.w, t, win, nw, self.cfgs, s.stride, s.pad, winner_cfg=wc,
                         w_f16=layer.w16))
+                    if layer.packed is not None:
+                        timed(f"pack{n}", layer.repack)
             t = tf
             li += 1
         if learn:
@@ -259,7 +294,10 @@ class RatePipeline:
         for li, spec in enumerate(wl.convs, start=1):
             w = torch.from_numpy(wls.make_weights(wl, li)).to(self.device)
             w16 = w.to(torch.float16) if spec.w_dtype == "f16" else None
-            self.layers.append(LayerState(spec, w, w16))
+            layer = LayerState(spec, w, w16)
+            if spec.readout and wl.coding == "rank":
+                layer.packed = spk.spk_conv_pack_weights(layer.w_op)
+            self.layers.append(layer)
         self.filters = [(f.ksize, f.sigma1, f.sigma2) for f in wl.dog]
 
     def step(self, keep: bool = False, timers: dict | None = None, only: set | None = None, gate=None,

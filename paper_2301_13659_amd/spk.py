@@ -59,6 +59,11 @@ _SIGNATURES = {
     "spk_conv_fire_noalloc": ([_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P,
                                _P], _I),
     "spk_pool": ([_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P], _I),
+    "spk_pool_conv_fire_workspace_size": ([_I] * 14 + [_F], _Z),
+    "spk_pool_conv_fire": ([_P] + [_I] * 9 + [_P, _P, _I, _P] + [_I] * 5 + [_F, _P, _P, _P, _Z, _P],
+                           _I),
+    "spk_conv_packed_weights_size": ([_I] * 5, _Z),
+    "spk_conv_pack_weights": ([_P, _I, _I, _I, _I, _I, _P, _Z, _P], _I),
     "spk_inhibit_winners_workspace_size": ([_I, _I, _I, _I], _Z),
     "spk_inhibit_winners": ([_P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _Z, _P],
                             _I),
@@ -273,6 +278,65 @@ def spk_conv_fire_noalloc(in_times, w, T: int, stride: int = 1, pad: int = 0,
                                    pad, float(theta), _ptr(out_times), _ptr(out_vkey), None,
                                    _stream(dev)))
     return out_times, out_vkey
+
+
+def spk_pool_conv_fire(in_times, pool, w, T: int, stride: int = 1, pad: int = 0,
+                       theta: float = math.inf, packed_w=None, keep_pooled: bool = True,
+                       out_times=None, out_vkey=None):
+    """Max-pooling then spk_conv_fire in one call.  pool: (k, stride, pad) of
+    a square window (k may be a (kh, kw) pair).  packed_w: optional uint8
+    tensor from spk_conv_pack_weights(w).  Returns (pooled, times, vkey), or
+    (times, vkey) with keep_pooled=False."""
+    _dev(in_times, torch.uint8, "in_times", 4)
+    if w.dtype not in (torch.float32, torch.float16):
+        raise ValueError("w: expected float32 or float16")
+    _dev(w, w.dtype, "w", 4)
+    k, pstride, ppad = pool
+    pkh, pkw = (k, k) if isinstance(k, int) else k
+    B, Ci, H0, W0 = in_times.shape
+    Co, Ci2, Kh, Kw = w.shape
+    if Ci != Ci2:
+        raise ValueError(f"w has {Ci2} input channels, input has {Ci}")
+    L = load()
+    Hi, Wi = L.spk_out_extent(H0, pkh, pstride, ppad), L.spk_out_extent(W0, pkw, pstride, ppad)
+    Ho = L.spk_out_extent(Hi, Kh, stride, pad) if Hi > 0 else -1
+    Wo = L.spk_out_extent(Wi, Kw, stride, pad) if Wi > 0 else -1
+    dev = in_times.device
+    pooled = _empty((B, Ci, max(Hi, 1), max(Wi, 1)), dtype=torch.uint8, device=dev) if keep_pooled else None
+    if out_times is None:
+        out_times = _empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.uint8, device=dev)
+    if out_vkey is None:
+        out_vkey = _empty((B, Co, max(Ho, 1), max(Wo, 1)), dtype=torch.float32, device=dev)
+    _dev(out_times, torch.uint8, "out_times", 4)
+    _dev(out_vkey, torch.float32, "out_vkey", 4)
+    if packed_w is not None:
+        _dev(packed_w, torch.uint8, "packed_w", 1)
+    nbytes = L.spk_pool_conv_fire_workspace_size(B, T, Ci, H0, W0, pkh, pkw, pstride, ppad, Co, Kh, Kw,
+                                                 stride, pad, float(theta))
+    ws = _workspace(nbytes, dev)
+    dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
+    _check(L.spk_pool_conv_fire(_ptr(in_times), B, T, Ci, H0, W0, pkh, pkw, pstride, ppad,
+                                _ptr(pooled), _ptr(w), dt, _ptr(packed_w), Co, Kh, Kw, stride, pad,
+                                float(theta), _ptr(out_times), _ptr(out_vkey), _ptr(ws), nbytes,
+                                _stream(dev)))
+    return (pooled, out_times, out_vkey) if keep_pooled else (out_times, out_vkey)
+
+
+def spk_conv_pack_weights(w, out=None):
+    """The weights as the readout kernel's B fragments (a flat uint8 tensor)."""
+    if w.dtype not in (torch.float32, torch.float16):
+        raise ValueError("w: expected float32 or float16")
+    _dev(w, w.dtype, "w", 4)
+    Co, Ci, Kh, Kw = w.shape
+    L = load()
+    dt = SPK_F16 if w.dtype == torch.float16 else SPK_F32
+    n = L.spk_conv_packed_weights_size(Co, Ci, Kh, Kw, dt)
+    if out is None:
+        out = _empty((max(n, 1),), dtype=torch.uint8, device=w.device)
+    _dev(out, torch.uint8, "out", 1)
+    _check(L.spk_conv_pack_weights(_ptr(w), dt, Co, Ci, Kh, Kw, _ptr(out), out.numel(),
+                                   _stream(w.device)))
+    return out
 
 
 def spk_pool(in_times, k, stride: int | None = None, pad: int = 0, out=None):

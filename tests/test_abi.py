@@ -91,6 +91,51 @@ def test_conv_fire_validation():
     _err(call(args(theta=math.nan)), spk.SPK_E_ARG, "NaN")
 
 
+def test_pool_conv_fire_and_pack_weights_validation():
+    L = spk.load()
+    F32, F16 = spk.SPK_F32, spk.SPK_F16
+
+    def call(B=2, T=15, Ci=30, H0=28, W0=28, pk=2, pw=2, ps=2, pp=0, packed=None, Co=250, K=3,
+             s=1, p=1, theta=10.0, ws=P1, nbytes=1 << 30, w=P1, src=P1):
+        return L.spk_pool_conv_fire(src, B, T, Ci, H0, W0, pk, pw, ps, pp, None, w, F32, packed, Co,
+                                    K, K, s, p, theta, P1, P1, ws, nbytes, None)
+    _err(call(src=None), spk.SPK_E_ARG, "NULL")
+    _err(call(w=None), spk.SPK_E_ARG, "NULL")
+    _err(call(ps=0), spk.SPK_E_ARG, "positive")
+    _err(call(pk=30), spk.SPK_E_SHAPE, "no pooled output")
+    _err(call(packed=ctypes.c_void_p(256 + 8)), spk.SPK_E_ARG, "aligned")
+    _err(call(T=300), spk.SPK_E_SHAPE, "T=")
+    _err(call(K=20, p=0), spk.SPK_E_SHAPE, "no output")
+    _err(call(theta=math.nan), spk.SPK_E_ARG, "NaN")
+    _err(call(ws=ctypes.c_void_p(256 + 16)), spk.SPK_E_ARG, "aligned")
+    need = L.spk_pool_conv_fire_workspace_size(2, 15, 30, 28, 28, 2, 2, 2, 0, 250, 3, 3, 1, 1, 10.0)
+    conv = L.spk_conv_fire_workspace_size(2, 15, 30, 14, 14, 250, 3, 3, 1, 1, 10.0, 0)
+    # the conv's own workspace, then room for a pooled map
+    assert need == (conv + 255) // 256 * 256 + (2 * 30 * 14 * 14 + 255) // 256 * 256
+    _err(call(nbytes=need - 1), spk.SPK_E_WORKSPACE, "workspace")
+    assert L.spk_pool_conv_fire_workspace_size(2, 15, 30, 28, 28, 40, 40, 1, 0, 250, 3, 3, 1, 1,
+                                               10.0) == 0
+
+    # B fragments of the three-layer net's readout: 7 tiles of 32 maps, 5 kernel
+    # rows of 5 x 264 taps (250 channels padded to 33 x 8) = 413 slices of 16
+    assert L.spk_conv_packed_weights_size(200, 250, 5, 5, F32) == 7 * 413 * 2 * 64 * 16
+    assert L.spk_conv_packed_weights_size(200, 250, 5, 5, F16) == 7 * 413 * 1 * 64 * 16
+    # 16 channels -> 24: 3 rows of 72 taps = 14 slices
+    assert L.spk_conv_packed_weights_size(40, 16, 3, 3, F32) == 2 * 14 * 2 * 64 * 16
+    assert L.spk_conv_packed_weights_size(1, 3, 1, 1, F16) == 1 * 1 * 1 * 64 * 16
+    assert L.spk_conv_packed_weights_size(200, 250, 5, 5, 7) == 0
+    assert L.spk_conv_packed_weights_size(0, 250, 5, 5, F32) == 0
+    n = L.spk_conv_packed_weights_size(200, 250, 5, 5, F32)
+    _err(L.spk_conv_pack_weights(None, F32, 200, 250, 5, 5, P1, n, None), spk.SPK_E_ARG, "NULL")
+    _err(L.spk_conv_pack_weights(P1, 9, 200, 250, 5, 5, P1, n, None), spk.SPK_E_UNSUPPORTED, "dtype")
+    _err(L.spk_conv_pack_weights(P1, F32, 200, 250, 5, 5, P1, n - 1, None), spk.SPK_E_WORKSPACE,
+         "needed")
+    _err(L.spk_conv_pack_weights(P1, F32, 200, 250, 5, 5, ctypes.c_void_p(264), n, None),
+         spk.SPK_E_ARG, "aligned")
+    _err(L.spk_conv_pack_weights(P1, F32, 2, 2000, 3, 3, P1, 1 << 30, None), spk.SPK_E_SHAPE, "taps")
+    _err(L.spk_conv_pack_weights(P1, F32, 0, 250, 5, 5, P1, n, None), spk.SPK_E_ARG, "positive")
+
+
 def test_pool_inhibit_stdp_validation():
     L = spk.load()
     _err(L.spk_pool(P1, 1, 1, 2, 2, 3, 3, 1, 0, P1, None), spk.SPK_E_SHAPE, "no output")
@@ -131,6 +176,19 @@ def test_conv_fire_planning_survives_every_layer_shape():
         st = L.spk_conv_fire(P1, B, T, Ci, H, W, P1, 0, Co, K, K, 1, pad, theta, P1, P1, None,
                              P1 if ws else None, ws, None)
         assert st == spk.SPK_E_HIP, spk.load().spk_last_error()
+    # and with the pooling in front: (B, T, Ci, H0, W0, pool k, stride, pad, Co, K, pad, theta, packed)
+    pooled = [(64, 15, 30, 28, 28, 2, 2, 0, 250, 3, 1, 10.0, None),
+              (64, 15, 250, 14, 14, 3, 3, 1, 200, 5, 2, math.inf, P1),
+              (32, 30, 4, 160, 250, 7, 6, 0, 20, 17, 0, 42.0, None),
+              (2, 40, 8, 12, 12, 2, 2, 1, 20, 3, 1, 5.0, None)]
+    for B, T, Ci, H0, W0, pk, ps, pp, Co, K, pad, theta, packed in pooled:
+        ws = L.spk_pool_conv_fire_workspace_size(B, T, Ci, H0, W0, pk, pk, ps, pp, Co, K, K, 1, pad,
+                                                 theta)
+        st = L.spk_pool_conv_fire(P1, B, T, Ci, H0, W0, pk, pk, ps, pp, P1, P1, 0, packed, Co, K, K,
+                                  1, pad, theta, P1, P1, P1, ws, None)
+        assert st == spk.SPK_E_HIP, spk.load().spk_last_error()
+    n = L.spk_conv_packed_weights_size(200, 250, 5, 5, 0)
+    assert L.spk_conv_pack_weights(P1, 0, 200, 250, 5, 5, P1, n, None) == spk.SPK_E_HIP
 
 
 def test_fc_validation():

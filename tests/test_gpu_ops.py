@@ -234,6 +234,80 @@ def test_pool_bit_exact(shape, k, s, p):
     np.testing.assert_array_equal(got, oracle.pool(times, k, s, p))
 
 
+# ------------------------------------------------------------ pool + conv
+
+POOL_CONV_CASES = [
+    # B, Ci, H0, W0, (pool k, stride, pad), Co, K, stride, pad, T, theta, density, dtype
+    (4, 30, 28, 28, (2, 2, 0), 250, 3, 1, 1, 15, 10.0, 0.3, "f32"),    # three-layer net, conv2
+    (3, 250, 14, 14, (3, 3, 1), 200, 5, 1, 2, 15, math.inf, 0.3, "f32"),  # and its readout
+    (2, 40, 11, 13, (2, 2, 0), 24, 3, 1, 1, 9, math.inf, 0.5, "f16"),  # half readout, ragged
+    (2, 4, 160, 250, (7, 6, 0), 20, 17, 1, 0, 30, 42.0, 0.05, "f32"),  # large-image conv2
+    (2, 8, 12, 12, ((2, 3), 2, 1), 20, 3, 1, 1, 40, 5.0, 0.3, "f32"),  # 2 x 3 window, T = 40
+    (2, 5, 9, 9, (1, 1, 0), 7, 3, 1, 1, 5, 2.0, 0.3, "f32"),           # 1 x 1 window: identity
+]
+
+
+@pytest.mark.parametrize("case", POOL_CONV_CASES)
+def test_pool_conv_fire_equals_pool_then_conv(case):
+    """spk_pool_conv_fire pools inside the conv's packing pass (or with the
+    pool kernel in front, on the paths that do not pack): its pooled map and
+    outputs are bit-identical to spk_pool followed by spk_conv_fire, and they
+    match the oracle's pool and conv."""
+    dev = gpu()
+    B, Ci, H0, W0, (pk, ps, pp), Co, K, s, p, T, theta, dens, dt = case
+    rng = np.random.default_rng(B * 1000 + Ci * 10 + K + 7)
+    times0 = random_times(rng, (B, Ci, H0, W0), T, dens)
+    w = rng.uniform(0.0, 1.0, size=(Co, Ci, K, K)).astype(np.float32)
+    if dt == "f16":
+        w = w.astype(np.float16).astype(np.float32)
+    w_dev = _t(w, dev).to(torch.float16) if dt == "f16" else _t(w, dev)
+    t0 = _t(times0, dev)
+    ref_pooled = spk.spk_pool(t0, pk, ps, pp)
+    ref_tf, ref_vk = spk.spk_conv_fire(ref_pooled, w_dev, T, s, p, theta)
+    pooled, tf, vk = spk.spk_pool_conv_fire(t0, (pk, ps, pp), w_dev, T, s, p, theta)
+    np.testing.assert_array_equal(np_(pooled), np_(ref_pooled))
+    np.testing.assert_array_equal(np_(tf), np_(ref_tf))
+    np.testing.assert_array_equal(np_(vk), np_(ref_vk))
+    tf1, vk1 = spk.spk_pool_conv_fire(t0, (pk, ps, pp), w_dev, T, s, p, theta, keep_pooled=False)
+    np.testing.assert_array_equal(np_(tf1), np_(ref_tf))
+    np.testing.assert_array_equal(np_(vk1), np_(ref_vk))
+    if math.isinf(theta):
+        # readout weights packed once, then read on every call
+        packed = spk.spk_conv_pack_weights(w_dev)
+        for _ in range(2):
+            tf2, vk2 = spk.spk_pool_conv_fire(t0, (pk, ps, pp), w_dev, T, s, p, theta,
+                                              packed_w=packed, keep_pooled=False)
+            np.testing.assert_array_equal(np_(tf2), np_(ref_tf))
+            np.testing.assert_array_equal(np_(vk2), np_(ref_vk))
+    # and the oracle, from the raw map
+    o_pooled = oracle.pool(times0, pk, ps, pp)
+    np.testing.assert_array_equal(np_(pooled), o_pooled)
+    o_tf, o_vk, o_V = oracle.conv_fire(o_pooled, w, T, s, p, theta, potentials=True)
+    if math.isinf(theta):
+        assert np.all(np_(tf) == NEVER)
+        check_potentials(np_(vk), o_vk, "readout v_key")
+    else:
+        check_fire(np_(tf), np_(vk), o_tf, o_vk, excused_from_potentials(o_V, theta))
+
+
+def test_packed_weights_follow_weight_updates():
+    """A readout layer whose weights change: the packed fragments are rebuilt
+    after the change and the readout matches a call that packs w itself."""
+    dev = gpu()
+    rng = np.random.default_rng(5)
+    times0 = random_times(rng, (2, 250, 14, 14), 15, 0.3)
+    w = _t(rng.uniform(0.0, 1.0, size=(200, 250, 5, 5)).astype(np.float32), dev)
+    t0 = _t(times0, dev)
+    packed = spk.spk_conv_pack_weights(w)
+    w.mul_(0.5).add_(0.25)
+    spk.spk_conv_pack_weights(w, out=packed)
+    tf, vk = spk.spk_pool_conv_fire(t0, (3, 3, 1), w, 15, 1, 2, math.inf, packed_w=packed,
+                                    keep_pooled=False)
+    ref_tf, ref_vk = spk.spk_pool_conv_fire(t0, (3, 3, 1), w, 15, 1, 2, math.inf, keep_pooled=False)
+    np.testing.assert_array_equal(np_(tf), np_(ref_tf))
+    np.testing.assert_array_equal(np_(vk), np_(ref_vk))
+
+
 # ------------------------------------------------------- inhibition + k-WTA
 
 def test_inhibit_wta_hand_example():
