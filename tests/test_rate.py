@@ -136,6 +136,7 @@ RATE_CASES = [
     (1, 20, 3, 11, 9, 70, 3, 2, 1, 1.5, 0.4, "f16"),
     (2, 16, 8, 7, 7, 33, 1, 1, 0, 0.9, 0.5, "q8"),
     (1, 9, 40, 6, 5, 20, 3, 1, 1, 3.0, 0.3, "q8"),
+    (1, 6, 4, 120, 110, 20, 3, 1, 1, 3.0, 0.3, "bin"),   # 52.8 KB frames: copied pixel by pixel
 ]
 
 
