@@ -462,8 +462,31 @@ __device__ __forceinline__ void write_out(const PGeom &g, int nt, int gs, int p_
     }
 }
 
+// Rows of a tile: output element e of a lane in wave half hh is row
+// 8*(e/4) + 4*hh + e%4.  The A fragment of row r is given the position slot
+// and step below.  TP = 16 and 8: each lane's elements are whole runs of
+// steps in order (TP = 16, slot hh, element e = step e; TP = 8, slot hh for
+// e < 8 and 2 + hh for e >= 8, step e % 8), so no lane needs the other half's
+// results.  TP = 32: step r, the two halves' elements interleaved.
+__device__ __forceinline__ void row_slot_step(int r, int lgTP, int &pl, int &tt)
+{
+    const int hi = r >> 3, half = (r >> 2) & 1, lo = r & 3;
+    if (lgTP == 3) {
+        pl = 2 * (hi >> 1) + half;
+        tt = ((hi & 1) << 2) | lo;
+    } else if (lgTP == 4) {
+        pl = half;
+        tt = (hi << 2) | lo;
+    } else {
+        pl = 0;
+        tt = r;
+    }
+}
+
 // Merge the two wave halves of one position slot (ft: step or NEVER; last:
-// the potential at step T-1, meaningful in the upper half only).
+// the potential at step T-1, meaningful in the upper half only).  Each swap
+// leaves both halves' values in every lane; min and sum do not depend on
+// their order.
 __device__ __forceinline__ void merge_halves(uint32_t ft, float fv, float last, int hh, uint32_t &tf,
                                              float &vk)
 {
@@ -472,7 +495,6 @@ __device__ __forceinline__ void merge_halves(uint32_t ft, float fv, float last, 
     const auto v2 = __builtin_amdgcn_permlane32_swap(fb, fb, false, false);
     const uint32_t lb = __builtin_bit_cast(uint32_t, hh ? last : 0.0f);
     const auto l2 = __builtin_amdgcn_permlane32_swap(lb, lb, false, false);
-    // every lane now holds both halves' values (in either order): x + 0 = x
     const uint32_t t0 = t2[0], t1 = t2[1];
     const float f0 = __builtin_bit_cast(float, (uint32_t)v2[0]);
     const float f1 = __builtin_bit_cast(float, (uint32_t)v2[1]);
@@ -482,29 +504,58 @@ __device__ __forceinline__ void merge_halves(uint32_t ft, float fv, float last, 
     vk = tf < (uint32_t)spk::kNever ? fsel : vl;
 }
 
-// Epilogue of a tile with TP steps per position: element e of a lane is row
-// 8*(e/4) + 4*hh + e%4 (steps ascend with e), map lane % 32.  Per position
-// slot (TP/2 elements per lane): the first element above theta, then the two
-// wave halves merged into the spike time and key potential.
+// First element in [e0, e0 + n) above theta (as an offset) and its value;
+// n when there is none.
+__device__ __forceinline__ void first_above(const f16v &acc, int e0, int n, float theta, int &fe, float &fv)
+{
+    fe = n;
+    fv = 0.0f;
+#pragma unroll
+    for (int e = 15; e >= 0; e--) {
+        if (e < e0 || e >= e0 + n) continue;
+        const bool c = acc[e] > theta;
+        fe = c ? e - e0 : fe;
+        fv = c ? acc[e] : fv;
+    }
+}
+
+// Epilogue of a tile with TP steps per position (rows past T - 1 repeat step
+// T - 1, so the last element of a run is the potential at T - 1): the spike
+// time (or NEVER) and key potential of each position slot this lane holds,
+// for its map lane % 32.  TP = 8: slots hh and 2 + hh (st/sv[0], [1]); TP =
+// 16: slot hh; TP = 32: the one slot, the two wave halves merged, in every
+// lane.
 template <int TP>
 __device__ __forceinline__ void tile_epilogue(const f16v &acc, float theta, int hh, uint32_t *st, float *sv)
 {
-    constexpr int EP = TP / 2;
+    if constexpr (TP == 8 || TP == 16) {
 #pragma unroll
-    for (int k = 0; k < 32 / TP; k++) {
-        int fe = 16;
-        float fv = 0.0f;
-#pragma unroll
-        for (int e = (k + 1) * EP - 1; e >= k * EP; e--) {
-            const bool c = acc[e] > theta;
-            fe = c ? e : fe;
-            fv = c ? acc[e] : fv;
+        for (int k = 0; k < 16 / TP; k++) {
+            int fe;
+            float fv;
+            first_above(acc, k * TP, TP, theta, fe, fv);
+            st[k] = fe < TP ? (uint32_t)fe : (uint32_t)spk::kNever;
+            sv[k] = fe < TP ? fv : acc[k * TP + TP - 1];
         }
-        const uint32_t ft = fe < 16 ? (uint32_t)((((fe >> 2) << 3) + 4 * hh + (fe & 3)) & (TP - 1))
-                                    : (uint32_t)spk::kNever;
-        merge_halves(ft, fv, acc[(k + 1) * EP - 1], hh, st[k], sv[k]);
+    } else {
+        // the first element above theta and its step (row 8*(e/4) + 4*hh +
+        // e%4), then the minimum over the two halves through lane swaps
+        int fe;
+        float fv;
+        first_above(acc, 0, 16, theta, fe, fv);
+        const uint32_t ft = fe < 16 ? (uint32_t)(((fe >> 2) << 3) + 4 * hh + (fe & 3)) : (uint32_t)spk::kNever;
+        const float last = acc[15];  // row 31: step T - 1, in the upper half
+        merge_halves(ft, fv, last, hh, st[0], sv[0]);
     }
 }
+
+// Position slots of the tile a lane stores (see tile_epilogue): count and
+// slot of entry k.
+__device__ __forceinline__ int slots_held(int lgTP, int hh)
+{
+    return lgTP == 3 ? 2 : (lgTP == 4 ? 1 : (hh == 0 ? 1 : 0));
+}
+__device__ __forceinline__ int slot_of(int lgTP, int hh, int k) { return lgTP == 3 ? 2 * k + hh : (lgTP == 4 ? hh : 0); }
 
 // SK: slices of the instance (all in registers), NP: 2 = hi/lo products of a
 // float master, 1 = half weights; kMode: alignment of the window runs; QC:
@@ -561,7 +612,8 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
     // row (p, t) of this lane: slot p = r / TP, step t = r % TP (capped at T - 1)
     const int r = lane & 31, hh = lane >> 5;
     const int lgTP = TPC == 8 ? 3 : (TPC == 16 ? 4 : (TPC == 32 ? 5 : g.lgTP));
-    const int pl = r >> lgTP, tt = r & ((1 << lgTP) - 1);
+    int pl, tt;
+    row_slot_step(r, lgTP, pl, tt);
     const uint32_t cbv = 0x6401u + (uint32_t)min(tt, g.T - 1);
     const h2 cc = as_h2(cbv | (cbv << 16));
     const int PT = 32 >> lgTP;  // positions per tile
@@ -671,20 +723,18 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
             }
             // the next tile's window origin, read while this one finishes
             if (tp0 + wstep < wp1) xo_next = tab[min(tp0 + wstep - gs + pl, cnt - 1)].xoff;
-            uint32_t st[4] = {0u, 0u, 0u, 0u};
-            float sv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            uint32_t st[2] = {0u, 0u};
+            float sv[2] = {0.0f, 0.0f};
             if (lgTP == 3) tile_epilogue<8>(acc, theta, hh, st, sv);
             else if (lgTP == 4) tile_epilogue<16>(acc, theta, hh, st, sv);
             else tile_epilogue<32>(acc, theta, hh, st, sv);
-            const int o = lane & 31;
-            if (hh == 0) {
+            const int o = lane & 31, ns = slots_held(lgTP, hh);
 #pragma unroll
-                for (int k = 0; k < 4; k++) {
-                    const int pi = tp0 - gs + k;
-                    if (k < PT && pi < cnt) {
-                        stv(cur)[o * kStageStride + pi] = sv[k];
-                        stt(cur)[o * kStageStride + pi] = (uint8_t)st[k];
-                    }
+            for (int k = 0; k < 2; k++) {
+                const int pi = tp0 - gs + slot_of(lgTP, hh, k);
+                if (k < ns && pi < cnt) {
+                    stv(cur)[o * kStageStride + pi] = sv[k];
+                    stt(cur)[o * kStageStride + pi] = (uint8_t)st[k];
                 }
             }
         }
@@ -730,7 +780,8 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
     const h8 *bcol = bp + (size_t)nt * g.SKp * NP * 64 + lane;
 
     const int r = lane & 31, hh = lane >> 5;
-    const int pl = r >> g.lgTP, tt = r & (g.TP - 1);
+    int pl, tt;
+    row_slot_step(r, g.lgTP, pl, tt);
     const uint32_t cbv = 0x6401u + (uint32_t)min(tt, g.T - 1);
     const h2 cc = as_h2(cbv | (cbv << 16));
     const int PT = 32 >> g.lgTP;
@@ -819,19 +870,18 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
             for (int j = 0; j < kRT; j++) {
                 const int ti = t0 + 4 * j;
                 if (ti >= ntiles) continue;
-                uint32_t st[4] = {0u, 0u, 0u, 0u};
-                float sv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                uint32_t st[2] = {0u, 0u};
+                float sv[2] = {0.0f, 0.0f};
                 if (g.lgTP == 3) tile_epilogue<8>(acc[j], theta, hh, st, sv);
                 else if (g.lgTP == 4) tile_epilogue<16>(acc[j], theta, hh, st, sv);
                 else tile_epilogue<32>(acc[j], theta, hh, st, sv);
-                if (hh == 0) {
+                const int ns = slots_held(g.lgTP, hh);
 #pragma unroll
-                    for (int k = 0; k < 4; k++) {
-                        const int pi = ti * PT + k;
-                        if (k < PT && pi < cnt) {
-                            stv(cur)[o * kStageStride + pi] = sv[k];
-                            stt(cur)[o * kStageStride + pi] = (uint8_t)st[k];
-                        }
+                for (int k = 0; k < 2; k++) {
+                    const int pi = ti * PT + slot_of(g.lgTP, hh, k);
+                    if (k < ns && pi < cnt) {
+                        stv(cur)[o * kStageStride + pi] = sv[k];
+                        stt(cur)[o * kStageStride + pi] = (uint8_t)st[k];
                     }
                 }
             }

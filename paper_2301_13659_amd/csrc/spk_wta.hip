@@ -11,6 +11,8 @@
 // sweep the records each round.  Readout layers (no threshold) and calls
 // without pointwise inhibition rank the neurons themselves instead of
 // per-location records.
+#include <algorithm>
+
 #include "spk_internal.h"
 
 namespace {
@@ -580,61 +582,20 @@ __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__
 // with several waves, one exchange through LDS; the lane that owns the
 // winner writes it, and every lane retires its own candidates that share the
 // winner's map or lie in its window.
-template <int NPL, int NW, bool kRec>
-__global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restrict__ times,
-                                                        const float *__restrict__ vkey,
-                                                        const Rec *__restrict__ recs, WtaArgs a,
-                                                        spk_winner *__restrict__ winners,
-                                                        int32_t *__restrict__ n_winners)
+// The k rounds of a sample's winner selection on candidates held in
+// registers (NPL per thread, NW waves): candidate keys kh = time << 32 |
+// order_desc(v) (kNone: not a candidate), ties to the lower kl = map*HW +
+// position; cc, yx, vv: its map, y << 16 | x and potential.
+template <int NPL, int NW>
+__device__ __forceinline__ void select_rounds(uint64_t (&kh)[NPL], const uint32_t (&kl)[NPL],
+                                              const int (&cc)[NPL], const int (&yx)[NPL],
+                                              const float (&vv)[NPL], const WtaArgs &a, int HW, int b,
+                                              uint64_t (&s_hi)[2][NW], uint32_t (&s_lo)[2][NW],
+                                              spk_winner *__restrict__ winners,
+                                              int32_t *__restrict__ n_winners)
 {
-    __shared__ uint64_t s_hi[2][NW];
-    __shared__ uint32_t s_lo[2][NW];
-    const int b = blockIdx.x;
-    const int HW = a.H * a.W;
-    const int n = kRec ? HW : a.C * HW;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint64_t kNone = ~0ull;
-    uint64_t kh[NPL];
-    uint32_t kl[NPL];
-    int cc[NPL], yx[NPL];
-    float vv[NPL];
-    // every candidate load first (clamped index, no branch), then the keys
-    uint32_t tq[NPL];
-#pragma unroll
-    for (int j = 0; j < NPL; j++) {
-        const int ii = min(tid + j * 64 * NW, n - 1);
-        if (kRec) {
-            const Rec r = recs[(size_t)b * HW + ii];
-            tq[j] = r.tc;
-            vv[j] = r.v;
-        } else {
-            const size_t at = (size_t)b * a.C * HW + ii;
-            tq[j] = times[at];
-            vv[j] = vkey[at];
-        }
-    }
-#pragma unroll
-    for (int j = 0; j < NPL; j++) {
-        const int i = tid + j * 64 * NW;
-        const int ii = min(i, n - 1);
-        int t, c, pos;
-        if (kRec) {
-            t = (int)(tq[j] >> 24);
-            c = (int)(tq[j] & 0xFFFFFFu);
-            pos = ii;
-        } else {
-            t = (int)tq[j];
-            c = ii / HW;
-            pos = ii - c * HW;
-        }
-        const bool alive = i < n && (a.readout || t != spk::kNever);
-        const uint32_t tk = a.readout ? 0u : (uint32_t)t;
-        kh[j] = alive ? (((uint64_t)tk << 32) | order_desc(vv[j])) : kNone;
-        kl[j] = (uint32_t)c * (uint32_t)HW + (uint32_t)pos;
-        cc[j] = c;
-        const int y = pos / a.W;
-        yx[j] = (y << 16) | (pos - y * a.W);
-    }
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int count = 0;
     for (int round = 0; round < a.k; round++) {
         uint64_t bh = kNone;
@@ -693,6 +654,64 @@ __global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restric
     if (tid == 0) n_winners[b] = count;
 }
 
+template <int NPL, int NW, bool kRec>
+__global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restrict__ times,
+                                                        const float *__restrict__ vkey,
+                                                        const Rec *__restrict__ recs, WtaArgs a,
+                                                        spk_winner *__restrict__ winners,
+                                                        int32_t *__restrict__ n_winners)
+{
+    __shared__ uint64_t s_hi[2][NW];
+    __shared__ uint32_t s_lo[2][NW];
+    const int b = blockIdx.x;
+    const int HW = a.H * a.W;
+    const int n = kRec ? HW : a.C * HW;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint64_t kNone = ~0ull;
+    uint64_t kh[NPL];
+    uint32_t kl[NPL];
+    int cc[NPL], yx[NPL];
+    float vv[NPL];
+    // every candidate load first (clamped index, no branch), then the keys
+    uint32_t tq[NPL];
+#pragma unroll
+    for (int j = 0; j < NPL; j++) {
+        const int ii = min(tid + j * 64 * NW, n - 1);
+        if (kRec) {
+            const Rec r = recs[(size_t)b * HW + ii];
+            tq[j] = r.tc;
+            vv[j] = r.v;
+        } else {
+            const size_t at = (size_t)b * a.C * HW + ii;
+            tq[j] = times[at];
+            vv[j] = vkey[at];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NPL; j++) {
+        const int i = tid + j * 64 * NW;
+        const int ii = min(i, n - 1);
+        int t, c, pos;
+        if (kRec) {
+            t = (int)(tq[j] >> 24);
+            c = (int)(tq[j] & 0xFFFFFFu);
+            pos = ii;
+        } else {
+            t = (int)tq[j];
+            c = ii / HW;
+            pos = ii - c * HW;
+        }
+        const bool alive = i < n && (a.readout || t != spk::kNever);
+        const uint32_t tk = a.readout ? 0u : (uint32_t)t;
+        kh[j] = alive ? (((uint64_t)tk << 32) | order_desc(vv[j])) : kNone;
+        kl[j] = (uint32_t)c * (uint32_t)HW + (uint32_t)pos;
+        cc[j] = c;
+        const int y = pos / a.W;
+        yx[j] = (y << 16) | (pos - y * a.W);
+    }
+    select_rounds<NPL, NW>(kh, kl, cc, yx, vv, a, HW, b, s_hi, s_lo, winners, n_winners);
+}
+
 template <int NPL, int NW>
 void launch_select_reg(int B, hipStream_t s, const uint8_t *times, const float *vkey,
                        const Rec *recs, const WtaArgs &a, spk_winner *winners, int32_t *n_winners)
@@ -741,6 +760,7 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     hipStream_t s = spk::stream_of(stream);
     const int HW = H * W;
     Rec *recs = (Rec *)ws;
+    WtaArgs a{C, H, W, T, k, radius, readout, pointwise};
     if (pointwise) {
         const long long total = (long long)B * HW;
         Rec *part = reinterpret_cast<Rec *>(reinterpret_cast<char *>(ws) +
@@ -752,7 +772,6 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
                                    s) == hipSuccess,
                     SPK_E_HIP, "spk_inhibit_winners: copy of the time map failed");
     }
-    WtaArgs a{C, H, W, T, k, radius, readout, pointwise};
     // candidates per sample: one record per location after pointwise
     // inhibition, else every neuron
     const long long n_cand = pointwise ? (long long)HW : (long long)C * HW;
