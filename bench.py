@@ -125,7 +125,10 @@ def hbm_stages(wl, pipe, kept, stage_ms):
                          "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
     rate = wl.coding == "rate"
-    if kept.dog is not None:
+    if kept.dog is not None and "dog" not in stage_ms and not rate:
+        # filter bank and coding in one call: image read, times written
+        put("code", pipe.images.numel() + kept.times0.numel())
+    elif kept.dog is not None:
         put("dog", pipe.images.numel() + kept.dog.numel() * 4)
         put("threshold", kept.dog.numel() * 8)
         if rate:  # values, then one draw read and one frame byte written per step

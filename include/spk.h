@@ -133,6 +133,31 @@ spk_status spk_latency_code(const float *x, int B, int C, int H, int W, int T,
                             void *ws, size_t ws_bytes, spk_stream stream);
 
 /*
+ * spk_dog_latency_code -- the network's input stage in one call: DoG
+ * filtering (§II-C.1, as spk_dog_filter) followed by rank-order coding of the
+ * filter outputs (§II-D.2, as spk_latency_code with SPK_CODE_RANK), giving
+ * times bit for bit equal to the two calls in sequence.
+ *   img, filters, pad   as for spk_dog_filter; Ho, Wo its output extent.
+ *   T, min_value        as for spk_latency_code.
+ *   times    uint8 B x (C*F) x Ho x Wo (device) first-spike times.
+ *   dog_out  nullable float B x (C*F) x Ho x Wo (device): also receives the
+ *            filter outputs.
+ *   ws       workspace of spk_dog_latency_code_workspace_size bytes (device,
+ *            256-byte aligned; may be NULL when that size is 0).
+ * When all F kernels fit one coefficient block (sum of K^2 <= 480), a sample
+ * has at most 8192 outputs and its image fits LDS, one kernel does both steps
+ * (one workgroup per sample) and the workspace size is 0; otherwise the two
+ * calls run in sequence, the filter outputs held in dog_out or the workspace.
+ * Errors: those of spk_dog_filter and spk_latency_code, SPK_E_WORKSPACE.
+ */
+size_t spk_dog_latency_code_workspace_size(int B, int C, int H, int W,
+                                           const spk_dog_desc *filters, int F, int pad);
+spk_status spk_dog_latency_code(const uint8_t *img, int B, int C, int H, int W,
+                                const spk_dog_desc *filters, int F, int pad, int T,
+                                float min_value, uint8_t *times, float *dog_out, void *ws,
+                                size_t ws_bytes, spk_stream stream);
+
+/*
  * spk_conv_fire -- spiking convolution with integrate-and-fire, §II-E.1
  * (Eq. 2 for the output size).  For every output neuron (b, o, y, x) and
  * step t, V_t = sum over c, ky, kx of W[o, c, ky, kx] * S_t[b, c, y*stride +

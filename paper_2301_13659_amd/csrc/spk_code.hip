@@ -21,6 +21,7 @@
 //    below).  The working arrays live in the caller workspace.
 #include <cstring>
 
+#include "spk_dog.h"
 #include "spk_internal.h"
 
 namespace {
@@ -160,21 +161,14 @@ __device__ void sort_and_time(uint64_t *src, uint64_t *dst, int N, int T, uint8_
 constexpr int kBk = 4096;
 constexpr int kBkMax = 96;
 
-__global__ __launch_bounds__(kThreads) void k_code_bucket(const float *__restrict__ x, int n, int T,
-                                                          float min_value, uint8_t *__restrict__ times)
+// The ranks of one sample whose values thread tid holds in xv[j] (flat index
+// tid + kThreads * j, for those below n), written to ts.  keys: 2 * n keys of
+// dynamic LDS; cnt, red, mm: the kernel's static LDS.
+__device__ __forceinline__ void bucket_code(const float (&xv)[8], int n, int T, float min_value,
+                                            uint8_t *__restrict__ ts, uint64_t *keys, int *cnt,
+                                            int *red, uint32_t *mm)
 {
-    extern __shared__ uint64_t keys[];  // two buffers of n keys (the second for the sort)
-    __shared__ int cnt[kBk + 1];        // bucket counts, then their first slots
-    __shared__ int red[kThreads / 64];
-    __shared__ uint32_t mm[3];          // lowest and highest value word, largest bucket
-    const int b = blockIdx.x;
-    const float *xs = x + (size_t)b * n;
-    uint8_t *ts = times + (size_t)b * n;
     const int tid = threadIdx.x, lane = tid & 63;
-
-    float xv[8];
-#pragma unroll
-    for (int j = 0; j < 8; j++) xv[j] = xs[min(tid + kThreads * j, n - 1)];  // coalesced, all loads first
     for (int e = tid; e <= kBk; e += kThreads) cnt[e] = 0;
     if (tid == 0) {
         mm[0] = ~0u;
@@ -258,6 +252,79 @@ __global__ __launch_bounds__(kThreads) void k_code_bucket(const float *__restric
         for (int m = s0; m < s1; m++) r += keys[m] < k8[j] ? 1 : 0;
         ts[tid + kThreads * j] = (uint8_t)(((long long)r * T) / N);
     }
+}
+
+__global__ __launch_bounds__(kThreads) void k_code_bucket(const float *__restrict__ x, int n, int T,
+                                                          float min_value, uint8_t *__restrict__ times)
+{
+    extern __shared__ uint64_t keys[];  // two buffers of n keys (the second for the sort)
+    __shared__ int cnt[kBk + 1];        // bucket counts, then their first slots
+    __shared__ int red[kThreads / 64];
+    __shared__ uint32_t mm[3];          // lowest and highest value word, largest bucket
+    const int b = blockIdx.x;
+    const float *xs = x + (size_t)b * n;
+    float xv[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) xv[j] = xs[min((int)threadIdx.x + kThreads * j, n - 1)];  // coalesced, all loads first
+    bucket_code(xv, n, T, min_value, times + (size_t)b * n, keys, cnt, red, mm);
+}
+
+// DoG filtering and rank coding of one sample per block (spk_dog_latency_code;
+// the filters fit one coefficient block, p.fidx[f] = f).  The sample's image
+// is staged in LDS as the filter kernel stages it (u / 255, 0 in the
+// padding), over the rows and columns every filter's window reaches.  Each
+// thread computes runs of kDogRun outputs along a row with the window
+// arithmetic of spk_dog_filter (so the values, and hence the ranks, are
+// those of the two calls in sequence) into an LDS array of the sample's
+// values, from which each thread takes its flat indices for the ranking.
+// The staged image and the values sit in the region the keys use later.
+constexpr int kDogRun = 7;
+
+__host__ __device__ inline int dog_runs(int Wo) { return (Wo + kDogRun - 1) / kDogRun; }
+
+__global__ __launch_bounds__(kThreads) void k_dog_code(const uint8_t *__restrict__ img, int C, int H, int W,
+                                                       int F, int Ho, int Wo, spk::dog::DogParams p, int T,
+                                                       float min_value, uint8_t *__restrict__ times,
+                                                       float *__restrict__ dog_out)
+{
+    extern __shared__ uint64_t keys[];
+    __shared__ int cnt[kBk + 1];
+    __shared__ int red[kThreads / 64];
+    __shared__ uint32_t mm[3];
+    __shared__ float coef[spk::dog::kMaxCoef];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int n = C * F * Ho * Wo, nr = dog_runs(Wo);
+    const int Hs = Ho + p.hi - p.lo, Ws = nr * kDogRun + p.hi - p.lo;  // staged rows and columns
+    float *stage = reinterpret_cast<float *>(keys);
+    float *vals = stage + (size_t)C * Hs * Ws;
+    const uint8_t *src = img + (size_t)b * C * H * W;
+    for (int i = tid; i < p.cbase[F - 1] + p.ks[F - 1] * p.ks[F - 1]; i += kThreads) coef[i] = p.coef[i];
+    for (int i = tid; i < C * Hs * Ws; i += kThreads) {
+        const int c = i / (Hs * Ws), r = i - c * Hs * Ws, yy = r / Ws, xx = r - yy * Ws;
+        stage[i] = spk::dog::pixel(src + (size_t)c * H * W, H, W, yy + p.lo, xx + p.lo);
+    }
+    __syncthreads();
+    for (int u = tid; u < C * F * Ho * nr; u += kThreads) {
+        const int pl = u / (Ho * nr), yq = u - pl * Ho * nr, y = yq / nr, x0 = (yq - y * nr) * kDogRun;
+        const int c = pl / F, f = pl - c * F, o = p.off[f] - p.lo;
+        float acc[kDogRun];
+        spk::dog::window_run_k<kDogRun>(p.ks[f], coef + p.cbase[f],
+                                        stage + ((size_t)c * Hs + y + o) * Ws + x0 + o, Ws, acc);
+#pragma unroll
+        for (int r = 0; r < kDogRun; r++) {
+            if (x0 + r < Wo) {
+                const int i = (pl * Ho + y) * Wo + x0 + r;
+                vals[i] = acc[r];
+                if (dog_out) dog_out[(size_t)b * n + i] = acc[r];
+            }
+        }
+    }
+    __syncthreads();
+    float xv[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) xv[j] = vals[min(tid + kThreads * j, n - 1)];
+    __syncthreads();  // the staged image and the values are dead: their LDS becomes the keys
+    bucket_code(xv, n, T, min_value, times + (size_t)b * n, keys, cnt, red, mm);
 }
 
 // ------------------------------------------------------------------------
@@ -613,6 +680,17 @@ ClWs cl_layout(int B, long long n)
 
 size_t ws_layout(int B, long long n) { return n <= kSmall ? 0 : cl_layout(B, n).total; }
 
+// The fused DoG + coding kernel applies when every filter fits one
+// coefficient block, the sample fits the bucketed coder and the staged image
+// fits LDS beside the kernel's static arrays; lds: its dynamic LDS bytes.
+bool dog_code_fits(int C, int F, int Ho, int Wo, const spk::dog::DogParams &p, size_t &lds)
+{
+    const long long n = (long long)C * F * Ho * Wo;
+    const long long stage = (long long)C * (Ho + p.hi - p.lo) * (dog_runs(Wo) * kDogRun + p.hi - p.lo) * 4;
+    lds = (size_t)std::max(2 * n * 8, stage + 4 * n);
+    return p.nf == F && n <= kSmall && lds + 20 * 1024 <= 160 * 1024;
+}
+
 }  // namespace
 
 extern "C" size_t spk_latency_code_workspace_size(int B, int C, int H, int W)
@@ -690,4 +768,59 @@ extern "C" spk_status spk_latency_code(const float *x, int B, int C, int H, int 
         SPK_LAUNCHED("spk_latency_code");
     }
     return SPK_OK;
+}
+
+extern "C" size_t spk_dog_latency_code_workspace_size(int B, int C, int H, int W,
+                                                     const spk_dog_desc *filters, int F, int pad)
+{
+    int Ho = 0, Wo = 0;
+    if (!filters || spk::dog::plan("spk_dog_latency_code_workspace_size", B, C, H, W, filters, F, pad, Ho,
+                                   Wo) != SPK_OK)
+        return 0;
+    spk::dog::DogParams p;
+    spk::dog::group(filters, F, pad, 0, p);
+    size_t lds = 0;
+    if (dog_code_fits(C, F, Ho, Wo, p, lds)) return 0;
+    return spk::align_up((size_t)B * C * F * Ho * Wo * sizeof(float), 256) +
+           spk_latency_code_workspace_size(B, C * F, Ho, Wo);
+}
+
+extern "C" spk_status spk_dog_latency_code(const uint8_t *img, int B, int C, int H, int W,
+                                           const spk_dog_desc *filters, int F, int pad, int T,
+                                           float min_value, uint8_t *times, float *dog_out, void *ws,
+                                           size_t ws_bytes, spk_stream stream)
+{
+    spk::clear_error();
+    SPK_REQUIRE(img && filters && times, SPK_E_ARG, "spk_dog_latency_code: NULL pointer");
+    int Ho = 0, Wo = 0;
+    const spk_status st = spk::dog::plan("spk_dog_latency_code", B, C, H, W, filters, F, pad, Ho, Wo);
+    if (st != SPK_OK) return st;
+    SPK_REQUIRE(T >= 1 && T <= SPK_MAX_T, SPK_E_SHAPE, "spk_dog_latency_code: T=%d not in [1, %d]", T,
+                SPK_MAX_T);
+    SPK_REQUIRE((long long)C * F * Ho * Wo < (1LL << 31), SPK_E_SHAPE,
+                "spk_dog_latency_code: sample of %lld values too large", (long long)C * F * Ho * Wo);
+    spk::dog::DogParams p;
+    spk::dog::group(filters, F, pad, 0, p);
+    size_t lds = 0;
+    if (dog_code_fits(C, F, Ho, Wo, p, lds)) {
+        SPK_REQUIRE(B <= 65535, SPK_E_SHAPE, "spk_dog_latency_code: B=%d > 65535", B);
+        if (lds > 64 * 1024)
+            (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_dog_code),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_dog_code, dim3(B), dim3(kThreads), lds, spk::stream_of(stream), img, C, H, W,
+                           F, Ho, Wo, p, T, min_value, times, dog_out);
+        SPK_LAUNCHED("spk_dog_latency_code");
+        return SPK_OK;
+    }
+    // the two calls in sequence, the filter outputs in dog_out or the workspace
+    const size_t xb = spk::align_up((size_t)B * C * F * Ho * Wo * sizeof(float), 256);
+    const size_t cw = spk_latency_code_workspace_size(B, C * F, Ho, Wo);
+    SPK_REQUIRE(ws && ws_bytes >= xb + cw, SPK_E_WORKSPACE,
+                "spk_dog_latency_code: workspace of %zu bytes needed, %zu given", xb + cw, ws_bytes);
+    SPK_REQUIRE_WS_ALIGNED(ws, "spk_dog_latency_code");
+    float *x = dog_out ? dog_out : static_cast<float *>(ws);
+    spk_status s2 = spk_dog_filter(img, B, C, H, W, filters, F, pad, x, stream);
+    if (s2 != SPK_OK) return s2;
+    return spk_latency_code(x, B, C * F, Ho, Wo, T, min_value, SPK_CODE_RANK, times, nullptr,
+                            cw ? static_cast<char *>(ws) + xb : nullptr, cw, stream);
 }

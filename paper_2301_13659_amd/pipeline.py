@@ -127,7 +127,18 @@ class Pipeline:
         if self.wl.lr_schedule is not None and learn:
             f = self.rate_factor()
             self.cfgs = [(a * f, b * f, lo, up, st) for a, b, lo, up, st in self.base_cfgs]
-        if self.images is not None:
+        if self.images is not None and not wl.log_stds and wl.pre_threshold is None:
+            # filter bank and coding in one call; the filter outputs are kept when asked for
+            x = None
+            if keep:
+                B, C, H, W = self.images.shape
+                x = torch.empty((B, C * len(self.filters), H, W), dtype=torch.float32,
+                                device=self.images.device)
+            t = timed("code", lambda: spk.spk_dog_latency_code(self.images, self.filters, wl.T,
+                                                               wl.min_value, dog_out=x))
+            if keep:
+                out.dog, out.times0 = x, t
+        elif self.images is not None:
             if wl.log_stds:
                 x = timed("dog", lambda: spk.spk_log_filter(self.images, wl.log_stds, wl.log_ksize))
             else:

@@ -53,6 +53,8 @@ _SIGNATURES = {
     "spk_dog_filter": ([_P, _I, _I, _I, _I, _P, _I, _I, _P, _P], _I),
     "spk_latency_code_workspace_size": ([_I, _I, _I, _I], _Z),
     "spk_latency_code": ([_P, _I, _I, _I, _I, _I, _F, _I, _P, _P, _P, _Z, _P], _I),
+    "spk_dog_latency_code_workspace_size": ([_I, _I, _I, _I, _P, _I, _I], _Z),
+    "spk_dog_latency_code": ([_P, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _Z, _P], _I),
     "spk_conv_fire_workspace_size": ([_I] * 10 + [_F, _I], _Z),
     "spk_conv_fire": ([_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P,
                        _Z, _P], _I),
@@ -214,6 +216,29 @@ def spk_latency_code(x, T: int, min_value: float = 0.01, mode: int = SPK_CODE_RA
     _check(L.spk_latency_code(_ptr(x), B, C, H, W, T, float(min_value), mode, _ptr(times),
                               _ptr(fr), _ptr(ws), nbytes, _stream(x.device)))
     return (times, fr) if fr is not None else times
+
+
+def spk_dog_latency_code(img, filters, T: int, min_value: float = 0.01, pad: int = -1,
+                         times=None, dog_out=None):
+    """DoG filtering then rank-order coding in one call; dog_out: optional float
+    tensor that also receives the filter outputs."""
+    _dev(img, torch.uint8, "img", 4)
+    B, C, H, W = img.shape
+    descs = (DogDesc * len(filters))(*[DogDesc(int(k), float(s1), float(s2)) for k, s1, s2 in filters])
+    K0 = int(filters[0][0])
+    Ho, Wo = (H, W) if pad < 0 else (H + 2 * pad - K0 + 1, W + 2 * pad - K0 + 1)
+    shape = (B, C * len(filters), Ho, Wo)
+    if times is None:
+        times = _empty(shape, dtype=torch.uint8, device=img.device)
+    _dev(times, torch.uint8, "times", 4)
+    if dog_out is not None:
+        _dev(dog_out, torch.float32, "dog_out", 4)
+    L = load()
+    nbytes = L.spk_dog_latency_code_workspace_size(B, C, H, W, descs, len(filters), pad)
+    ws = _workspace(nbytes, img.device)
+    _check(L.spk_dog_latency_code(_ptr(img), B, C, H, W, descs, len(filters), pad, T, float(min_value),
+                                  _ptr(times), _ptr(dog_out), _ptr(ws), nbytes, _stream(img.device)))
+    return times
 
 
 def spk_conv_fire(in_times, w, T: int, stride: int = 1, pad: int = 0, theta: float = math.inf,

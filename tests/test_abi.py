@@ -74,6 +74,28 @@ def test_latency_code_validation_and_workspace():
          spk.SPK_E_WORKSPACE, "workspace")
 
 
+def test_dog_latency_code_validation_and_workspace():
+    L = spk.load()
+    six = (spk.DogDesc * 6)(*[spk.DogDesc(k, s1, s2) for k, s1, s2 in
+                              [(3, 0.43, 0.86), (3, 0.86, 0.43), (7, 1.0, 2.0), (7, 2.0, 1.0),
+                               (13, 1.86, 3.71), (13, 3.71, 1.86)]])
+    # the three-layer net's input stage runs fused: no workspace
+    assert L.spk_dog_latency_code_workspace_size(64, 1, 28, 28, six, 6, -1) == 0
+    # 6 x 160 x 250 values per sample: filter outputs plus the large-sample coder's workspace
+    need = L.spk_dog_latency_code_workspace_size(32, 1, 160, 250, six, 6, -1)
+    assert need >= 32 * 6 * 160 * 250 * 4 + L.spk_latency_code_workspace_size(32, 6, 160, 250)
+    _err(L.spk_dog_latency_code(P1, 32, 1, 160, 250, six, 6, -1, 30, 0.01, P1, None, P1, need - 1, None),
+         spk.SPK_E_WORKSPACE, "workspace")
+    _err(L.spk_dog_latency_code(None, 1, 1, 28, 28, six, 6, -1, 15, 0.01, P1, None, None, 0, None),
+         spk.SPK_E_ARG, "NULL")
+    _err(L.spk_dog_latency_code(P1, 1, 1, 28, 28, six, 6, -1, 255, 0.01, P1, None, None, 0, None),
+         spk.SPK_E_SHAPE, "T=")
+    even = (spk.DogDesc * 1)(spk.DogDesc(6, 1.0, 2.0))
+    _err(L.spk_dog_latency_code(P1, 1, 1, 8, 8, even, 1, -1, 15, 0.01, P1, None, None, 0, None),
+         spk.SPK_E_ARG, "odd")
+    assert L.spk_dog_latency_code_workspace_size(1, 1, 8, 8, even, 1, -1) == 0
+
+
 def test_conv_fire_validation():
     L = spk.load()
     args = lambda **kw: dict(dict(B=1, T=5, Ci=2, Hi=8, Wi=8, dt=0, Co=3, Kh=3, Kw=3, s=1, p=1,

@@ -46,6 +46,38 @@ def test_dog_bit_exact(shape, filters, pad):
     np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
 
 
+_DOG6 = [(3, 3 / 7, 6 / 7), (3, 6 / 7, 3 / 7), (7, 1.0, 2.0), (7, 2.0, 1.0),
+         (13, 13 / 7, 26 / 7), (13, 26 / 7, 13 / 7)]
+
+
+# fused (one workgroup per sample) and two-call cases: the three-layer net's
+# input stage, an explicit pad, a 21x21 kernel beside a 1x1, more values per
+# sample than the fused kernel ranks, and more coefficients than one block holds
+@pytest.mark.parametrize("shape,filters,pad,T", [
+    ((64, 1, 28, 28), _DOG6, -1, 15),
+    ((2, 3, 17, 9), [(5, 1.0, 2.0), (5, 0.7, 1.9)], 2, 15),
+    ((3, 1, 5, 4), [(21, 3.0, 6.0), (1, 1.0, 2.0)], -1, 4),
+    ((3, 2, 37, 70), [(7, 1.0, 2.0), (7, 2.0, 1.0)], -1, 30),
+    ((2, 1, 30, 20), [(13, 1.0, 2.0), (13, 2.0, 1.0), (13, 1.5, 3.0)], -1, 15),
+])
+def test_dog_latency_code_equals_filter_then_code(shape, filters, pad, T):
+    dev = gpu()
+    rng = np.random.default_rng(sum(shape) + T)
+    img = rng.integers(0, 256, size=shape, dtype=np.uint8)
+    img[1] = 0                                        # a sample with no eligible value
+    ti = _t(img, dev)
+    x = spk.spk_dog_filter(ti, filters, pad)
+    ref = np_(spk.spk_latency_code(x, T, 0.01))
+    np.testing.assert_array_equal(ref, oracle.latency_code(oracle.dog_filter(img, filters, pad), T, 0.01))
+    times = torch.full(tuple(x.shape), 0xAB, dtype=torch.uint8, device=dev)
+    d = torch.full(tuple(x.shape), float("nan"), dtype=torch.float32, device=dev)
+    spk.spk_dog_latency_code(ti, filters, T, 0.01, pad, times=times, dog_out=d)
+    np.testing.assert_array_equal(np_(times), ref)
+    np.testing.assert_array_equal(np_(d).view(np.uint32), np_(x).view(np.uint32))
+    alone = spk.spk_dog_latency_code(ti, filters, T, 0.01, pad)  # no filter outputs asked for
+    np.testing.assert_array_equal(np_(alone), ref)
+
+
 # ------------------------------------------------------------ latency code
 
 @pytest.mark.parametrize("shape,T", [((5, 2, 28, 28), 15), ((3, 6, 28, 28), 15), ((2, 1, 1, 1), 4),
