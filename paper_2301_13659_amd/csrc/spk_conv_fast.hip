@@ -283,8 +283,23 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
         const int b = blockIdx.x / g.Hp, py = blockIdx.x - b * g.Hp;
         const int iy = py - g.pad;
         uint8_t *row = xp + ((size_t)b * g.Hp + py) * g.rowb;
+        // rows of a multiple of 8 bytes start 8-byte aligned: 8-byte fills and stores
+        const bool wide = (g.rowb & 7) == 0;
+        const uint64_t fill8 = 0x0101010101010101ull * fill;
+        auto store_row = [&](auto get8, auto get1) {
+            if (wide) {
+                for (int e = threadIdx.x; e < g.rowb / 8; e += blockDim.x)
+                    reinterpret_cast<uint64_t *>(row)[e] = get8(e);
+            } else {
+                for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = get1(e);
+            }
+        };
         if ((unsigned)iy < (unsigned)g.Hi) {
-            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = fill;
+            if (wide) {
+                for (int e = threadIdx.x; e < g.rowb / 8; e += blockDim.x) reinterpret_cast<uint64_t *>(sm)[e] = fill8;
+            } else {
+                for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = fill;
+            }
             __syncthreads();
             const int n = g.Cin * g.Wi, step = (int)blockDim.x;
             auto put = [&](int e, uint8_t v) {
@@ -313,9 +328,9 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
                 for (; e < n; e += step) put(e, get(e));
             }
             __syncthreads();
-            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = sm[e];
+            store_row([&](int e) { return reinterpret_cast<const uint64_t *>(sm)[e]; }, [&](int e) { return sm[e]; });
         } else {
-            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = fill;
+            store_row([&](int) { return fill8; }, [&](int) { return fill; });
         }
         if ((int)blockIdx.x == nb_in - 1)
             for (int e = threadIdx.x; e < kSlack; e += blockDim.x) row[g.rowb + e] = fill;

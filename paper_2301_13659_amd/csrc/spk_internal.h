@@ -57,7 +57,7 @@ __device__ __forceinline__ void pool_row(const PoolIn &p, long long plane0, int 
     const long long plane_b = (long long)p.H0 * p.W0;
     const long long last_full = p.bytes / 4;  // dwords [0, last_full) lie wholly inside src
     const int n = C * SW;
-    constexpr int kIn = 8;
+    constexpr int kIn = 16;
     for (int f0 = threadIdx.x; f0 < n; f0 += kIn * (int)blockDim.x) {
         uint32_t v[kIn];
 #pragma unroll
