@@ -41,7 +41,7 @@ MAX_CPU_THREADS = 16
 # hashes to the value recorded with the counters.
 PROFILES = os.path.join(ROOT, "profiles")
 CONV_SOURCES = [os.path.join(ROOT, "paper_2301_13659_amd", "csrc", f)
-                for f in ("spk_conv.hip", "spk_conv_pt.hip", "spk_conv_fast.hip", "spk_conv_mfma.hip")]
+                for f in ("spk_conv.hip", "spk_conv_pt.hip", "spk_conv_fast.hip", "spk_conv_mfma.hip", "spk_internal.h")]
 
 
 def conv_source_hash():
