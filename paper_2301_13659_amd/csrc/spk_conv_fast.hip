@@ -410,6 +410,107 @@ __global__ __launch_bounds__(256) void k_pack(const uint8_t *__restrict__ in,
     }
 }
 
+// Pooled readout input in whole planes, for maps whose planes are small: block
+// (b, chunk of kPlaneC channels of Xp) reads the chunk's planes of the
+// unpooled map (one contiguous run of bytes) into LDS, pools every cell of
+// the chunk (a thread per (channel, cell), kept in pool.pooled when that is
+// set) into an LDS tile [cell][channel], then writes every padded pixel's run
+// of the chunk's channels, 8 channels per 8-byte store.  The map is read once,
+// in full cache lines, instead of in window-row pieces per output row.
+// Channels of the chunk past Cin, and the padding, hold the fill (0: not
+// fired); block 0 also fills the readable slack.  Needs Xp channels (g.Ci) a
+// multiple of 8 (make_ro_geom's are).
+constexpr int kPlaneC = 32;
+
+__host__ __device__ inline int align_up16(int n) { return (n + 15) & ~15; }
+
+__host__ __device__ inline bool planes_fit(const FGeom &g, const spk::PoolIn &p)
+{
+    return g.ind && g.Ci % 8 == 0 && (long long)kPlaneC * (p.H0 * p.W0 + g.Hi * g.Wi) <= 48 * 1024;
+}
+
+__global__ __launch_bounds__(256) void k_pack_planes(FGeom g, spk::PoolIn pool, uint8_t *__restrict__ xp)
+{
+    extern __shared__ __align__(16) uint8_t sm[];
+    const int nch = (g.Ci + kPlaneC - 1) / kPlaneC;
+    const int b = blockIdx.x / nch, c0 = (blockIdx.x - b * nch) * kPlaneC;
+    const int cn = min(kPlaneC, g.Cin - c0);  // real channels of the chunk (<= 0: none)
+    const int plane = pool.H0 * pool.W0, cells = g.Hi * g.Wi;
+    uint8_t *tile = sm + align_up16(kPlaneC * plane);  // [cell][kPlaneC] indicator bytes
+    if (cn > 0) {
+        const uint8_t *src = pool.src + ((long long)b * g.Cin + c0) * plane;
+        const int n = cn * plane;
+        if ((((uintptr_t)src) & 3) == 0) {
+            // all of a thread's loads (up to 8 dwords) in flight before any store
+            const int n4 = n >> 2;
+            for (int e0 = threadIdx.x; e0 < n4; e0 += 8 * (int)blockDim.x) {
+                uint32_t v[8];
+#pragma unroll
+                for (int u = 0; u < 8; u++) {
+                    const int e = e0 + u * (int)blockDim.x;
+                    v[u] = e < n4 ? reinterpret_cast<const uint32_t *>(src)[e] : 0u;
+                }
+#pragma unroll
+                for (int u = 0; u < 8; u++) {
+                    const int e = e0 + u * (int)blockDim.x;
+                    if (e < n4) reinterpret_cast<uint32_t *>(sm)[e] = v[u];
+                }
+            }
+            for (int e = 4 * n4 + threadIdx.x; e < n; e += blockDim.x) sm[e] = src[e];
+        } else {
+            for (int e = threadIdx.x; e < n; e += blockDim.x) sm[e] = src[e];
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kPlaneC * cells; e += blockDim.x) {
+        const int c = e / cells, cell = e - c * cells;
+        uint8_t v = 0;
+        if (c < cn) {
+            const int iy = cell / g.Wi, ix = cell - iy * g.Wi;
+            const int y0 = iy * pool.stride - pool.pad, x0 = ix * pool.stride - pool.pad;
+            const int ylo = max(y0, 0), yhi = min(y0 + pool.kh, pool.H0);
+            const int xlo = max(x0, 0), xhi = min(x0 + pool.kw, pool.W0);
+            const uint8_t *pl = sm + c * plane;
+            uint32_t m = (uint32_t)spk::kNever;
+            if (pool.kh <= 3 && pool.kw <= 3) {
+                // windows up to 3 x 3: the nine reads together (cells outside
+                // the window or the map read the window's first cell; an empty
+                // window, all in the padding, never fires)
+                const bool any = ylo < yhi && xlo < xhi;
+                const int first = any ? ylo * pool.W0 + xlo : 0;
+                uint32_t t[9];
+#pragma unroll
+                for (int u = 0; u < 9; u++) {
+                    const int y = ylo + u / 3, x = xlo + u % 3;
+                    t[u] = pl[(y < yhi && x < xhi) ? y * pool.W0 + x : first];
+                }
+#pragma unroll
+                for (int u = 0; u < 9; u++) m = min(m, t[u]);
+                if (!any) m = (uint32_t)spk::kNever;
+            } else {
+                for (int y = ylo; y < yhi; y++)
+                    for (int x = xlo; x < xhi; x++) m = min(m, (uint32_t)pl[y * pool.W0 + x]);
+            }
+            if (pool.pooled) pool.pooled[((long long)b * g.Cin + c0 + c) * cells + cell] = (uint8_t)m;
+            v = m < (uint32_t)g.T ? (uint8_t)0x3C : (uint8_t)0;
+        }
+        tile[cell * kPlaneC + c] = v;
+    }
+    __syncthreads();
+    const int ngrp = min(kPlaneC, g.Ci - c0) / 8;
+    for (int e = threadIdx.x; e < g.Hp * g.Wp * ngrp; e += blockDim.x) {
+        const int pix = e / ngrp, q = e - pix * ngrp;
+        const int py = pix / g.Wp, px = pix - py * g.Wp;
+        const int iy = py - g.pad, ix = px - g.pad;
+        uint2 v = make_uint2(0u, 0u);
+        if ((unsigned)iy < (unsigned)g.Hi && (unsigned)ix < (unsigned)g.Wi)
+            v = *reinterpret_cast<const uint2 *>(tile + (iy * g.Wi + ix) * kPlaneC + q * 8);
+        *reinterpret_cast<uint2 *>(xp + ((size_t)(b * g.Hp + py) * g.Wp + px) * g.Ci + c0 + q * 8) = v;
+    }
+    if (blockIdx.x == 0)
+        for (int e = threadIdx.x; e < kSlack; e += blockDim.x) xp[(size_t)g.B * g.Hp * g.rowb + e] = 0;
+}
+
 // Launch of the packing pass for a fragment shape.  in_rows: pack the input
 // (nb_in blocks); weights: pack the B fragments (one block per map).
 void launch_pack(const uint8_t *in, const void *w, bool half_w, bool big, const FGeom &g,
@@ -1327,7 +1428,16 @@ spk_status readout_fast(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
                       : reinterpret_cast<h8 *>(reinterpret_cast<char *>(ws) + xp_bytes(g));
     float *part = reinterpret_cast<float *>(reinterpret_cast<char *>(ws) + xp_bytes(g) +
                                             spk::align_up(bp_bytes(g, 2), 256));
-    launch_pack(in, w, half_w, true, g, xp, bp, s, true, packed_w == nullptr, pool);
+    if (pool && planes_fit(g, *pool)) {
+        // the pooled input in whole planes; the weights, when not given packed, in their own pass
+        const size_t lds = align_up16(kPlaneC * pool->H0 * pool->W0) + (size_t)kPlaneC * g.Hi * g.Wi;
+        hipLaunchKernelGGL(k_pack_planes, dim3(g.B * ((g.Ci + kPlaneC - 1) / kPlaneC)), dim3(256), lds, s,
+                           g, *pool, xp);
+        SPK_LAUNCHED("spk_conv_fire");
+        if (!packed_w) launch_pack(in, w, half_w, true, g, xp, bp, s, false, true);
+    } else {
+        launch_pack(in, w, half_w, true, g, xp, bp, s, true, packed_w == nullptr, pool);
+    }
     SPK_LAUNCHED("spk_conv_fire");
 
     const int splits = ro_splits(g);

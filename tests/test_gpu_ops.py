@@ -276,6 +276,7 @@ POOL_CONV_CASES = [
     (2, 4, 160, 250, (7, 6, 0), 20, 17, 1, 0, 30, 42.0, 0.05, "f32"),  # large-image conv2
     (2, 8, 12, 12, ((2, 3), 2, 1), 20, 3, 1, 1, 40, 5.0, 0.3, "f32"),  # 2 x 3 window, T = 40
     (2, 5, 9, 9, (1, 1, 0), 7, 3, 1, 1, 5, 2.0, 0.3, "f32"),           # 1 x 1 window: identity
+    (1, 16, 100, 90, (2, 2, 0), 12, 3, 1, 1, 7, math.inf, 0.3, "f32"),  # readout, planes too big to stage
 ]
 
 
