@@ -491,15 +491,19 @@ struct WtaArgs {
     int C, H, W, T, k, radius, readout, by_record;
 };
 
-__global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__ times,
+// 1024 threads: one block per sample is all the grid has, so each sweep of
+// the candidates is spread over as many lanes as a block holds.
+constexpr int kSelT = 1024;
+
+__global__ __launch_bounds__(kSelT) void k_select(const uint8_t *__restrict__ times,
                                                      const float *__restrict__ vkey,
                                                      const Rec *__restrict__ recs, WtaArgs a,
                                                      int stage_recs, spk_winner *__restrict__ winners,
                                                      int32_t *__restrict__ n_winners)
 {
     extern __shared__ uint32_t bits[];  // [positions][maps] dead bits, then staged records
-    __shared__ uint64_t s_hi[kThreads / 64];
-    __shared__ uint32_t s_lo[kThreads / 64];
+    __shared__ uint64_t s_hi[kSelT / 64];
+    __shared__ uint32_t s_lo[kSelT / 64];
     const int b = blockIdx.x;
     const int HW = a.H * a.W;
     const int pw = (HW + 31) / 32, cw = (a.C + 31) / 32;
@@ -517,32 +521,54 @@ __global__ __launch_bounds__(kThreads) void k_select(const uint8_t *__restrict__
     for (int round = 0; round < a.k; round++) {
         uint64_t hi = kNone;
         uint32_t lo = ~0u;
+        // candidates in batches of kScan per thread: a batch's loads are all
+        // issued before any is tested
+        constexpr int kScan = 8;
         if (a.by_record) {
-            for (int p = threadIdx.x; p < HW; p += blockDim.x) {
-                if (pos_dead[p >> 5] & (1u << (p & 31))) continue;
-                const Rec r = rb[p];
-                const uint32_t t = r.tc >> 24, c = r.tc & 0xFFFFFFu;
-                if (t == (uint32_t)spk::kNever || (map_dead[c >> 5] & (1u << (c & 31)))) continue;
-                const uint64_t h = ((uint64_t)t << 32) | order_desc(r.v);
-                const uint32_t l = c * (uint32_t)HW + (uint32_t)p;
-                if (h < hi || (h == hi && l < lo)) {
-                    hi = h;
-                    lo = l;
+            for (int p0 = threadIdx.x; p0 < HW; p0 += kScan * (int)blockDim.x) {
+                Rec rr[kScan];
+#pragma unroll
+                for (int u = 0; u < kScan; u++) rr[u] = rb[min(p0 + u * (int)blockDim.x, HW - 1)];
+#pragma unroll
+                for (int u = 0; u < kScan; u++) {
+                    const int p = p0 + u * (int)blockDim.x;
+                    if (p >= HW || (pos_dead[p >> 5] & (1u << (p & 31)))) continue;
+                    const uint32_t t = rr[u].tc >> 24, c = rr[u].tc & 0xFFFFFFu;
+                    if (t == (uint32_t)spk::kNever || (map_dead[c >> 5] & (1u << (c & 31)))) continue;
+                    const uint64_t h = ((uint64_t)t << 32) | order_desc(rr[u].v);
+                    const uint32_t l = c * (uint32_t)HW + (uint32_t)p;
+                    if (h < hi || (h == hi && l < lo)) {
+                        hi = h;
+                        lo = l;
+                    }
                 }
             }
         } else {
             const size_t base = (size_t)b * a.C * HW;
             const int n = a.C * HW;
-            for (int i = threadIdx.x; i < n; i += blockDim.x) {
-                const int c = i / HW, p = i - c * HW;
-                if (pos_dead[p >> 5] & (1u << (p & 31))) continue;
-                if (map_dead[c >> 5] & (1u << (c & 31))) continue;
-                const uint32_t t = times[base + i];
-                if (!a.readout && t == (uint32_t)spk::kNever) continue;
-                const uint64_t h = ((uint64_t)(a.readout ? 0u : t) << 32) | order_desc(vkey[base + i]);
-                if (h < hi || (h == hi && (uint32_t)i < lo)) {
-                    hi = h;
-                    lo = (uint32_t)i;
+            for (int i0 = threadIdx.x; i0 < n; i0 += kScan * (int)blockDim.x) {
+                uint32_t tt[kScan];
+                float vv[kScan];
+#pragma unroll
+                for (int u = 0; u < kScan; u++) {
+                    const int i = min(i0 + u * (int)blockDim.x, n - 1);
+                    tt[u] = times[base + i];
+                    vv[u] = vkey[base + i];
+                }
+#pragma unroll
+                for (int u = 0; u < kScan; u++) {
+                    const int i = i0 + u * (int)blockDim.x;
+                    if (i >= n) continue;
+                    const int c = i / HW, p = i - c * HW;
+                    if (pos_dead[p >> 5] & (1u << (p & 31))) continue;
+                    if (map_dead[c >> 5] & (1u << (c & 31))) continue;
+                    const uint32_t t = tt[u];
+                    if (!a.readout && t == (uint32_t)spk::kNever) continue;
+                    const uint64_t h = ((uint64_t)(a.readout ? 0u : t) << 32) | order_desc(vv[u]);
+                    if (h < hi || (h == hi && (uint32_t)i < lo)) {
+                        hi = h;
+                        lo = (uint32_t)i;
+                    }
                 }
             }
         }
@@ -797,7 +823,7 @@ extern "C" spk_status spk_inhibit_winners(const uint8_t *times, const float *vke
     if (lds > 64 * 1024)
         (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_select),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(k_select, dim3(B), dim3(k > 0 ? kThreads : 64), lds, s, times, vkey, recs, a,
+    hipLaunchKernelGGL(k_select, dim3(B), dim3(k > 0 ? kSelT : 64), lds, s, times, vkey, recs, a,
                        stage, winners, n_winners);
     SPK_LAUNCHED("spk_inhibit_winners");
     return SPK_OK;
