@@ -267,8 +267,16 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
         const int b = blockIdx.x / g.Hp, py = blockIdx.x - b * g.Hp;
         const int iy = py - g.pad;
         uint8_t *row = xp + ((size_t)b * g.Hp + py) * g.rowb;
+        // rows of a multiple of 16 bytes start 16-byte aligned: 16-byte fills and stores
+        const bool wide = (g.rowb & 15) == 0;
+        const uint4 never16 = make_uint4(0x01010101u * never, 0x01010101u * never, 0x01010101u * never,
+                                         0x01010101u * never);
         if ((unsigned)iy < (unsigned)g.Hi) {
-            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = never;
+            if (wide) {
+                for (int e = threadIdx.x; e < g.rowb / 16; e += blockDim.x) reinterpret_cast<uint4 *>(sm)[e] = never16;
+            } else {
+                for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) sm[e] = never;
+            }
             __syncthreads();
             auto put = [&](int c, int x, uint8_t v) { sm[(x + g.pad) * g.Cp + c] = v < never ? v : never; };
             if (pool.src) {
@@ -277,14 +285,44 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
                               reinterpret_cast<uint32_t *>(sm + pool.stage), put);
             } else {
                 const uint8_t *src = in + (size_t)b * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi;
-                const int n = g.Ci * g.Wi;
-                for (int e = threadIdx.x; e < n; e += blockDim.x) {
-                    const int c = e / g.Wi, x = e - c * g.Wi;
-                    put(c, x, src[(size_t)c * g.Hi * g.Wi + x]);
+                const size_t plane = (size_t)g.Hi * g.Wi;
+                if ((g.Wi & 3) == 0 && (plane & 3) == 0 && (((uintptr_t)src) & 3) == 0) {
+                    // the row of every channel as dwords, all of a thread's loads in flight first
+                    const int wq = g.Wi >> 2, n4 = g.Ci * wq;
+                    for (int e0 = threadIdx.x; e0 < n4; e0 += 8 * (int)blockDim.x) {
+                        uint32_t v[8];
+#pragma unroll
+                        for (int u = 0; u < 8; u++) {
+                            const int e = min(e0 + u * (int)blockDim.x, n4 - 1);
+                            const int c = e / wq, x4 = e - c * wq;
+                            v[u] = *reinterpret_cast<const uint32_t *>(src + c * plane + 4 * x4);
+                        }
+#pragma unroll
+                        for (int u = 0; u < 8; u++) {
+                            const int e = e0 + u * (int)blockDim.x;
+                            if (e >= n4) break;
+                            const int c = e / wq, x4 = e - c * wq;
+#pragma unroll
+                            for (int q = 0; q < 4; q++) put(c, 4 * x4 + q, (uint8_t)(v[u] >> (8 * q)));
+                        }
+                    }
+                } else {
+                    const int n = g.Ci * g.Wi;
+                    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+                        const int c = e / g.Wi, x = e - c * g.Wi;
+                        put(c, x, src[(size_t)c * plane + x]);
+                    }
                 }
             }
             __syncthreads();
-            for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = sm[e];
+            if (wide) {
+                for (int e = threadIdx.x; e < g.rowb / 16; e += blockDim.x)
+                    reinterpret_cast<uint4 *>(row)[e] = reinterpret_cast<const uint4 *>(sm)[e];
+            } else {
+                for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = sm[e];
+            }
+        } else if (wide) {
+            for (int e = threadIdx.x; e < g.rowb / 16; e += blockDim.x) reinterpret_cast<uint4 *>(row)[e] = never16;
         } else {
             for (int e = threadIdx.x; e < g.rowb; e += blockDim.x) row[e] = never;
         }
