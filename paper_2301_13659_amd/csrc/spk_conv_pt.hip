@@ -286,7 +286,42 @@ __global__ __launch_bounds__(256) void k_pack_pt(const uint8_t *__restrict__ in,
             } else {
                 const uint8_t *src = in + (size_t)b * g.Ci * g.Hi * g.Wi + (size_t)iy * g.Wi;
                 const size_t plane = (size_t)g.Hi * g.Wi;
-                if ((g.Wi & 3) == 0 && (plane & 3) == 0 && (((uintptr_t)src) & 3) == 0) {
+                if ((g.Wi & 3) == 0 && (plane & 3) == 0 && (((uintptr_t)src) & 3) == 0 && (g.Ci & 3) == 0 &&
+                    (g.Cp & 3) == 0) {
+                    // 4 channels x 4 pixels per thread: four dword loads (one per channel),
+                    // times clamped to T byte-wise, a byte transpose to four dwords of 4
+                    // channels each, written to LDS as dwords
+                    const int wq = g.Wi >> 2, cq = g.Ci >> 2, n16 = cq * wq;
+                    const uint32_t t4 = 0x01010101u * never;
+                    for (int e = threadIdx.x; e < n16; e += blockDim.x) {
+                        const int x4 = e % wq, c4 = e / wq;
+                        uint32_t d[4];
+#pragma unroll
+                        for (int k = 0; k < 4; k++)
+                            d[k] = *reinterpret_cast<const uint32_t *>(src + (4 * c4 + k) * plane + 4 * x4);
+#pragma unroll
+                        for (int k = 0; k < 4; k++) {
+                            // bytes above T (T <= 32) become T: a byte is above T when its
+                            // top bit is set or its low 7 bits plus 127 - T carry into it
+                            const uint32_t gt =
+                                (((d[k] & 0x7f7f7f7fu) + 0x01010101u * (uint32_t)(127 - (int)never)) | d[k]) &
+                                0x80808080u;
+                            const uint32_t full = (gt >> 7) * 0xFFu;
+                            d[k] = (d[k] & ~full) | (t4 & full);
+                        }
+                        const uint32_t t0 = __builtin_amdgcn_perm(d[1], d[0], 0x05010400u);
+                        const uint32_t t1 = __builtin_amdgcn_perm(d[3], d[2], 0x05010400u);
+                        const uint32_t t2 = __builtin_amdgcn_perm(d[1], d[0], 0x07030602u);
+                        const uint32_t t3 = __builtin_amdgcn_perm(d[3], d[2], 0x07030602u);
+                        const uint32_t o[4] = {__builtin_amdgcn_perm(t1, t0, 0x05040100u),
+                                               __builtin_amdgcn_perm(t1, t0, 0x07060302u),
+                                               __builtin_amdgcn_perm(t3, t2, 0x05040100u),
+                                               __builtin_amdgcn_perm(t3, t2, 0x07060302u)};
+#pragma unroll
+                        for (int q = 0; q < 4; q++)
+                            *reinterpret_cast<uint32_t *>(sm + (4 * x4 + q + g.pad) * g.Cp + 4 * c4) = o[q];
+                    }
+                } else if ((g.Wi & 3) == 0 && (plane & 3) == 0 && (((uintptr_t)src) & 3) == 0) {
                     // the row of every channel as dwords, all of a thread's loads in flight first
                     const int wq = g.Wi >> 2, n4 = g.Ci * wq;
                     for (int e0 = threadIdx.x; e0 < n4; e0 += 8 * (int)blockDim.x) {
