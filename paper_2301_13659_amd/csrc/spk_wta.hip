@@ -658,19 +658,29 @@ __device__ __forceinline__ void select_rounds(uint64_t (&kh)[NPL], const uint32_
         if (bh == kNone) break;
         const int wc = (int)(bl / (uint32_t)HW), wp = (int)(bl - (uint32_t)wc * (uint32_t)HW);
         const int wy = wp / a.W, wx = wp - wy * a.W;
+        if (tid == 0) {
+            // the winner's potential from its key (the map of order_desc back to the float bits)
+            const uint32_t asc = ~(uint32_t)bh;
+            const uint32_t u = (asc & 0x80000000u) ? (asc & 0x7FFFFFFFu) : ~asc;
+            spk_winner wn;
+            wn.c = wc;
+            wn.y = wy;
+            wn.x = wx;
+            wn.t = a.readout ? a.T - 1 : (int)(bh >> 32);
+            wn.v = __uint_as_float(u);
+            winners[(size_t)b * a.k + count] = wn;
+        }
+        // a candidate is suppressed by the winner's map, or by lying within
+        // the radius: with both coordinates packed as 16-bit halves,
+        // (y - wy + r) and (x - wx + r), taken modulo 2^16, are both at most 2r
+        const uint32_t base = ((uint32_t)(wy - a.radius) << 16) | (uint32_t)((wx - a.radius) & 0xFFFF);
+        const uint32_t lim = 0x00010001u * (uint32_t)(2 * a.radius);
 #pragma unroll
         for (int j = 0; j < NPL; j++) {
-            if (kh[j] == bh && kl[j] == bl) {
-                spk_winner wn;
-                wn.c = wc;
-                wn.y = wy;
-                wn.x = wx;
-                wn.t = a.readout ? a.T - 1 : (int)(bh >> 32);
-                wn.v = vv[j];
-                winners[(size_t)b * a.k + count] = wn;
-            }
-            const int dy = (yx[j] >> 16) - wy, dx = (yx[j] & 0xFFFF) - wx;
-            const bool near = dy <= a.radius && -dy <= a.radius && dx <= a.radius && -dx <= a.radius;
+            typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+            const us2 e = __builtin_bit_cast(us2, (uint32_t)yx[j]) - __builtin_bit_cast(us2, base);
+            const us2 over = __builtin_elementwise_sub_sat(e, __builtin_bit_cast(us2, lim));
+            const bool near = __builtin_bit_cast(uint32_t, over) == 0u;
             if (cc[j] == wc || near) kh[j] = kNone;
         }
         count++;
