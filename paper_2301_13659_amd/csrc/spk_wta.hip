@@ -612,7 +612,7 @@ __global__ __launch_bounds__(kSelT) void k_select(const uint8_t *__restrict__ ti
 // registers (NPL per thread, NW waves): candidate keys kh = time << 32 |
 // order_desc(v) (kNone: not a candidate), ties to the lower kl = map*HW +
 // position; cc, yx, vv: its map, y << 16 | x and potential.
-template <int NPL, int NW>
+template <int NPL, int NW, bool kPacked>
 __device__ __forceinline__ void select_rounds(uint64_t (&kh)[NPL], const uint32_t (&kl)[NPL],
                                               const int (&cc)[NPL], const int (&yx)[NPL],
                                               const float (&vv)[NPL], const WtaArgs &a, int HW, int b,
@@ -626,13 +626,18 @@ __device__ __forceinline__ void select_rounds(uint64_t (&kh)[NPL], const uint32_
     for (int round = 0; round < a.k; round++) {
         uint64_t bh = kNone;
         uint32_t bl = ~0u;
+        if constexpr (kPacked) {
+            // keys t << 56 | order << 24 | index: one 64-bit minimum
 #pragma unroll
-        for (int j = 0; j < NPL; j++)
-            if (kh[j] < bh || (kh[j] == bh && kl[j] < bl)) {
-                bh = kh[j];
-                bl = kl[j];
-            }
-        {
+            for (int j = 0; j < NPL; j++) bh = kh[j] < bh ? kh[j] : bh;
+            bh = wave_min_u64(bh);
+        } else {
+#pragma unroll
+            for (int j = 0; j < NPL; j++)
+                if (kh[j] < bh || (kh[j] == bh && kl[j] < bl)) {
+                    bh = kh[j];
+                    bl = kl[j];
+                }
             // the smallest key, then the smallest index among the lanes holding it
             const uint64_t wh = wave_min_u64(bh);
             bl = wave_min_u32(bh == wh ? bl : ~0u);
@@ -649,24 +654,31 @@ __device__ __forceinline__ void select_rounds(uint64_t (&kh)[NPL], const uint32_
             for (int w = 0; w < NW; w++) {
                 const uint64_t h2 = s_hi[slot][w];
                 const uint32_t l2 = s_lo[slot][w];
-                if (h2 < bh || (h2 == bh && l2 < bl)) {
+                if (h2 < bh || (!kPacked && h2 == bh && l2 < bl)) {
                     bh = h2;
                     bl = l2;
                 }
             }
         }
         if (bh == kNone) break;
+        uint32_t order = (uint32_t)bh;  // order_desc of the winner's potential
+        int tw = (int)(bh >> 32);       // its time
+        if constexpr (kPacked) {
+            bl = (uint32_t)bh & 0xFFFFFFu;
+            order = (uint32_t)(bh >> 24);
+            tw = (int)(bh >> 56);
+        }
         const int wc = (int)(bl / (uint32_t)HW), wp = (int)(bl - (uint32_t)wc * (uint32_t)HW);
         const int wy = wp / a.W, wx = wp - wy * a.W;
         if (tid == 0) {
             // the winner's potential from its key (the map of order_desc back to the float bits)
-            const uint32_t asc = ~(uint32_t)bh;
+            const uint32_t asc = ~order;
             const uint32_t u = (asc & 0x80000000u) ? (asc & 0x7FFFFFFFu) : ~asc;
             spk_winner wn;
             wn.c = wc;
             wn.y = wy;
             wn.x = wx;
-            wn.t = a.readout ? a.T - 1 : (int)(bh >> 32);
+            wn.t = a.readout ? a.T - 1 : tw;
             wn.v = __uint_as_float(u);
             winners[(size_t)b * a.k + count] = wn;
         }
@@ -690,7 +702,9 @@ __device__ __forceinline__ void select_rounds(uint64_t (&kh)[NPL], const uint32_
     if (tid == 0) n_winners[b] = count;
 }
 
-template <int NPL, int NW, bool kRec>
+// kPacked: candidate indices below 2^24, so (time, potential order, index) fit
+// one 64-bit key.
+template <int NPL, int NW, bool kRec, bool kPacked>
 __global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restrict__ times,
                                                         const float *__restrict__ vkey,
                                                         const Rec *__restrict__ recs, WtaArgs a,
@@ -739,25 +753,33 @@ __global__ __launch_bounds__(64 * NW) void k_select_reg(const uint8_t *__restric
         }
         const bool alive = i < n && (a.readout || t != spk::kNever);
         const uint32_t tk = a.readout ? 0u : (uint32_t)t;
-        kh[j] = alive ? (((uint64_t)tk << 32) | order_desc(vv[j])) : kNone;
+        kh[j] = !alive ? kNone
+                : kPacked ? (((uint64_t)tk << 56) | ((uint64_t)order_desc(vv[j]) << 24) |
+                             (uint64_t)((uint32_t)c * (uint32_t)HW + (uint32_t)pos))
+                          : (((uint64_t)tk << 32) | order_desc(vv[j]));
         kl[j] = (uint32_t)c * (uint32_t)HW + (uint32_t)pos;
         cc[j] = c;
         const int y = pos / a.W;
         yx[j] = (y << 16) | (pos - y * a.W);
     }
-    select_rounds<NPL, NW>(kh, kl, cc, yx, vv, a, HW, b, s_hi, s_lo, winners, n_winners);
+    select_rounds<NPL, NW, kPacked>(kh, kl, cc, yx, vv, a, HW, b, s_hi, s_lo, winners, n_winners);
 }
 
 template <int NPL, int NW>
 void launch_select_reg(int B, hipStream_t s, const uint8_t *times, const float *vkey,
                        const Rec *recs, const WtaArgs &a, spk_winner *winners, int32_t *n_winners)
 {
-    if (a.by_record)
-        hipLaunchKernelGGL((k_select_reg<NPL, NW, true>), dim3(B), dim3(64 * NW), 0, s, times, vkey,
-                           recs, a, winners, n_winners);
-    else
-        hipLaunchKernelGGL((k_select_reg<NPL, NW, false>), dim3(B), dim3(64 * NW), 0, s, times, vkey,
-                           recs, a, winners, n_winners);
+    const bool packed = (long long)a.C * a.H * a.W <= (1ll << 24);
+    auto run = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(B), dim3(64 * NW), 0, s, times, vkey, recs, a, winners, n_winners);
+    };
+    if (a.by_record) {
+        if (packed) run(k_select_reg<NPL, NW, true, true>);
+        else run(k_select_reg<NPL, NW, true, false>);
+    } else {
+        if (packed) run(k_select_reg<NPL, NW, false, true>);
+        else run(k_select_reg<NPL, NW, false, false>);
+    }
 }
 
 }  // namespace
