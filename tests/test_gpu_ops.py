@@ -193,6 +193,8 @@ CONV_CASES = [
     (2, 6, 160, 250, 4, 5, 1, 2, 30, 15.0, 0.05, "f32"),    # four maps: 2 x 4 position blocks, ragged x
     (2, 3, 21, 23, 5, 3, 2, 1, 12, 2.0, 0.4, "f32"),        # few maps, stride 2, ragged blocks
     (2, 8, 17, 19, 2, 5, 1, 2, 9, 3.0, 0.3, "f16"),         # two maps, half weights: 4 x 4 blocks
+    (3, 12, 11, 20, 24, 3, 1, 1, 9, 4.0, 0.3, "f32"),       # 4 x 4 byte-transpose packing, padded channels
+    (2, 4, 15, 16, 10, 3, 2, 1, 6, 2.0, 0.4, "f16"),        # the same with 4 channels and stride 2
 ]
 
 
