@@ -61,14 +61,16 @@ constexpr int kSlackPT = 64;                   // readable bytes past the end of
 constexpr uint32_t kSelLo = 0x04010400u;       // bytes 0,1 -> halves 1024 + b
 constexpr uint32_t kSelHi = 0x04030402u;       // bytes 2,3 -> halves 1024 + b
 
-// LDS: [staged V x 2 | staged t x 2 | position table x 3 | fire flag per 16
-// input bytes | input as halves (2 bytes per input byte, sized per launch to
-// the largest group's range, so small images leave room for more blocks)]
+// LDS: [staged V x 2 | staged t x 2 | position table x 3 | word counts per
+// wave | fire flag per 16 input bytes | input as halves (2 bytes per input
+// byte, sized per launch to the largest group's range, so small images leave
+// room for more blocks)]
 constexpr size_t kStvOff = 0;
 constexpr size_t kSttOff = kStvOff + 2 * 32 * kStageStride * sizeof(float);
 constexpr size_t kTabOff = (kSttOff + 2 * 32 * kStageStride + 15) / 16 * 16;
 constexpr size_t kTabBytes = 3 * kG * 3 * sizeof(int);
-constexpr size_t kFlagOff = kTabOff + kTabBytes;
+constexpr size_t kCntOff = kTabOff + kTabBytes;
+constexpr size_t kFlagOff = kCntOff + 2 * (kThreads / 64) * sizeof(int);
 constexpr size_t kHalOff = (kFlagOff + kRange / 16 + 15) / 16 * 16;
 
 // Layers with few maps take their output positions in blocks of by x bx
@@ -471,16 +473,11 @@ __device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words,
 
 // Staged words to LDS as halves 1024 + t, plus a flag per word: does any of
 // its 16 times fire within the window (clamped times: any byte below T)?
-// Returns, uniform over the wave, whether the range [0, nw) is sparse enough
-// to test slices in: a tile's slice can be skipped only when none of the
-// tile's words under it fires, so with a fraction u of the wave's words
-// unflagged about u^pt of the slices are skipped, pt being the words a
-// slice of the tile covers (one per position when window runs are 16-byte
-// aligned, two otherwise); testing pays when that is above 40 % (below it the
-// tests cost more than the skipped products save).
-__device__ __forceinline__ bool store_range(const Staged &st, uint8_t *hal, uint8_t *flags,
-                                            uint32_t never4, int nw, int hw, int pt)
+// Each wave also records how many of its words are flagged, for
+// group_sparse.
+__device__ __forceinline__ void store_range(const Staged &st, uint8_t *lds, uint32_t never4, int nw, int hw)
 {
+    uint8_t *hal = lds + kHalOff, *flags = lds + kFlagOff;
     int flagged = 0, words = 0;
 #pragma unroll
     for (int i = 0; i < kPf; i++) {
@@ -500,6 +497,31 @@ __device__ __forceinline__ bool store_range(const Staged &st, uint8_t *hal, uint
         flagged += __builtin_popcountll(__builtin_amdgcn_ballot_w64(f && k < nw));
         words += __builtin_popcountll(__builtin_amdgcn_ballot_w64(k < nw));
     }
+    if ((threadIdx.x & 63) == 0) {
+        int *cnt = reinterpret_cast<int *>(lds + kCntOff) + 2 * (threadIdx.x >> 6);
+        cnt[0] = flagged;
+        cnt[1] = words;
+    }
+}
+
+// Whether the staged group is sparse enough to test slices in, the same for
+// every wave of the block (from the counts store_range left; call after the
+// barrier that follows it).  A tile's slice can be skipped only when none of
+// the tile's words under it fires, so with a fraction u of the words
+// unflagged about u^pt of the slices are skipped, pt being the words a slice
+// of the tile covers (one per position when window runs are 16-byte aligned,
+// two otherwise); testing pays when that is above 40 % (below it the tests
+// cost more than the skipped products save).  One decision for the block
+// keeps its waves equally loaded between barriers.
+__device__ __forceinline__ bool group_sparse(const uint8_t *lds, int pt)
+{
+    const int *cnt = reinterpret_cast<const int *>(lds + kCntOff);
+    int flagged = 0, words = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; w++) {
+        flagged += cnt[2 * w];
+        words += cnt[2 * w + 1];
+    }
     const float u = words > 0 ? (float)(words - flagged) / (float)words : 0.0f;
     float skip = u;
     for (int i = 1; i < pt; i++) skip *= u;
@@ -507,31 +529,44 @@ __device__ __forceinline__ bool store_range(const Staged &st, uint8_t *hal, uint
 }
 
 // Staged results of positions [gs, min(gs + 64, p_end)) to the outputs:
-// consecutive threads take consecutive positions of one map.
+// consecutive threads take consecutive positions of one map, each thread one
+// position of every fourth map; all its staged values are read before the
+// stores.
 __device__ __forceinline__ void write_out(const PGeom &g, int nt, int gs, int p_end, const Tab *tab,
                                           const float *stv, const uint8_t *stt,
                                           uint8_t *__restrict__ out_t, float *__restrict__ out_v)
 {
+    constexpr int kPer = 32 * kG / kThreads;  // maps per thread
+    constexpr int kMapStep = kThreads / kG;
     const int HoWo = g.Ho * g.Wo;
     const int cnt = min(p_end, gs + kG) - gs;
+    const int pi = threadIdx.x & (kG - 1), oc0 = threadIdx.x / kG;
+    if (pi >= cnt) return;
+    const Tab tb = tab[pi];
+    float v[kPer];
+    uint8_t t[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const int oc = oc0 + kMapStep * j;
+        v[j] = stv[oc * kStageStride + pi];
+        t[j] = stt[oc * kStageStride + pi];
+    }
     const bool blocked = g.by * g.bx > 1;
-    for (int idx = threadIdx.x; idx < 32 * kG; idx += kThreads) {
-        const int pi = idx & (kG - 1), oc = idx / kG;
-        const int ov = nt * 32 + oc;
-        if (pi < cnt && ov < g.Cv) {
-            int n;
-            if (blocked) {  // virtual map (jy*bx + jx)*Co + o
-                const int jb = ov / g.Co, o = ov - jb * g.Co;
-                const int jy = jb / g.bx, jx = jb - jy * g.bx;
-                const int yx = tab[pi].yx;
-                if ((yx >> 16) + jy >= g.Ho || (yx & 0xffff) + jx >= g.Wo) continue;
-                n = tab[pi].obase + o * HoWo + jy * g.Wo + jx;
-            } else {
-                n = tab[pi].obase + ov * HoWo;
-            }
-            out_v[n] = stv[oc * kStageStride + pi];
-            out_t[n] = stt[oc * kStageStride + pi];
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+        const int ov = nt * 32 + oc0 + kMapStep * j;
+        if (ov >= g.Cv) continue;
+        int n;
+        if (blocked) {  // virtual map (jy*bx + jx)*Co + o
+            const int jb = ov / g.Co, o = ov - jb * g.Co;
+            const int jy = jb / g.bx, jx = jb - jy * g.bx;
+            if ((tb.yx >> 16) + jy >= g.Ho || (tb.yx & 0xffff) + jx >= g.Wo) continue;
+            n = tb.obase + o * HoWo + jy * g.Wo + jx;
+        } else {
+            n = tb.obase + ov * HoWo;
         }
+        out_v[n] = v[j];
+        out_t[n] = t[j];
     }
 }
 
@@ -643,9 +678,8 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
                uint8_t *__restrict__ out_t, float *__restrict__ out_v)
 {
     extern __shared__ __align__(16) uint8_t lds[];
-    uint8_t *hal = lds + kHalOff;
-    uint8_t *flags = lds + kFlagOff;
-    const uint8_t *flag = flags;
+    const uint8_t *hal = lds + kHalOff;
+    const uint8_t *flag = lds + kFlagOff;
     auto stv = [&](int i) { return reinterpret_cast<float *>(lds + kStvOff) + i * 32 * kStageStride; };
     auto stt = [&](int i) { return lds + kSttOff + i * 32 * kStageStride; };
     Tab *tabs = reinterpret_cast<Tab *>(lds + kTabOff);
@@ -694,13 +728,11 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
     // words a slice of the tile covers (see store_range)
     const int skip_pow = PT * ((g.Cp & 15) == 0 ? 1 : 2);
 
-    bool sparse;
     {
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        sparse = store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw,
-                             skip_pow);
+        store_range(load_range(xp, xp_words, a0, a1), lds, never4, range_words(a0, a1), g.hw);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -731,6 +763,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (it > 0)
             write_out(g, nt, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1), stt(cur ^ 1), out_t, out_v);
+        const bool sparse = group_sparse(lds, skip_pow);
         // tiles of the group go round the waves
         const int wp0 = gs + wv * PT, wp1 = gs + cnt, wstep = 4 * PT;
         int xo_next = tab[min(wp0 - gs + pl, cnt - 1)].xoff;
@@ -813,7 +846,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            sparse = store_range(nxt, hal, flags, never4, nxt_words, g.hw, skip_pow);
+            store_range(nxt, lds, never4, nxt_words, g.hw);
         }
     }
     __syncthreads();  // the last group is staged
@@ -834,8 +867,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
                  float theta, int nranges, uint8_t *__restrict__ out_t, float *__restrict__ out_v)
 {
     extern __shared__ __align__(16) uint8_t lds[];
-    uint8_t *hal = lds + kHalOff;
-    uint8_t *flags = lds + kFlagOff;
+    const uint8_t *hal = lds + kHalOff;
     auto stv = [&](int i) { return reinterpret_cast<float *>(lds + kStvOff) + i * 32 * kStageStride; };
     auto stt = [&](int i) { return lds + kSttOff + i * 32 * kStageStride; };
     Tab *tabs = reinterpret_cast<Tab *>(lds + kTabOff);
@@ -864,7 +896,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        (void)store_range(load_range(xp, xp_words, a0, a1), hal, flags, never4, range_words(a0, a1), g.hw, 1);
+        store_range(load_range(xp, xp_words, a0, a1), lds, never4, range_words(a0, a1), g.hw);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -961,7 +993,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            (void)store_range(nxt, hal, flags, never4, nxt_words, g.hw, 1);
+            store_range(nxt, lds, never4, nxt_words, g.hw);
         }
     }
     __syncthreads();  // the last group is staged
