@@ -528,10 +528,12 @@ __device__ __forceinline__ bool group_sparse(const uint8_t *lds, int pt)
     return skip > 0.4f;
 }
 
-// Staged results of positions [gs, min(gs + 64, p_end)) to the outputs:
-// consecutive threads take consecutive positions of one map, each thread one
-// position of every fourth map; all its staged values are read before the
-// stores.
+// Staged results of positions [gs, min(gs + 64, p_end)) to the outputs,
+// consecutive threads on consecutive positions of one map.  Unblocked
+// layouts: a thread takes four consecutive positions of two maps, each
+// written with one 16-byte and one 4-byte store where the four are
+// contiguous in the output.  Blocked layouts: a thread takes one position of
+// eight maps, all its staged values read before the stores.
 __device__ __forceinline__ void write_out(const PGeom &g, int nt, int gs, int p_end, const Tab *tab,
                                           const float *stv, const uint8_t *stt,
                                           uint8_t *__restrict__ out_t, float *__restrict__ out_v)
@@ -540,6 +542,42 @@ __device__ __forceinline__ void write_out(const PGeom &g, int nt, int gs, int p_
     constexpr int kMapStep = kThreads / kG;
     const int HoWo = g.Ho * g.Wo;
     const int cnt = min(p_end, gs + kG) - gs;
+    const bool blocked = g.by * g.bx > 1;
+    // (output bases aligned for the word stores: 16 bytes for V, 4 for t)
+    const bool aligned = ((reinterpret_cast<uintptr_t>(out_v) & 15) | (reinterpret_cast<uintptr_t>(out_t) & 3)) == 0;
+    if (!blocked && (HoWo & 3) == 0) {
+        // four consecutive positions of a map per thread, stored as one
+        // 16-byte V word and one 4-byte time word when they are contiguous
+        // and aligned in the output
+        constexpr int kQ = kG / 4, kMaps = kThreads / kQ;
+        const int p4 = 4 * (threadIdx.x % kQ), oc0 = threadIdx.x / kQ;
+        if (p4 >= cnt) return;
+        const Tab t0 = tab[p4];
+        const int n3 = tab[min(p4 + 3, kG - 1)].obase;
+        const bool vec = p4 + 3 < cnt && n3 == t0.obase + 3 && (t0.obase & 3) == 0 && aligned;
+#pragma unroll
+        for (int j = 0; j < 32 / kMaps; j++) {
+            const int oc = oc0 + kMaps * j, ov = nt * 32 + oc;
+            if (ov >= g.Cv) continue;
+            const float *sv = stv + oc * kStageStride + p4;
+            const uint8_t *st = stt + oc * kStageStride + p4;
+            if (vec) {
+                const float4 v4 = make_float4(sv[0], sv[1], sv[2], sv[3]);
+                const uint32_t tw = (uint32_t)st[0] | ((uint32_t)st[1] << 8) | ((uint32_t)st[2] << 16) |
+                                    ((uint32_t)st[3] << 24);
+                const int n = t0.obase + ov * HoWo;
+                *reinterpret_cast<float4 *>(out_v + n) = v4;
+                *reinterpret_cast<uint32_t *>(out_t + n) = tw;
+            } else {
+                for (int i = 0; i < 4 && p4 + i < cnt; i++) {
+                    const int n = tab[p4 + i].obase + ov * HoWo;
+                    out_v[n] = sv[i];
+                    out_t[n] = st[i];
+                }
+            }
+        }
+        return;
+    }
     const int pi = threadIdx.x & (kG - 1), oc0 = threadIdx.x / kG;
     if (pi >= cnt) return;
     const Tab tb = tab[pi];
@@ -551,7 +589,6 @@ __device__ __forceinline__ void write_out(const PGeom &g, int nt, int gs, int p_
         v[j] = stv[oc * kStageStride + pi];
         t[j] = stt[oc * kStageStride + pi];
     }
-    const bool blocked = g.by * g.bx > 1;
 #pragma unroll
     for (int j = 0; j < kPer; j++) {
         const int ov = nt * 32 + oc0 + kMapStep * j;

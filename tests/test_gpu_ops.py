@@ -255,6 +255,29 @@ def test_conv_fire_silent_input_and_negative_weights():
     check_fire(np_(g_tf2), np_(g_vk2), o_tf, o_vk, excused_from_potentials(o_V, 0.5))
 
 
+@pytest.mark.parametrize("case", [CONV_CASES[5], CONV_CASES[21]])
+def test_conv_fire_unaligned_outputs(case):
+    """Outputs off the 16-byte (V) and 4-byte (t) alignment the word stores
+    need: the element stores give the same bits, and nothing outside the
+    outputs is written."""
+    dev = gpu()
+    B, Ci, Hi, Wi, Co, K, s, p, T, theta, dens, dt = case
+    rng = np.random.default_rng(7)
+    times = _t(random_times(rng, (B, Ci, Hi, Wi), T, dens), dev)
+    w = _t(rng.uniform(0.0, 1.0, size=(Co, Ci, K, K)).astype(np.float32), dev)
+    w = w.to(torch.float16) if dt == "f16" else w
+    tf, vk = spk.spk_conv_fire(times, w, T, s, p, theta)
+    n = tf.numel()
+    bt = torch.full((n + 2,), 0xAB, dtype=torch.uint8, device=dev)
+    bv = torch.full((n + 2,), float("nan"), dtype=torch.float32, device=dev)
+    tf2, vk2 = spk.spk_conv_fire(times, w, T, s, p, theta, out_times=bt[1:n + 1].view(tf.shape),
+                                 out_vkey=bv[1:n + 1].view(vk.shape))
+    np.testing.assert_array_equal(np_(tf2), np_(tf))
+    np.testing.assert_array_equal(np_(vk2).view(np.uint32), np_(vk).view(np.uint32))
+    assert int(bt[0]) == 0xAB and int(bt[-1]) == 0xAB
+    assert math.isnan(float(bv[0])) and math.isnan(float(bv[-1]))
+
+
 # --------------------------------------------------------------------- pool
 
 @pytest.mark.parametrize("shape,k,s,p", [((3, 30, 28, 28), 2, 2, 0), ((2, 250, 14, 14), 3, 3, 1),
