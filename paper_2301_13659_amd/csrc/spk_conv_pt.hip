@@ -56,7 +56,6 @@ constexpr int kThreads = 256;
 constexpr int kG = 64;                         // positions per group
 constexpr int kStageStride = kG + 1;           // staged results: [map][position], padded
 constexpr int kRange = 16 * 1024;              // Xp bytes of a group's input rows (at most)
-constexpr int kPf = kRange / 16 / kThreads;    // 16-byte words per thread of a group's input
 constexpr int kSlackPT = 64;                   // readable bytes past the end of Xp
 constexpr uint32_t kSelLo = 0x04010400u;       // bytes 0,1 -> halves 1024 + b
 constexpr uint32_t kSelHi = 0x04030402u;       // bytes 2,3 -> halves 1024 + b
@@ -446,23 +445,27 @@ __device__ __forceinline__ void fill_table(const PGeom &g, int gs, int cnt, Tab 
     }
 }
 
-// The Xp bytes [a0, a1 + 32) (a0 16-aligned) as 16-byte words, kPf per
-// thread (word threadIdx.x + 256*i); words past the end of Xp read its last.
+// The Xp bytes [a0, a1 + 32) (a0 16-aligned) as 16-byte words, PF per
+// thread of a block of NTH (word threadIdx.x + NTH*i); words past the end of
+// Xp read its last.
+template <int NTH = kThreads>
 struct Staged {
-    uint4 w[kPf];
+    static constexpr int PF = (kRange / 16 + NTH - 1) / NTH;
+    uint4 w[PF];
 };
 
 __device__ __forceinline__ int range_words(int a0, int a1) { return (a1 - a0 + 32 + 15) / 16; }
 
-__device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words, int a0, int a1)
+template <int NTH = kThreads>
+__device__ __forceinline__ Staged<NTH> load_range(const uint8_t *xp, size_t xp_words, int a0, int a1)
 {
-    Staged st;
+    Staged<NTH> st;
     const size_t w0 = (size_t)a0 / 16;
     const int nw = range_words(a0, a1);
 #pragma unroll
-    for (int i = 0; i < kPf; i++) {
-        const int k = (int)threadIdx.x + kThreads * i;
-        if (kThreads * i < nw) {  // words past the range are neither loaded nor stored
+    for (int i = 0; i < Staged<NTH>::PF; i++) {
+        const int k = (int)threadIdx.x + NTH * i;
+        if (NTH * i < nw) {  // words past the range are neither loaded nor stored
             size_t w = w0 + (size_t)min(k, nw - 1);
             w = w < xp_words ? w : xp_words - 1;
             st.w[i] = reinterpret_cast<const uint4 *>(xp)[w];
@@ -473,16 +476,17 @@ __device__ __forceinline__ Staged load_range(const uint8_t *xp, size_t xp_words,
 
 // Staged words to LDS as halves 1024 + t, plus a flag per word: does any of
 // its 16 times fire within the window (clamped times: any byte below T)?
-// Each wave also records how many of its words are flagged, for
+// Each wave also records in cnt how many of its words are flagged, for
 // group_sparse.
-__device__ __forceinline__ void store_range(const Staged &st, uint8_t *lds, uint32_t never4, int nw, int hw)
+template <int NTH>
+__device__ __forceinline__ void store_range(const Staged<NTH> &st, uint8_t *hal, uint8_t *flags, int *cnt,
+                                            uint32_t never4, int nw, int hw)
 {
-    uint8_t *hal = lds + kHalOff, *flags = lds + kFlagOff;
     int flagged = 0, words = 0;
 #pragma unroll
-    for (int i = 0; i < kPf; i++) {
-        const int k = (int)threadIdx.x + kThreads * i;
-        if (kThreads * i >= nw) break;
+    for (int i = 0; i < Staged<NTH>::PF; i++) {
+        const int k = (int)threadIdx.x + NTH * i;
+        if (NTH * i >= nw) break;
         const uint4 v = st.w[i];
         const u4 lo = {__builtin_amdgcn_perm(0x64646464u, v.x, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.x, kSelHi),
                        __builtin_amdgcn_perm(0x64646464u, v.y, kSelLo), __builtin_amdgcn_perm(0x64646464u, v.y, kSelHi)};
@@ -493,14 +497,13 @@ __device__ __forceinline__ void store_range(const Staged &st, uint8_t *lds, uint
             reinterpret_cast<u4 *>(hal)[2 * k + 1] = hi;
         }
         const bool f = ((v.x ^ never4) | (v.y ^ never4) | (v.z ^ never4) | (v.w ^ never4)) != 0u;
-        flags[k] = f ? 1 : 0;
+        if (k < kRange / 16) flags[k] = f ? 1 : 0;  // (larger blocks have threads past the flag bytes)
         flagged += __builtin_popcountll(__builtin_amdgcn_ballot_w64(f && k < nw));
         words += __builtin_popcountll(__builtin_amdgcn_ballot_w64(k < nw));
     }
     if ((threadIdx.x & 63) == 0) {
-        int *cnt = reinterpret_cast<int *>(lds + kCntOff) + 2 * (threadIdx.x >> 6);
-        cnt[0] = flagged;
-        cnt[1] = words;
+        cnt[2 * (threadIdx.x >> 6)] = flagged;
+        cnt[2 * (threadIdx.x >> 6) + 1] = words;
     }
 }
 
@@ -513,12 +516,12 @@ __device__ __forceinline__ void store_range(const Staged &st, uint8_t *lds, uint
 // two otherwise); testing pays when that is above 40 % (below it the tests
 // cost more than the skipped products save).  One decision for the block
 // keeps its waves equally loaded between barriers.
-__device__ __forceinline__ bool group_sparse(const uint8_t *lds, int pt)
+template <int NW = kThreads / 64>
+__device__ __forceinline__ bool group_sparse(const int *cnt, int pt)
 {
-    const int *cnt = reinterpret_cast<const int *>(lds + kCntOff);
     int flagged = 0, words = 0;
 #pragma unroll
-    for (int w = 0; w < kThreads / 64; w++) {
+    for (int w = 0; w < NW; w++) {
         flagged += cnt[2 * w];
         words += cnt[2 * w + 1];
     }
@@ -769,7 +772,8 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        store_range(load_range(xp, xp_words, a0, a1), lds, never4, range_words(a0, a1), g.hw);
+        store_range(load_range(xp, xp_words, a0, a1), lds + kHalOff, lds + kFlagOff,
+                    reinterpret_cast<int *>(lds + kCntOff), never4, range_words(a0, a1), g.hw);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -788,7 +792,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         __syncthreads();  // this group's input and table are in LDS; group it-1 is staged
         const int gn = gs + kG;
         const bool more = gn < p_end;
-        Staged nxt;
+        Staged<> nxt;
         int nxt_words = 0;
         if (more) {
             int n0, n1;
@@ -800,7 +804,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (it > 0)
             write_out(g, nt, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1), stt(cur ^ 1), out_t, out_v);
-        const bool sparse = group_sparse(lds, skip_pow);
+        const bool sparse = group_sparse(reinterpret_cast<const int *>(lds + kCntOff), skip_pow);
         // tiles of the group go round the waves
         const int wp0 = gs + wv * PT, wp1 = gs + cnt, wstep = 4 * PT;
         int xo_next = tab[min(wp0 - gs + pl, cnt - 1)].xoff;
@@ -883,7 +887,8 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            store_range(nxt, lds, never4, nxt_words, g.hw);
+            store_range(nxt, lds + kHalOff, lds + kFlagOff, reinterpret_cast<int *>(lds + kCntOff), never4,
+                        nxt_words, g.hw);
         }
     }
     __syncthreads();  // the last group is staged
@@ -933,7 +938,8 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         int r0, r1;
         group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
         const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
-        store_range(load_range(xp, xp_words, a0, a1), lds, never4, range_words(a0, a1), g.hw);
+        store_range(load_range(xp, xp_words, a0, a1), lds + kHalOff, lds + kFlagOff,
+                    reinterpret_cast<int *>(lds + kCntOff), never4, range_words(a0, a1), g.hw);
         fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
     }
 
@@ -948,7 +954,7 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         __syncthreads();  // this group's input and table are in LDS; group it-1 is staged
         const int gn = gs + kG;
         const bool more = gn < p_end;
-        Staged nxt;
+        Staged<> nxt;
         int nxt_words = 0;
         if (more) {
             int n0, n1;
@@ -1030,12 +1036,264 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
         }
         if (more) {
             __syncthreads();  // every wave is done with this group's input
-            store_range(nxt, lds, never4, nxt_words, g.hw);
+            store_range(nxt, lds + kHalOff, lds + kFlagOff, reinterpret_cast<int *>(lds + kCntOff), never4,
+                        nxt_words, g.hw);
         }
     }
     __syncthreads();  // the last group is staged
     write_out(g, nt, p_begin + (it - 1) * kG, p_end, tabs + ((it - 1) % 3) * kG, stv((it - 1) & 1),
               stt((it - 1) & 1), out_t, out_v);
+}
+
+// ------------------------------------------------------------ LDS-fed firing
+//
+// k_fire_lb: the firing kernel with the B fragments of two column tiles (64
+// maps) in LDS instead of registers.  One block of NW waves fills a CU (the
+// fragments take SK*NP*2 KB of its LDS); each A fragment serves the products
+// of both column tiles, and with the fragments out of the registers three
+// waves share a SIMD, so one wave's epilogue, staging and waits overlap the
+// others' products.  Positions, groups, staging, slice skipping and the
+// epilogue are those of k_fire_pt; a block owns two column tiles of a range.
+constexpr int kNTB = 2;         // column tiles per block
+constexpr int kMB = 32 * kNTB;  // maps per block
+
+template <int SK, int NP>
+struct LbLayout {
+    static constexpr size_t stv = (size_t)SK * NP * kNTB * 64 * sizeof(h8);  // B fragments [s][k][c][lane] first
+    static constexpr size_t stt = stv + 2 * kMB * kStageStride * sizeof(float);
+    static constexpr size_t tab = (stt + 2 * kMB * kStageStride + 15) / 16 * 16;
+    static constexpr size_t cnt = tab + kTabBytes;
+    static constexpr size_t flag = cnt + 2 * 16 * sizeof(int);
+    static constexpr size_t hal = (flag + kRange / 16 + 15) / 16 * 16;
+};
+
+// Staged results of positions [gs, min(gs + 64, p_end)) of the block's 64
+// maps (first output map m0) to the outputs: four consecutive positions of a
+// map per thread, as in write_out.
+template <int NTH>
+__device__ __forceinline__ void write_out_lb(const PGeom &g, int m0, int gs, int p_end, const Tab *tab,
+                                             const float *stv, const uint8_t *stt,
+                                             uint8_t *__restrict__ out_t, float *__restrict__ out_v)
+{
+    constexpr int kQ = kG / 4;
+    const int HoWo = g.Ho * g.Wo;
+    const int cnt = min(p_end, gs + kG) - gs;
+    const bool aligned = ((reinterpret_cast<uintptr_t>(out_v) & 15) | (reinterpret_cast<uintptr_t>(out_t) & 3)) == 0;
+    for (int idx = threadIdx.x; idx < kQ * kMB; idx += NTH) {
+        const int p4 = 4 * (idx % kQ), oc = idx / kQ, ov = m0 + oc;
+        if (p4 >= cnt || ov >= g.Cv) continue;
+        const Tab t0 = tab[p4];
+        const int n3 = tab[min(p4 + 3, kG - 1)].obase;
+        const float *sv = stv + oc * kStageStride + p4;
+        const uint8_t *st = stt + oc * kStageStride + p4;
+        if (p4 + 3 < cnt && n3 == t0.obase + 3 && (t0.obase & 3) == 0 && (HoWo & 3) == 0 && aligned) {
+            const int n = t0.obase + ov * HoWo;
+            *reinterpret_cast<float4 *>(out_v + n) = make_float4(sv[0], sv[1], sv[2], sv[3]);
+            *reinterpret_cast<uint32_t *>(out_t + n) =
+                (uint32_t)st[0] | ((uint32_t)st[1] << 8) | ((uint32_t)st[2] << 16) | ((uint32_t)st[3] << 24);
+        } else {
+            for (int i = 0; i < 4 && p4 + i < cnt; i++) {
+                const int n = tab[p4 + i].obase + ov * HoWo;
+                out_v[n] = sv[i];
+                out_t[n] = st[i];
+            }
+        }
+    }
+}
+
+// SK (= the layer's packed slices), NP, kMode, QC and TPC as in k_fire_pt
+// (QC and TPC fixed: instances are made per layout); NW waves per block.
+template <int SK, int NP, int kMode, int QC, int TPC, int NW>
+__global__ __launch_bounds__(64 * NW) void k_fire_lb(const uint8_t *__restrict__ xp, size_t xp_words,
+                                                     const h8 *__restrict__ bp, PGeom g, float theta,
+                                                     int nranges, uint8_t *__restrict__ out_t,
+                                                     float *__restrict__ out_v)
+{
+    constexpr int NTH = 64 * NW;
+    typedef LbLayout<SK, NP> L;
+    extern __shared__ __align__(16) uint8_t lds[];
+    h8 *bl = reinterpret_cast<h8 *>(lds);
+    const uint8_t *hal = lds + L::hal;
+    const uint8_t *flag = lds + L::flag;
+    int *cntw = reinterpret_cast<int *>(lds + L::cnt);
+    auto stv = [&](int i) { return reinterpret_cast<float *>(lds + L::stv) + i * kMB * kStageStride; };
+    auto stt = [&](int i) { return lds + L::stt + i * kMB * kStageStride; };
+    Tab *tabs = reinterpret_cast<Tab *>(lds + L::tab);
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // block -> (column pair, range); the column pairs of a range share an XCD
+    const int ncb = (g.NT + kNTB - 1) / kNTB;
+    const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
+    const int cb = q % ncb;
+    const int range = xcd + 8 * (q / ncb);
+    if (range >= nranges) return;
+    const int p_begin = (int)((long long)range * g.P / nranges);
+    const int p_end = (int)((long long)(range + 1) * g.P / nranges);
+    if (p_begin >= p_end) return;
+
+    // the B fragments of column tiles 2cb and 2cb + 1 (zero past the last)
+    for (int i = threadIdx.x; i < SK * NP * kNTB * 64; i += NTH) {
+        const int ln = i & 63, c = (i >> 6) % kNTB, sk = i / (64 * kNTB);
+        const int nt = cb * kNTB + c;
+        h8 v = (h8)((_Float16)0.0f);
+        if (nt < g.NT) v = bp[((size_t)nt * g.SKp * NP + sk) * 64 + ln];
+        bl[i] = v;
+    }
+
+    int off2[SK];
+#pragma unroll
+    for (int s = 0; s < SK; s++) off2[s] = 2 * (s / QC) * g.rowb + 32 * (s % QC);
+    const int my_off = lane < g.SK ? (lane / g.Q16) * g.rowb + (lane % g.Q16) * 16 : -1;
+
+    const int r = lane & 31, hh = lane >> 5;
+    constexpr int lgTP = TPC == 8 ? 3 : (TPC == 16 ? 4 : 5);
+    int pl, tt;
+    row_slot_step(r, lgTP, pl, tt);
+    const uint32_t cbv = 0x6401u + (uint32_t)min(tt, g.T - 1);
+    const h2 cc = as_h2(cbv | (cbv << 16));
+    constexpr int PT = 32 >> lgTP;
+    const uint32_t never4 = 0x01010101u * (uint32_t)g.T;
+    const int skip_pow = PT * ((g.Cp & 15) == 0 ? 1 : 2);
+
+    {
+        int r0, r1;
+        group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
+        store_range(load_range<NTH>(xp, xp_words, a0, a1), lds + L::hal, lds + L::flag, cntw, never4,
+                    range_words(a0, a1), g.hw);
+        fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
+    }
+
+    int it = 0;
+    for (int gs = p_begin; gs < p_end; gs += kG, it++) {
+        const int cnt = min(p_end, gs + kG) - gs;
+        const int cur = it & 1;
+        const Tab *tab = tabs + (it % 3) * kG;
+        int r0, r1;
+        group_rows(g, gs, gs + cnt - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15;
+        __syncthreads();  // this group's input and table are in LDS; group it-1 is staged
+        const int gn = gs + kG;
+        const bool more = gn < p_end;
+        Staged<NTH> nxt;
+        int nxt_words = 0;
+        if (more) {
+            int n0, n1;
+            group_rows(g, gn, min(p_end, gn + kG) - 1, n0, n1);
+            const int b0 = (n0 * g.rowb) & ~15, b1 = n1 * g.rowb;
+            nxt = load_range<NTH>(xp, xp_words, b0, b1);
+            nxt_words = range_words(b0, b1);
+            fill_table(g, gn, min(p_end, gn + kG) - gn, tabs + ((it + 1) % 3) * kG);
+        }
+        if (it > 0)
+            write_out_lb<NTH>(g, cb * kMB, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1),
+                              stt(cur ^ 1), out_t, out_v);
+        const bool sparse = group_sparse<NW>(cntw, skip_pow);
+        // tiles of the group go round the waves
+        const int wp0 = gs + wv * PT, wp1 = gs + cnt, wstep = NW * PT;
+        int xo_next = tab[min(wp0 - gs + pl, cnt - 1)].xoff;
+        for (int tp0 = wp0; tp0 < wp1; tp0 += wstep) {
+            const int org2 = 2 * (xo_next - a0 + 8 * hh);
+            auto rdw = [&](int s) -> u4 { return lds_read16<kMode>(hal, org2 + off2[s]); };
+            auto rdb = [&](int s, int k, int c) -> h8 { return bl[((s * NP + k) * kNTB + c) * 64 + lane]; };
+            f16v acc[kNTB];
+#pragma unroll
+            for (int c = 0; c < kNTB; c++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) acc[c][e] = 0.0f;
+            uint64_t live = ~0ull;
+            if (sparse) {
+                live = 0ull;
+                for (int j = 0; j < PT; j++) {
+                    const int xo = tab[min(tp0 - gs + j, cnt - 1)].xoff - a0;
+                    bool f = false;
+                    if (my_off >= 0) {
+                        const int at = xo + my_off;
+                        f = (flag[at >> 4] | flag[(at + 15) >> 4]) != 0;
+                    }
+                    live |= __builtin_amdgcn_ballot_w64(f);
+                }
+            }
+            // window reads two slices ahead, B reads one
+            constexpr int kAhead = 2, kAheadB = 1;
+            u4 win[kAhead];
+            h8 bq[kAheadB][NP][kNTB];
+#pragma unroll
+            for (int s = 0; s < kAhead && s < SK; s++) win[s] = rdw(s);
+#pragma unroll
+            for (int s = 0; s < kAheadB && s < SK; s++)
+#pragma unroll
+                for (int k = 0; k < NP; k++)
+#pragma unroll
+                    for (int c = 0; c < kNTB; c++) bq[s][k][c] = rdb(s, k, c);
+            auto slice = [&](int s, bool run) {
+                const u4 x = win[s % kAhead];
+                h8 b[NP][kNTB];
+#pragma unroll
+                for (int k = 0; k < NP; k++)
+#pragma unroll
+                    for (int c = 0; c < kNTB; c++) b[k][c] = bq[s % kAheadB][k][c];
+                if (s + kAhead < SK) win[s % kAhead] = rdw(s + kAhead);
+                if (s + kAheadB < SK)
+#pragma unroll
+                    for (int k = 0; k < NP; k++)
+#pragma unroll
+                        for (int c = 0; c < kNTB; c++) bq[s % kAheadB][k][c] = rdb(s + kAheadB, k, c);
+                if (run) {
+                    const h8 a = frag_upto(x, cc);
+#pragma unroll
+                    for (int k = 0; k < NP; k++)
+#pragma unroll
+                        for (int c = 0; c < kNTB; c++)
+                            acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b[k][c], acc[c], 0, 0, 0);
+                }
+            };
+            if (!sparse) {
+#pragma unroll
+                for (int s = 0; s < SK; s++) {
+                    slice(s, true);
+                    if constexpr (kMode >= 1) {
+                        // per slice: the window and B reads, the fragment's four
+                        // VALU ops, then the products
+                        constexpr int kReads = (kMode == 1 ? 2 : 1) + NP * kNTB;
+                        if (s + kAheadB < SK) __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x008, NP * kNTB, 0);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int s = 0; s < SK; s++) {
+                    const uint32_t lw = s < 32 ? (uint32_t)live : (uint32_t)(live >> 32);
+                    slice(s, __builtin_expect((lw >> (s & 31)) & 1u, 1));
+                }
+            }
+            if (tp0 + wstep < wp1) xo_next = tab[min(tp0 + wstep - gs + pl, cnt - 1)].xoff;
+            const int o = lane & 31, ns = slots_held(lgTP, hh);
+#pragma unroll
+            for (int c = 0; c < kNTB; c++) {
+                uint32_t st[2] = {0u, 0u};
+                float sv[2] = {0.0f, 0.0f};
+                tile_epilogue<TPC>(acc[c], theta, hh, st, sv);
+#pragma unroll
+                for (int k = 0; k < 2; k++) {
+                    const int pi = tp0 - gs + slot_of(lgTP, hh, k);
+                    if (k < ns && pi < cnt) {
+                        stv(cur)[(c * 32 + o) * kStageStride + pi] = sv[k];
+                        stt(cur)[(c * 32 + o) * kStageStride + pi] = (uint8_t)st[k];
+                    }
+                }
+            }
+        }
+        if (more) {
+            __syncthreads();  // every wave is done with this group's input
+            store_range(nxt, lds + L::hal, lds + L::flag, cntw, never4, nxt_words, g.hw);
+        }
+    }
+    __syncthreads();  // the last group is staged
+    write_out_lb<NTH>(g, cb * kMB, p_begin + (it - 1) * kG, p_end, tabs + ((it - 1) % 3) * kG,
+                      stv((it - 1) & 1), stt((it - 1) & 1), out_t, out_v);
 }
 
 // Kernel instances: slice counts rounded up to these (the extra slices have
@@ -1105,6 +1363,31 @@ const PtLaunch kLaunch1[9][4] = {SPK_PT(4, 1),  SPK_PT(8, 1),  SPK_PT(12, 1), SP
 const PtLaunch kDeep[2][4] = {{&launch_deep<1, 0>, &launch_deep<1, 1>, &launch_deep<1, 2>, &launch_deep<1, 3>},
                               {&launch_deep<2, 0>, &launch_deep<2, 1>, &launch_deep<2, 2>, &launch_deep<2, 3>}};
 
+template <int SK, int NP, int kMode, int QC, int TPC, int NW>
+void launch_lb(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t xw, const h8 *bp,
+               const PGeom &g, float theta, int nranges, uint8_t *ot, float *ov)
+{
+    auto kern = k_fire_lb<SK, NP, kMode, QC, TPC, NW>;
+    static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 160 * 1024) == hipSuccess;
+    (void)attr;
+    hipLaunchKernelGGL(kern, grid, dim3(64 * NW), lds, s, xp, xw, bp, g, theta, nranges, ot, ov);
+}
+
+// Layouts the LDS-fed kernel is made for (as kExact), with the LDS it needs
+// before the staged input: 3x3 over 64 channels with half weights and 32
+// steps per position.  (3x3 over 32 padded channels with float masters, the
+// three-layer net's conv2, ran slower in it: 56 against 54 us.)
+struct LbExact {
+    int SK, QC, NP, mode, TP;
+    size_t hal;
+    PtLaunch fn;
+};
+const LbExact kLbExact[] = {
+    {36, 12, 1, 3, 32, LbLayout<36, 1>::hal, &launch_lb<36, 1, 3, 12, 32, 12>},
+};
+
 // Largest staged row range over the groups of every range (exact, per geometry).
 int max_rows(const PGeom &g, int nranges)
 {
@@ -1155,6 +1438,14 @@ int n_ranges(const PGeom &g)
 }
 
 size_t fire_lds(const PGeom &g) { return kHalOff + 32 * (size_t)g.hw; }
+
+// Ranges of the LDS-fed kernel: one block per CU, ncb column pairs per range.
+int n_ranges_lb(const PGeom &g, int ncb)
+{
+    int nr = std::max(1, cu_count() / ncb);
+    nr = std::min(nr, std::max(1, g.P / 16));
+    return nr;
+}
 
 }  // namespace
 
@@ -1223,6 +1514,26 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
     const int per_xcd = (nranges + 7) / 8;
     const dim3 grid(8 * g.NT * per_xcd);
     const size_t xw = ((size_t)g.B * g.Hp * g.rowb + g.slack) / 16;
+    // the LDS-fed kernel for the layouts it is made for, when a group's rows
+    // fit its staging and everything fits a CU's LDS
+    if (g.by * g.bx == 1 && g.NT >= 2 && g.SKp == g.SK) {
+        for (const LbExact &e : kLbExact) {
+            if (e.SK != g.SK || e.QC != g.Q16 || e.NP != (half_w ? 1 : 2) || e.mode != read_mode(g.Cp) ||
+                e.TP != g.TP)
+                continue;
+            const int ncb = (g.NT + kNTB - 1) / kNTB;
+            const int nr = n_ranges_lb(g, ncb);
+            const long long rows = max_rows(g, nr);
+            if (rows * g.rowb + 64 > kRange) break;
+            PGeom gl = g;
+            gl.hw = (int)((rows * g.rowb + 64 + 47) / 16);
+            const size_t lds = e.hal + 32 * (size_t)gl.hw;
+            if (lds > 160 * 1024) break;
+            const size_t xw = ((size_t)g.B * g.Hp * g.rowb + g.slack) / 16;
+            e.fn(dim3(8 * ncb * ((nr + 7) / 8)), lds, s, xp, xw, bp, gl, theta, nr, out_t, out_v);
+            return check_launch("spk_conv_fire");
+        }
+    }
     PtLaunch launch;
     if (instance_sk(g.SK, half_w)) {
         int idx = 0;

@@ -195,6 +195,9 @@ CONV_CASES = [
     (2, 8, 17, 19, 2, 5, 1, 2, 9, 3.0, 0.3, "f16"),         # two maps, half weights: 4 x 4 blocks
     (3, 12, 11, 20, 24, 3, 1, 1, 9, 4.0, 0.3, "f32"),       # 4 x 4 byte-transpose packing, padded channels
     (2, 4, 15, 16, 10, 3, 2, 1, 6, 2.0, 0.4, "f16"),        # the same with 4 channels and stride 2
+    (2, 64, 12, 12, 96, 3, 1, 1, 30, 20.0, 0.05, "f16"),    # LDS-fed kernel: three column tiles (a pair
+                                                            # with a zero second tile)
+    (2, 64, 9, 13, 40, 3, 1, 1, 20, 12.0, 0.1, "f16"),      # LDS-fed kernel: 40 maps, T = 20, ragged
 ]
 
 
