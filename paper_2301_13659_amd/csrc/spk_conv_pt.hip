@@ -513,11 +513,12 @@ __device__ __forceinline__ void store_range(const Staged<NTH> &st, uint8_t *hal,
 // the tile's words under it fires, so with a fraction u of the words
 // unflagged about u^pt of the slices are skipped, pt being the words a slice
 // of the tile covers (one per position when window runs are 16-byte aligned,
-// two otherwise); testing pays when that is above 40 % (below it the tests
-// cost more than the skipped products save).  One decision for the block
-// keeps its waves equally loaded between barriers.
+// two otherwise); testing pays when that is above min_skip (below it the
+// tests cost more than the skipped products save: 40 % for k_fire_pt, 15 %
+// for k_fire_lb, where a skipped slice saves two products).  One decision for
+// the block keeps its waves equally loaded between barriers.
 template <int NW = kThreads / 64>
-__device__ __forceinline__ bool group_sparse(const int *cnt, int pt)
+__device__ __forceinline__ bool group_sparse(const int *cnt, int pt, float min_skip)
 {
     int flagged = 0, words = 0;
 #pragma unroll
@@ -528,7 +529,7 @@ __device__ __forceinline__ bool group_sparse(const int *cnt, int pt)
     const float u = words > 0 ? (float)(words - flagged) / (float)words : 0.0f;
     float skip = u;
     for (int i = 1; i < pt; i++) skip *= u;
-    return skip > 0.4f;
+    return skip > min_skip;
 }
 
 // Staged results of positions [gs, min(gs + 64, p_end)) to the outputs,
@@ -804,7 +805,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
         }
         if (it > 0)
             write_out(g, nt, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1), stt(cur ^ 1), out_t, out_v);
-        const bool sparse = group_sparse(reinterpret_cast<const int *>(lds + kCntOff), skip_pow);
+        const bool sparse = group_sparse(reinterpret_cast<const int *>(lds + kCntOff), skip_pow, 0.4f);
         // tiles of the group go round the waves
         const int wp0 = gs + wv * PT, wp1 = gs + cnt, wstep = 4 * PT;
         int xo_next = tab[min(wp0 - gs + pl, cnt - 1)].xoff;
@@ -1189,7 +1190,7 @@ __global__ __launch_bounds__(64 * NW) void k_fire_lb(const uint8_t *__restrict__
         if (it > 0)
             write_out_lb<NTH>(g, cb * kMB, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1),
                               stt(cur ^ 1), out_t, out_v);
-        const bool sparse = group_sparse<NW>(cntw, skip_pow);
+        const bool sparse = group_sparse<NW>(cntw, skip_pow, 0.15f);
         // tiles of the group go round the waves
         const int wp0 = gs + wv * PT, wp1 = gs + cnt, wstep = NW * PT;
         int xo_next = tab[min(wp0 - gs + pl, cnt - 1)].xoff;
