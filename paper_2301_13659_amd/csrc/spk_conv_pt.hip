@@ -1378,8 +1378,9 @@ void launch_lb(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t x
 
 // Layouts the LDS-fed kernel is made for (as kExact), with the LDS it needs
 // before the staged input: 3x3 over 64 channels with half weights and 32
-// steps per position.  (3x3 over 32 padded channels with float masters, the
-// three-layer net's conv2, ran slower in it: 56 against 54 us.)
+// steps per position; 5x5 over 6 channels with float masters and 16.  (3x3
+// over 32 padded channels with float masters, the three-layer net's conv2,
+// ran slower in it: 56 against 54 us.)
 struct LbExact {
     int SK, QC, NP, mode, TP;
     size_t hal;
@@ -1387,6 +1388,7 @@ struct LbExact {
 };
 const LbExact kLbExact[] = {
     {36, 12, 1, 3, 32, LbLayout<36, 1>::hal, &launch_lb<36, 1, 3, 12, 32, 12>},
+    {10, 2, 2, 1, 16, LbLayout<10, 2>::hal, &launch_lb<10, 2, 1, 2, 16, 12>},
 };
 
 // Largest staged row range over the groups of every range (exact, per geometry).

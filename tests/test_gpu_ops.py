@@ -198,6 +198,8 @@ CONV_CASES = [
     (2, 64, 12, 12, 96, 3, 1, 1, 30, 20.0, 0.05, "f16"),    # LDS-fed kernel: three column tiles (a pair
                                                             # with a zero second tile)
     (2, 64, 9, 13, 40, 3, 1, 1, 20, 12.0, 0.1, "f16"),      # LDS-fed kernel: 40 maps, T = 20, ragged
+    (2, 6, 20, 22, 70, 5, 1, 2, 15, 16.0, 0.3, "f32"),      # LDS-fed kernel, 5x5 over 6 channels, float
+                                                            # masters: three column tiles
 ]
 
 
