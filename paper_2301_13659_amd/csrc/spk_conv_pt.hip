@@ -843,6 +843,8 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
             u4 win[kAhead];
 #pragma unroll
             for (int s = 0; s < kAhead && s < SK; s++) win[s] = rd(s);
+            // the products at a raised wave priority (see k_fire_lb)
+            __builtin_amdgcn_s_setprio(2);
             if (!sparse) {
 #pragma unroll
                 for (int s = 0; s < SK; s++) {
@@ -869,6 +871,7 @@ void k_fire_pt(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__rest
                     if (__builtin_expect((lw >> (s & 31)) & 1u, 1)) step(s, x);
                 }
             }
+            __builtin_amdgcn_s_setprio(0);
             // the next tile's window origin, read while this one finishes
             if (tp0 + wstep < wp1) xo_next = tab[min(tp0 + wstep - gs + pl, cnt - 1)].xoff;
             uint32_t st[2] = {0u, 0u};
@@ -1250,6 +1253,10 @@ __global__ __launch_bounds__(64 * NW) void k_fire_lb(const uint8_t *__restrict__
                             acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b[k][c], acc[c], 0, 0, 0);
                 }
             };
+            // the products run at a raised wave priority, so that a wave in
+            // its slice loop issues ahead of the waves in their epilogue or
+            // staging on the same SIMD
+            __builtin_amdgcn_s_setprio(2);
             if (!sparse) {
 #pragma unroll
                 for (int s = 0; s < SK; s++) {
@@ -1270,6 +1277,7 @@ __global__ __launch_bounds__(64 * NW) void k_fire_lb(const uint8_t *__restrict__
                     slice(s, __builtin_expect((lw >> (s & 31)) & 1u, 1));
                 }
             }
+            __builtin_amdgcn_s_setprio(0);
             if (tp0 + wstep < wp1) xo_next = tab[min(tp0 + wstep - gs + pl, cnt - 1)].xoff;
             const int o = lane & 31, ns = slots_held(lgTP, hh);
 #pragma unroll
