@@ -478,6 +478,9 @@ void k_rate_conv16(const uint8_t *__restrict__ x8, const h8 *__restrict__ bp, RG
             f4 acc[NC];
 #pragma unroll
             for (int c = 0; c < NC; c++) acc[c] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+            // the step's products at a raised wave priority, ahead of other
+            // waves' fire updates and stores on the SIMD
+            __builtin_amdgcn_s_setprio(2);
 #pragma unroll
             for (int kb = 0; kb < KB; kb++) {
                 const h8 a = frag_ind(A[j][kb]);
@@ -487,6 +490,7 @@ void k_rate_conv16(const uint8_t *__restrict__ x8, const h8 *__restrict__ bp, RG
                     for (int k = 0; k < NP; k++)
                         acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw[c][kb][k], acc[c], 0, 0, 0);
             }
+            __builtin_amdgcn_s_setprio(0);
             // the operands of step t + D replace this step's
             if (t + D < g.T) load_step(t + D, A[j]);
 #pragma unroll
