@@ -1054,9 +1054,9 @@ void k_fire_deep(const uint8_t *__restrict__ xp, size_t xp_words, const h8 *__re
 // k_fire_lb: the firing kernel with the B fragments of two column tiles (64
 // maps) in LDS instead of registers.  One block of NW waves fills a CU (the
 // fragments take SK*NP*2 KB of its LDS); each A fragment serves the products
-// of both column tiles, and with the fragments out of the registers three
-// waves share a SIMD, so one wave's epilogue, staging and waits overlap the
-// others' products.  Positions, groups, staging, slice skipping and the
+// of both column tiles, and with the fragments out of the registers three or
+// four waves share a SIMD, so one wave's epilogue, staging and waits overlap
+// the others' products.  Positions, groups, staging, slice skipping and the
 // epilogue are those of k_fire_pt; a block owns two column tiles of a range.
 constexpr int kNTB = 2;         // column tiles per block
 constexpr int kMB = 32 * kNTB;  // maps per block
@@ -1219,31 +1219,20 @@ __global__ __launch_bounds__(64 * NW) void k_fire_lb(const uint8_t *__restrict__
                     live |= __builtin_amdgcn_ballot_w64(f);
                 }
             }
-            // window reads two slices ahead, B reads one
-            constexpr int kAhead = 2, kAheadB = 1;
+            // window reads two slices ahead; the B fragments are read where
+            // they are used (in a sparse tile, only for its live slices)
+            constexpr int kAhead = 2;
             u4 win[kAhead];
-            h8 bq[kAheadB][NP][kNTB];
 #pragma unroll
             for (int s = 0; s < kAhead && s < SK; s++) win[s] = rdw(s);
-#pragma unroll
-            for (int s = 0; s < kAheadB && s < SK; s++)
-#pragma unroll
-                for (int k = 0; k < NP; k++)
-#pragma unroll
-                    for (int c = 0; c < kNTB; c++) bq[s][k][c] = rdb(s, k, c);
             auto slice = [&](int s, bool run) {
                 const u4 x = win[s % kAhead];
                 h8 b[NP][kNTB];
 #pragma unroll
                 for (int k = 0; k < NP; k++)
 #pragma unroll
-                    for (int c = 0; c < kNTB; c++) b[k][c] = bq[s % kAheadB][k][c];
+                    for (int c = 0; c < kNTB; c++) b[k][c] = rdb(s, k, c);
                 if (s + kAhead < SK) win[s % kAhead] = rdw(s + kAhead);
-                if (s + kAheadB < SK)
-#pragma unroll
-                    for (int k = 0; k < NP; k++)
-#pragma unroll
-                        for (int c = 0; c < kNTB; c++) bq[s % kAheadB][k][c] = rdb(s + kAheadB, k, c);
                 if (run) {
                     const h8 a = frag_upto(x, cc);
 #pragma unroll
@@ -1265,7 +1254,7 @@ __global__ __launch_bounds__(64 * NW) void k_fire_lb(const uint8_t *__restrict__
                         // per slice: the window and B reads, the fragment's four
                         // VALU ops, then the products
                         constexpr int kReads = (kMode == 1 ? 2 : 1) + NP * kNTB;
-                        if (s + kAheadB < SK) __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
                         __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
                         __builtin_amdgcn_sched_group_barrier(0x008, NP * kNTB, 0);
                     }
@@ -1395,7 +1384,7 @@ struct LbExact {
     PtLaunch fn;
 };
 const LbExact kLbExact[] = {
-    {36, 12, 1, 3, 32, LbLayout<36, 1>::hal, &launch_lb<36, 1, 3, 12, 32, 12>},
+    {36, 12, 1, 3, 32, LbLayout<36, 1>::hal, &launch_lb<36, 1, 3, 12, 32, 16>},
     {10, 2, 2, 1, 16, LbLayout<10, 2>::hal, &launch_lb<10, 2, 1, 2, 16, 12>},
 };
 
