@@ -283,6 +283,26 @@ def test_conv_fire_unaligned_outputs(case):
     assert math.isnan(float(bv[0])) and math.isnan(float(bv[-1]))
 
 
+@pytest.mark.parametrize("shape", [(128, 10, 10, 128, 0.05), (128, 20, 20, 96, 0.1)])
+def test_conv_fire_ranges_of_several_groups(shape):
+    """Half weights, 3x3 over 64 channels, T = 30, B = 128 samples of 10x10 or
+    20x20 (one sample per block range: two or seven 64-position groups, the
+    last one ragged; 96 maps leave the second tile of a column pair empty).
+    The oracle's event form gives the same bits (half weights sum exactly in
+    any order)."""
+    dev = gpu()
+    B, H, W, Co, dens = shape
+    T, theta = 30, 20.0
+    rng = np.random.default_rng(H * 1000 + Co)
+    times = random_times(rng, (B, 64, H, W), T, dens)
+    w16 = rng.uniform(0.7, 0.9, size=(Co, 64, 3, 3)).astype(np.float16)
+    tf, vk = spk.spk_conv_fire(_t(times, dev), _t(w16, dev), T, 1, 1, theta)
+    sp, off = oracle.times_to_spikes(times, T)
+    o_tf, o_vk = oracle.conv_fire_spikes(sp, off, times.shape[1:], w16.astype(np.float32), T, 1, 1, theta)
+    np.testing.assert_array_equal(np_(tf), o_tf)
+    np.testing.assert_array_equal(np_(vk), o_vk)
+
+
 # --------------------------------------------------------------------- pool
 
 @pytest.mark.parametrize("shape,k,s,p", [((3, 30, 28, 28), 2, 2, 0), ((2, 250, 14, 14), 3, 3, 1),
