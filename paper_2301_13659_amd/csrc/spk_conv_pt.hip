@@ -1071,10 +1071,10 @@ struct LbLayout {
     static constexpr size_t hal = (flag + kRange / 16 + 15) / 16 * 16;
 };
 
-// Staged results of positions [gs, min(gs + 64, p_end)) of the block's 64
+// Staged results of positions [gs, min(gs + 64, p_end)) of the block's NM
 // maps (first output map m0) to the outputs: four consecutive positions of a
 // map per thread, as in write_out.
-template <int NTH>
+template <int NTH, int NM = kMB>
 __device__ __forceinline__ void write_out_lb(const PGeom &g, int m0, int gs, int p_end, const Tab *tab,
                                              const float *stv, const uint8_t *stt,
                                              uint8_t *__restrict__ out_t, float *__restrict__ out_v)
@@ -1083,7 +1083,7 @@ __device__ __forceinline__ void write_out_lb(const PGeom &g, int m0, int gs, int
     const int HoWo = g.Ho * g.Wo;
     const int cnt = min(p_end, gs + kG) - gs;
     const bool aligned = ((reinterpret_cast<uintptr_t>(out_v) & 15) | (reinterpret_cast<uintptr_t>(out_t) & 3)) == 0;
-    for (int idx = threadIdx.x; idx < kQ * kMB; idx += NTH) {
+    for (int idx = threadIdx.x; idx < kQ * NM; idx += NTH) {
         const int p4 = 4 * (idx % kQ), oc = idx / kQ, ov = m0 + oc;
         if (p4 >= cnt || ov >= g.Cv) continue;
         const Tab t0 = tab[p4];
@@ -1294,6 +1294,211 @@ __global__ __launch_bounds__(64 * NW) void k_fire_lb(const uint8_t *__restrict__
                       stv((it - 1) & 1), stt((it - 1) & 1), out_t, out_v);
 }
 
+// k_fire_lbk: the LDS-fed firing kernel for layers whose B fragments do not
+// fit LDS whole (k_fire_deep's layers): one column tile per block, its
+// fragments staged KC slices (one kernel row) at a time.  A wave keeps the
+// accumulators of its TPW tiles of the group across the chunks; the next
+// chunk's fragments are loaded into registers while the current one's
+// products run.  Staging, slice skipping, the epilogue and the write-out are
+// those of k_fire_lb.
+template <int KC, int NP>
+struct LbkLayout {
+    static constexpr size_t stv = (size_t)KC * NP * 64 * sizeof(h8);  // B chunk [s][k][lane] first
+    static constexpr size_t stt = stv + 2 * 32 * kStageStride * sizeof(float);
+    static constexpr size_t tab = (stt + 2 * 32 * kStageStride + 15) / 16 * 16;
+    static constexpr size_t cnt = tab + kTabBytes;
+    static constexpr size_t flag = cnt + 2 * 16 * sizeof(int);
+    static constexpr size_t hal = (flag + kRange / 16 + 15) / 16 * 16;
+};
+
+template <int SKT, int NP, int kMode, int QC, int TPC, int NW, int KC>
+__global__ __launch_bounds__(64 * NW) void k_fire_lbk(const uint8_t *__restrict__ xp, size_t xp_words,
+                                                      const h8 *__restrict__ bp, PGeom g, float theta,
+                                                      int nranges, uint8_t *__restrict__ out_t,
+                                                      float *__restrict__ out_v)
+{
+    static_assert(SKT % KC == 0 && SKT <= 64, "whole chunks, slices within the live mask");
+    constexpr int NTH = 64 * NW;
+    constexpr int NCH = SKT / KC;
+    constexpr int lgTP = TPC == 8 ? 3 : (TPC == 16 ? 4 : 5);
+    constexpr int PT = 32 >> lgTP;
+    constexpr int TPW = (kG / PT + NW - 1) / NW;          // tiles of a group per wave
+    constexpr int CW = KC * NP * 64;                      // fragments of a chunk
+    constexpr int BPF = (CW + NTH - 1) / NTH;             // of them per thread
+    typedef LbkLayout<KC, NP> L;
+    extern __shared__ __align__(16) uint8_t lds[];
+    h8 *bl = reinterpret_cast<h8 *>(lds);
+    const uint8_t *hal = lds + L::hal;
+    const uint8_t *flag = lds + L::flag;
+    int *cntw = reinterpret_cast<int *>(lds + L::cnt);
+    auto stv = [&](int i) { return reinterpret_cast<float *>(lds + L::stv) + i * 32 * kStageStride; };
+    auto stt = [&](int i) { return lds + L::stt + i * 32 * kStageStride; };
+    Tab *tabs = reinterpret_cast<Tab *>(lds + L::tab);
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // block -> (column tile, range); the column tiles of a range share an XCD
+    const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
+    const int nt = q % g.NT;
+    const int range = xcd + 8 * (q / g.NT);
+    if (range >= nranges) return;
+    const int p_begin = (int)((long long)range * g.P / nranges);
+    const int p_end = (int)((long long)(range + 1) * g.P / nranges);
+    if (p_begin >= p_end) return;
+
+    // chunk c's fragments of this thread into registers (slices past the
+    // layer's are zero in the packed operand)
+    const h8 *bcol = bp + (size_t)nt * g.SKp * NP * 64;
+    h8 bpre[BPF];
+    auto fetch = [&](int c) {
+#pragma unroll
+        for (int i = 0; i < BPF; i++) {
+            const int e = (int)threadIdx.x + NTH * i;
+            if (e < CW) bpre[i] = bcol[(size_t)c * CW + e];
+        }
+    };
+    auto put = [&]() {
+#pragma unroll
+        for (int i = 0; i < BPF; i++) {
+            const int e = (int)threadIdx.x + NTH * i;
+            if (e < CW) bl[e] = bpre[i];
+        }
+    };
+    fetch(0);
+
+    const int my_off = lane < g.SK ? (lane / g.Q16) * g.rowb + (lane % g.Q16) * 16 : -1;
+    const int r = lane & 31, hh = lane >> 5;
+    int pl, tt;
+    row_slot_step(r, lgTP, pl, tt);
+    const uint32_t cbv = 0x6401u + (uint32_t)min(tt, g.T - 1);
+    const h2 cc = as_h2(cbv | (cbv << 16));
+    const uint32_t never4 = 0x01010101u * (uint32_t)g.T;
+    const int skip_pow = PT * ((g.Cp & 15) == 0 ? 1 : 2);
+
+    {
+        int r0, r1;
+        group_rows(g, p_begin, min(p_end, p_begin + kG) - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15, a1 = r1 * g.rowb;
+        store_range(load_range<NTH>(xp, xp_words, a0, a1), lds + L::hal, lds + L::flag, cntw, never4,
+                    range_words(a0, a1), g.hw);
+        fill_table(g, p_begin, min(p_end, p_begin + kG) - p_begin, tabs);
+    }
+
+    int it = 0;
+    for (int gs = p_begin; gs < p_end; gs += kG, it++) {
+        const int cnt = min(p_end, gs + kG) - gs;
+        const int cur = it & 1;
+        const Tab *tab = tabs + (it % 3) * kG;
+        int r0, r1;
+        group_rows(g, gs, gs + cnt - 1, r0, r1);
+        const int a0 = (r0 * g.rowb) & ~15;
+        __syncthreads();  // this group's input and table are in LDS; group it-1 is staged
+        const int gn = gs + kG;
+        const bool more = gn < p_end;
+        Staged<NTH> nxt;
+        int nxt_words = 0;
+        if (more) {
+            int n0, n1;
+            group_rows(g, gn, min(p_end, gn + kG) - 1, n0, n1);
+            const int b0 = (n0 * g.rowb) & ~15, b1 = n1 * g.rowb;
+            nxt = load_range<NTH>(xp, xp_words, b0, b1);
+            nxt_words = range_words(b0, b1);
+            fill_table(g, gn, min(p_end, gn + kG) - gn, tabs + ((it + 1) % 3) * kG);
+        }
+        if (it > 0)
+            write_out_lb<NTH, 32>(g, nt * 32, gs - kG, p_end, tabs + ((it + 2) % 3) * kG, stv(cur ^ 1),
+                                  stt(cur ^ 1), out_t, out_v);
+        const bool sparse = group_sparse<NW>(cntw, skip_pow, 0.15f);
+        // this wave's tiles of the group: wv, wv + NW, ...
+        const int ntiles = (cnt + PT - 1) / PT;
+        int org2[TPW];
+        uint64_t live[TPW];
+        f16v acc[TPW];
+#pragma unroll
+        for (int j = 0; j < TPW; j++) {
+            const int ti = wv + NW * j;
+            org2[j] = 2 * (tab[min(ti * PT + pl, cnt - 1)].xoff - a0 + 8 * hh);
+            live[j] = ti < ntiles ? ~0ull : 0ull;
+            if (sparse && ti < ntiles) {
+                uint64_t m = 0ull;
+                for (int k = 0; k < PT; k++) {
+                    const int xo = tab[min(ti * PT + k, cnt - 1)].xoff - a0;
+                    bool f = false;
+                    if (my_off >= 0) {
+                        const int at = xo + my_off;
+                        f = (flag[at >> 4] | flag[(at + 15) >> 4]) != 0;
+                    }
+                    m |= __builtin_amdgcn_ballot_w64(f);
+                }
+                live[j] = m;
+            }
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[j][e] = 0.0f;
+        }
+#pragma unroll
+        for (int ch = 0; ch < NCH; ch++) {
+            if (ch > 0) __syncthreads();  // every wave is done with chunk ch - 1
+            put();
+            __syncthreads();  // chunk ch is in LDS
+            fetch(ch + 1 < NCH ? ch + 1 : 0);  // the next chunk (the next group starts again at 0)
+            __builtin_amdgcn_s_setprio(2);
+#pragma unroll
+            for (int j = 0; j < TPW; j++) {
+                if (!(live[j] >> (ch * KC) & ((KC < 64 ? (1ull << KC) : 0ull) - 1ull))) continue;  // no live slice here
+                constexpr int kAhead = 2;
+                auto rdw = [&](int sl) -> u4 {
+                    return lds_read16<kMode>(hal, org2[j] + 2 * ((ch * KC + sl) / QC) * g.rowb +
+                                                      32 * ((ch * KC + sl) % QC));
+                };
+                u4 win[kAhead];
+#pragma unroll
+                for (int sl = 0; sl < kAhead && sl < KC; sl++) win[sl] = rdw(sl);
+                const uint64_t lw = live[j] >> (ch * KC);
+#pragma unroll
+                for (int sl = 0; sl < KC; sl++) {
+                    const u4 x = win[sl % kAhead];
+                    if (sl + kAhead < KC) win[sl % kAhead] = rdw(sl + kAhead);
+                    const uint32_t lb = sl < 32 ? (uint32_t)lw : (uint32_t)(lw >> 32);
+                    if ((lb >> (sl & 31)) & 1u) {
+                        h8 b[NP];
+#pragma unroll
+                        for (int k = 0; k < NP; k++) b[k] = bl[(sl * NP + k) * 64 + lane];
+                        const h8 a = frag_upto(x, cc);
+#pragma unroll
+                        for (int k = 0; k < NP; k++)
+                            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b[k], acc[j], 0, 0, 0);
+                    }
+                }
+            }
+            __builtin_amdgcn_s_setprio(0);
+        }
+        const int o = lane & 31, ns = slots_held(lgTP, hh);
+#pragma unroll
+        for (int j = 0; j < TPW; j++) {
+            const int ti = wv + NW * j;
+            if (ti >= ntiles) continue;
+            uint32_t st[2] = {0u, 0u};
+            float sv[2] = {0.0f, 0.0f};
+            tile_epilogue<TPC>(acc[j], theta, hh, st, sv);
+#pragma unroll
+            for (int k = 0; k < 2; k++) {
+                const int pi = ti * PT + slot_of(lgTP, hh, k);
+                if (k < ns && pi < cnt) {
+                    stv(cur)[o * kStageStride + pi] = sv[k];
+                    stt(cur)[o * kStageStride + pi] = (uint8_t)st[k];
+                }
+            }
+        }
+        if (more) {
+            __syncthreads();  // every wave is done with this group's input
+            store_range(nxt, lds + L::hal, lds + L::flag, cntw, never4, nxt_words, g.hw);
+        }
+    }
+    __syncthreads();  // the last group is staged
+    write_out_lb<NTH, 32>(g, nt * 32, p_begin + (it - 1) * kG, p_end, tabs + ((it - 1) % 3) * kG,
+                          stv((it - 1) & 1), stt((it - 1) & 1), out_t, out_v);
+}
+
 // Kernel instances: slice counts rounded up to these (the extra slices have
 // zero weights).  Float masters (hi/lo) keep 4*2*SK registers of B fragments,
 // halves 4*SK: both up to 144.
@@ -1386,6 +1591,25 @@ struct LbExact {
 const LbExact kLbExact[] = {
     {36, 12, 1, 3, 32, LbLayout<36, 1>::hal, &launch_lb<36, 1, 3, 12, 32, 16>},
     {10, 2, 2, 1, 16, LbLayout<10, 2>::hal, &launch_lb<10, 2, 1, 2, 16, 12>},
+};
+
+template <int SKT, int NP, int kMode, int QC, int TPC, int NW, int KC>
+void launch_lbk(dim3 grid, size_t lds, hipStream_t s, const uint8_t *xp, size_t xw, const h8 *bp,
+                const PGeom &g, float theta, int nranges, uint8_t *ot, float *ov)
+{
+    auto kern = k_fire_lbk<SKT, NP, kMode, QC, TPC, NW, KC>;
+    static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 160 * 1024) == hipSuccess;
+    (void)attr;
+    hipLaunchKernelGGL(kern, grid, dim3(64 * NW), lds, s, xp, xw, bp, g, theta, nranges, ot, ov);
+}
+
+// Layouts of the chunked LDS-fed kernel: 3x3 over 100 channels with float
+// masters and 16 steps per position (the example network's conv2), a kernel
+// row of 19 slices per chunk.
+const LbExact kLbkExact[] = {
+    {57, 19, 2, 2, 16, LbkLayout<19, 2>::hal, &launch_lbk<57, 2, 2, 19, 16, 16, 19>},
 };
 
 // Largest staged row range over the groups of every range (exact, per geometry).
@@ -1531,6 +1755,24 @@ spk_status conv_fire_pt(const uint8_t *in, int B, int T, int Ci, int Hi, int Wi,
             if (lds > 160 * 1024) break;
             const size_t xw = ((size_t)g.B * g.Hp * g.rowb + g.slack) / 16;
             e.fn(dim3(8 * ncb * ((nr + 7) / 8)), lds, s, xp, xw, bp, gl, theta, nr, out_t, out_v);
+            return check_launch("spk_conv_fire");
+        }
+    }
+    // the chunked LDS-fed kernel for the deep layouts it is made for
+    if (g.by * g.bx == 1 && !instance_sk(g.SK, half_w)) {
+        for (const LbExact &e : kLbkExact) {
+            if (e.SK != g.SK || e.QC != g.Q16 || e.NP != (half_w ? 1 : 2) || e.mode != read_mode(g.Cp) ||
+                e.TP != g.TP)
+                continue;
+            const int nr = n_ranges_lb(g, g.NT);
+            const long long rows = max_rows(g, nr);
+            if (rows * g.rowb + 64 > kRange) break;
+            PGeom gl = g;
+            gl.hw = (int)((rows * g.rowb + 64 + 47) / 16);
+            const size_t lds = e.hal + 32 * (size_t)gl.hw;
+            if (lds > 160 * 1024) break;
+            const size_t xw = ((size_t)g.B * g.Hp * g.rowb + g.slack) / 16;
+            e.fn(dim3(8 * g.NT * ((nr + 7) / 8)), lds, s, xp, xw, bp, gl, theta, nr, out_t, out_v);
             return check_launch("spk_conv_fire");
         }
     }

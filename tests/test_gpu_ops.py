@@ -200,6 +200,8 @@ CONV_CASES = [
     (2, 64, 9, 13, 40, 3, 1, 1, 20, 12.0, 0.1, "f16"),      # LDS-fed kernel: 40 maps, T = 20, ragged
     (2, 6, 20, 22, 70, 5, 1, 2, 15, 16.0, 0.3, "f32"),      # LDS-fed kernel, 5x5 over 6 channels, float
                                                             # masters: three column tiles
+    (2, 100, 14, 14, 200, 3, 1, 1, 15, 5.0, 0.3, "f32"),    # chunked LDS-fed kernel: 3x3 over 100
+                                                            # channels, one kernel row of slices per chunk
 ]
 
 
