@@ -69,7 +69,7 @@ __global__ void k_rate_max(const float *__restrict__ x, int64_t n, float min_val
 // frames[b][t][i] = u[b][t][i] < x[b][i] / max_b (0 for x <= min_value).
 // Thread: 4 consecutive values (kVec: n a multiple of 4, 16-byte vectors) or
 // one, for kRateTT consecutive steps starting at blockIdx.y * kRateTT.
-constexpr int kRateTT = 10;
+constexpr int kRateTT = 3;  // (10 held 40 draws per thread and ran at half the rate)
 
 template <bool kVec>
 __global__ void k_rate_frames(const float *__restrict__ x, const float *__restrict__ u, int64_t n,
@@ -667,7 +667,7 @@ __global__ __launch_bounds__(kThreads) void k_rate_conv(const uint16_t *__restri
 // One thread per output neuron and chunk of kPoolTT steps (blockIdx.y): the
 // window's neuron with the most spikes (first in row-major order among
 // equals) passes its train on; chunk 0 also writes the count.
-constexpr int kPoolTT = 32;
+constexpr int kPoolTT = 64;
 
 __global__ void k_rate_pool(const uint8_t *__restrict__ in, const int32_t *__restrict__ cin, int B,
                             int T, int C, int Hi, int Wi, int Kh, int Kw, int stride, int pad, int Ho,
